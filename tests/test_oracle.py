@@ -1,0 +1,374 @@
+"""Pins for the CPU oracle: each check is fixed by the paper or by mathematics,
+not by re-typing the oracle's own formula.
+
+Sources of truth used here:
+* closed forms (cyclic supports of Sec. 4.5 Eq. 12, constant and ramp planes,
+  the gate at zero input, the tau limits of Sec. 3.3);
+* invariants (convexity of Sec. 3.3, coverage of Sec. 3.4, the temperature
+  reparameterisation of Sec. 3.3);
+* library routines on tiny inputs (Python ``sorted``, numpy ``mean``/``einsum``,
+  ``numpy.logaddexp``, ``scipy.special.softmax``, ``torch.nn`` layers in
+  float64) standing in for the textbook definitions.
+"""
+import math
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle
+from paper_2608_23794_amd import inputs
+
+pytestmark = pytest.mark.usefixtures("oracle_lib")
+
+
+def rand_support(rng, C, R, k):
+    s = np.array([rng.choice(C, size=k, replace=False) for _ in range(R)], np.int32).reshape(R, k)
+    w = rng.standard_normal((R, k)).astype(np.float32)
+    return s, w
+
+
+# --------------------------------------------------------------------------
+# Support preparation (Sec. 3.2 Eq. 2, Sec. 3.3 gate input order, Sec. 3.4 U)
+
+@pytest.mark.parametrize("C,E,k", [(64, 16, 8), (64, 5, 8), (64, 9, 8), (100, 7, 13), (32, 32, 32),
+                                   (17, 3, 5), (64, 1, 4), (2048, 512, 128)])
+def test_cyclic_supports_closed_form_U(C, E, k):
+    # Eq. 12 (0-based): expert e reads channels (e*k + j) mod C, j < k.
+    R = E - 1
+    s = np.array([[(e * k + j) % C for j in range(k)] for e in range(R)], np.int32).reshape(R, k)
+    w = np.zeros((R, k), np.float32)
+    _, _, covered, U, nU = oracle.prepare(C, E, s, w)
+    expected = [] if R * k >= C else list(range(R * k, C))
+    assert U.tolist() == expected
+    assert nU == len(expected)
+    assert covered.tolist() == [0 if c in set(expected) else 1 for c in range(C)]
+
+
+def test_prepare_brute_force_tiny():
+    rng = np.random.default_rng(11)
+    for trial in range(50):
+        C = int(rng.integers(2, 40))
+        E = int(rng.integers(1, C + 1))
+        k = int(rng.integers(1, C + 1))
+        s, w = rand_support(rng, C, E - 1, k)
+        if trial % 3 == 0:  # force ties in the logits
+            w = np.round(w).astype(np.float32)
+        s_c, w_c, covered, U, nU = oracle.prepare(C, E, s, w)
+        union = set(int(v) for v in s.ravel())
+        assert U.tolist() == sorted(set(range(C)) - union)
+        assert nU == C - len(union)
+        assert covered.tolist() == [int(c in union) for c in range(C)]
+        for o in range(E - 1):
+            ref = sorted(zip(w[o].tolist(), s[o].tolist()), key=lambda t: (-t[0], t[1]))
+            assert list(zip(w_c[o].tolist(), s_c[o].tolist())) == ref
+            assert not (set(U.tolist()) & set(s[o].tolist()))
+
+
+def test_prepare_tie_order_explicit():
+    s = np.array([[5, 9, 3, 0]], np.int32)
+    w = np.array([[1.0, 2.0, 2.0, 1.0]], np.float32)
+    s_c, w_c, _, U, nU = oracle.prepare(10, 2, s, w)
+    assert s_c.tolist() == [[3, 9, 0, 5]]
+    assert w_c.tolist() == [[2.0, 2.0, 1.0, 1.0]]
+    assert U.tolist() == [1, 2, 4, 6, 7, 8] and nU == 6
+
+
+def test_prepare_signed_zero_is_a_tie():
+    s = np.array([[4, 1]], np.int32)
+    w = np.array([[0.0, -0.0]], np.float32)
+    s_c, _, _, _, _ = oracle.prepare(6, 2, s, w)
+    assert s_c.tolist() == [[1, 4]]
+
+
+@pytest.mark.parametrize("bad", ["dup", "neg", "range", "nan", "inf"])
+def test_prepare_rejects_invalid_rows(bad):
+    rng = np.random.default_rng(3)
+    s, w = rand_support(rng, 50, 6, 5)
+    o = 3
+    if bad == "dup":
+        s[o, 4] = s[o, 1]
+    elif bad == "neg":
+        s[o, 2] = -1
+    elif bad == "range":
+        s[o, 0] = 50
+    elif bad == "nan":
+        w[o, 3] = np.nan
+    elif bad == "inf":
+        w[o, 3] = -np.inf
+    s[5, 0] = s[5, 1]  # a later bad row must not be reported first
+    with pytest.raises(oracle.SupportError) as ei:
+        oracle.prepare(50, 7, s, w)
+    assert ei.value.expert == o
+
+
+@pytest.mark.parametrize("C,E,k", [(8, 9, 2), (8, 0, 2), (8, 3, 0), (8, 3, 9)])
+def test_prepare_rejects_bad_shapes(C, E, k):
+    R = max(E - 1, 0)
+    with pytest.raises(ValueError):
+        oracle.prepare(C, E, np.zeros((R, k), np.int32), np.zeros((R, k), np.float32))
+
+
+# --------------------------------------------------------------------------
+# Global average pooling (Sec. 3.3)
+
+@pytest.mark.parametrize("layout", [oracle.NCHW, oracle.NHWC])
+def test_pool_constant_and_ramp_planes(layout):
+    B, C, H, W = 3, 5, 7, 9
+    HW = H * W
+    const = np.arange(1, B * C + 1, dtype=np.float32).reshape(B, C, 1, 1) * np.float32(0.375)
+    x = np.broadcast_to(const, (B, C, H, W)).astype(np.float32)
+    ramp = np.broadcast_to(np.arange(HW, dtype=np.float32).reshape(1, 1, H, W), (B, C, H, W))
+    if layout == oracle.NHWC:
+        x = np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+        ramp = np.ascontiguousarray(ramp.transpose(0, 2, 3, 1))
+    assert np.array_equal(oracle.pool(x, layout), const.reshape(B, C).astype(np.float64))
+    assert np.all(oracle.pool(np.ascontiguousarray(ramp), layout) == (HW - 1) / 2)
+
+
+def test_pool_bf16_bit_patterns():
+    # 0x3F80 = 1.0, 0xC020 = -2.5, 0x4049 = 3.140625, 0x0000 = 0
+    vals = {0x3F80: 1.0, 0xC020: -2.5, 0x4049: 3.140625, 0x0000: 0.0}
+    pats = np.array(list(vals.keys()), np.uint16)
+    x = np.tile(pats, 3).reshape(1, 1, 3, 4)
+    assert oracle.pool(x, oracle.NCHW)[0, 0] == pytest.approx(sum(vals.values()) / 4, abs=0)
+
+
+def test_pool_matches_numpy_mean_both_layouts():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((4, 6, 5, 3)).astype(np.float32)
+    ref = x.astype(np.float64).mean(axis=(2, 3))
+    np.testing.assert_allclose(oracle.pool(x, oracle.NCHW), ref, rtol=1e-14, atol=1e-15)
+    xl = np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+    np.testing.assert_allclose(oracle.pool(xl, oracle.NHWC), ref, rtol=1e-14, atol=1e-15)
+
+
+# --------------------------------------------------------------------------
+# Temperature gates (Sec. 3.3)
+
+def _canon(C, E, k, seed):
+    rng = np.random.default_rng(seed)
+    s, w = rand_support(rng, C, E - 1, k)
+    s_c, w_c, _, U, nU = oracle.prepare(C, E, s, w)
+    return rng, s, w, s_c, w_c, U
+
+
+def test_softplus_gate_zero_slopes_is_log2():
+    _, _, _, s_c, _, _ = _canon(20, 6, 4, 1)
+    d = np.random.default_rng(2).random((3, 20))
+    tau = oracle.gate_softplus(d, s_c, np.zeros((5, 4), np.float32), np.zeros(5, np.float32))
+    assert np.all(np.abs(tau - 0.6941471805599453) < 1e-15)
+
+
+def test_softplus_gate_offsets_match_logaddexp():
+    _, _, _, s_c, _, _ = _canon(20, 6, 4, 1)
+    c = np.array([-50.0, -3.0, 0.25, 4.0, 50.0], np.float32)
+    d = np.random.default_rng(2).random((2, 20))
+    tau = oracle.gate_softplus(d, s_c, np.zeros((5, 4), np.float32), c)
+    ref = np.logaddexp(0.0, c.astype(np.float64)) + 1e-3
+    np.testing.assert_allclose(tau, np.broadcast_to(ref, tau.shape), rtol=1e-15)
+    assert abs(tau[0, 0] - 1e-3) < 1e-18  # softplus(-50) = 2e-22 sits below one ulp of 1e-3
+
+
+def test_softplus_gate_constant_descriptor():
+    rng, _, _, s_c, _, _ = _canon(30, 8, 6, 4)
+    a = rng.standard_normal((7, 6)).astype(np.float32)
+    c = rng.standard_normal(7).astype(np.float32)
+    kappa = 0.8125
+    d = np.full((2, 30), kappa)
+    tau = oracle.gate_softplus(d, s_c, a, c)
+    g = c.astype(np.float64) + kappa * a.astype(np.float64).sum(1)
+    np.testing.assert_allclose(tau, np.broadcast_to(np.logaddexp(0, g) + 1e-3, tau.shape), rtol=1e-14)
+
+
+def test_softplus_gate_reads_support_in_canonical_order():
+    # a one-hot slope at position i reads the descriptor of the i-th most
+    # preferred channel of that expert, for that image
+    rng, s, w, s_c, w_c, _ = _canon(30, 5, 6, 9)
+    d = rng.random((3, 30))
+    for i in (0, 2, 5):
+        a = np.zeros((4, 6), np.float32)
+        a[:, i] = 1.0
+        tau = oracle.gate_softplus(d, s_c, a, np.zeros(4, np.float32))
+        for b in range(3):
+            for o in range(4):
+                order = sorted(range(6), key=lambda j: (-w[o, j], s[o, j]))
+                ch = s[o, order[i]]
+                assert tau[b, o] == pytest.approx(np.logaddexp(0, d[b, ch]) + 1e-3, rel=1e-15)
+
+
+def test_mlp_gate_zero_params_midpoint_and_bounds():
+    rng, _, _, s_c, _, _ = _canon(24, 6, 5, 3)
+    d = rng.random((2, 24))
+    z = np.zeros
+    tau = oracle.gate_mlp(d, s_c, z((5, 5), np.float32), z(5, np.float32), z(5, np.float32), 0.0, 0.2, 6.0)
+    lo32 = float(np.float32(0.2))  # the bounds are float32 parameters
+    assert np.all(np.abs(tau - (lo32 + 6.0) / 2) < 1e-15)
+    hi = oracle.gate_mlp(d, s_c, z((5, 5), np.float32), z(5, np.float32), z(5, np.float32), 100.0, 0.2, 6.0)
+    lo = oracle.gate_mlp(d, s_c, z((5, 5), np.float32), z(5, np.float32), z(5, np.float32), -100.0, 0.2, 6.0)
+    assert np.all(np.abs(hi - 6.0) < 1e-12) and np.all(np.abs(lo - lo32) < 1e-12)
+
+
+def test_mlp_gate_matches_torch_layers():
+    C, E, k = 40, 9, 6
+    rng, s, w, s_c, w_c, _ = _canon(C, E, k, 21)
+    d = rng.standard_normal((3, C))
+    W1 = rng.standard_normal((k, k)).astype(np.float32)
+    b1 = rng.standard_normal(k).astype(np.float32)
+    w2 = rng.standard_normal(k).astype(np.float32)
+    b2 = np.float32(0.3)
+    tau = oracle.gate_mlp(d, s_c, W1, b1, w2, b2, 0.2, 6.0)
+    net = torch.nn.Sequential(torch.nn.Linear(k, k), torch.nn.ReLU(), torch.nn.Linear(k, 1)).double()
+    with torch.no_grad():
+        net[0].weight.copy_(torch.from_numpy(W1.astype(np.float64)))
+        net[0].bias.copy_(torch.from_numpy(b1.astype(np.float64)))
+        net[2].weight.copy_(torch.from_numpy(w2.astype(np.float64)).reshape(1, k))
+        net[2].bias.fill_(float(b2))
+        for b in range(3):
+            for o in range(E - 1):
+                order = sorted(range(k), key=lambda j: (-w[o, j], s[o, j]))
+                z = torch.tensor([d[b, s[o, j]] for j in order], dtype=torch.float64)
+                lo32 = float(np.float32(0.2))
+                ref = lo32 + (6.0 - lo32) * torch.sigmoid(net(z)).item()
+                assert tau[b, o] == pytest.approx(ref, rel=1e-13)
+
+
+# --------------------------------------------------------------------------
+# Mixing coefficients, Eq. 4
+
+def test_softmax_matches_scipy():
+    rng = np.random.default_rng(8)
+    w = np.sort(rng.standard_normal((6, 9)).astype(np.float32), axis=1)[:, ::-1].copy()
+    tau = rng.uniform(0.05, 4.0, (3, 6))
+    al = oracle.softmax(w, tau)
+    ref = scipy.special.softmax(w[None].astype(np.float64) / tau[:, :, None], axis=2)
+    np.testing.assert_allclose(al, ref, rtol=1e-13, atol=1e-300)
+
+
+def test_softmax_convex_and_order_preserving():
+    rng = np.random.default_rng(9)
+    w = np.sort(rng.standard_normal((20, 16)).astype(np.float32), axis=1)[:, ::-1].copy()
+    tau = np.exp(rng.uniform(-5, 5, (4, 20)))
+    al = oracle.softmax(w, tau)
+    assert np.all(al >= 0)
+    np.testing.assert_allclose(al.sum(-1), 1.0, rtol=0, atol=1e-14)
+    assert np.all(np.diff(al, axis=-1) <= 0)
+
+
+def test_softmax_equal_logits_exactly_uniform_and_k1():
+    for k in (1, 2, 4, 8, 64):
+        w = np.full((3, k), 0.7, np.float32)
+        al = oracle.softmax(w, np.array([[1e-3, 1.0, 1e6]]))
+        assert np.all(al == 1.0 / k)
+
+
+def test_softmax_temperature_limits():
+    rng = np.random.default_rng(10)
+    w = np.sort(rng.standard_normal((50, 12)).astype(np.float32), axis=1)[:, ::-1].copy()
+    w[:, 1:] = np.minimum(w[:, 1:], w[:, :1] - np.float32(0.1001))  # top-2 gap > 0.1 after float32 rounding
+    big = oracle.softmax(w, np.full((1, 50), 1e6))
+    spread = (w.max(1) - w.min(1)).astype(np.float64)
+    assert np.all(np.abs(big[0] - 1 / 12) <= spread[:, None] / 1e6)
+    small = oracle.softmax(w, np.full((1, 50), 1e-3))
+    assert np.all(np.abs(small[0, :, 0] - 1.0) <= 11 * math.exp(-100))
+    assert np.all(small[0, :, 1:] <= math.exp(-100))
+
+
+def test_softmax_reparameterisation_invariance():
+    rng = np.random.default_rng(12)
+    w = rng.standard_normal((7, 5)).astype(np.float32)
+    tau = rng.uniform(0.3, 3, (2, 7))
+    lam = 4.0  # exact scaling of float32 logits
+    a1 = oracle.softmax(w, tau)
+    a2 = oracle.softmax((w * lam).astype(np.float32), tau * lam)
+    np.testing.assert_allclose(a1, a2, rtol=1e-14)
+
+
+# --------------------------------------------------------------------------
+# Routed experts (Eq. 5) and residual (Eq. 6)
+
+def dense_equivalent(s_c, alpha, U, C, E):
+    """W_eff[b, o, c]: the dense projection that the layer equals per image."""
+    B, R, k = alpha.shape
+    W = np.zeros((B, E, C))
+    for b in range(B):
+        for o in range(R):
+            for i in range(k):
+                W[b, o, s_c[o, i]] += alpha[b, o, i]
+        if len(U):
+            W[b, E - 1, U] = 1.0 / len(U)
+    return W
+
+
+@pytest.mark.parametrize("layout", [oracle.NCHW, oracle.NHWC])
+@pytest.mark.parametrize("C,E,k,nU_zero", [(24, 6, 3, False), (16, 16, 4, True), (20, 1, 3, False)])
+def test_mix_equals_dense_equivalent_matmul(layout, C, E, k, nU_zero):
+    rng = np.random.default_rng(C * 100 + E)
+    B, H, W = 3, 4, 5
+    x = rng.standard_normal((B, C, H, W)).astype(np.float32)
+    if nU_zero:
+        s = np.array([[(e * k + j) % C for j in range(k)] for e in range(E - 1)], np.int32)
+        w = rng.standard_normal((E - 1, k)).astype(np.float32)
+    else:
+        s, w = rand_support(rng, C, E - 1, k)
+        s = s.reshape(E - 1, k)
+        w = w.reshape(E - 1, k)
+    s_c, w_c, _, U, nU = oracle.prepare(C, E, s, w)
+    if nU_zero:
+        assert nU == 0
+    tau = rng.uniform(0.2, 3.0, (B, E - 1))
+    al = oracle.softmax(w_c, tau)
+    Weff = dense_equivalent(s_c, al, U, C, E)
+    if E > 1:
+        np.testing.assert_allclose(Weff[:, :E - 1].sum(-1), 1.0, atol=1e-14)
+    ref = np.einsum("boc,bchw->bohw", Weff, x.astype(np.float64))
+    xin = x if layout == oracle.NCHW else np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+    y, mag = oracle.mix(xin, s_c, al, U, E, layout)
+    if layout == oracle.NHWC:
+        y = y.transpose(0, 3, 1, 2)
+        mag = mag.transpose(0, 3, 1, 2)
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+    assert np.all(mag >= np.abs(y) - 1e-12)
+    if nU == 0:
+        assert np.all(y[:, E - 1] == 0.0)
+    if E == 1:
+        np.testing.assert_allclose(y[:, 0], x.astype(np.float64).mean(axis=1), rtol=1e-12, atol=1e-14)
+
+
+def test_mix_k1_and_one_hot_are_exact_copies():
+    rng = np.random.default_rng(13)
+    B, C, E, HW = 2, 12, 7, 10
+    x = inputs.f32_to_bf16_bits(rng.standard_normal((B, C, HW)).astype(np.float32))
+    s, w = rand_support(rng, C, E - 1, 1)
+    s_c, w_c, _, U, _ = oracle.prepare(C, E, s, w)
+    al = oracle.softmax(w_c, rng.uniform(0.1, 2, (B, E - 1)))
+    y, _ = oracle.mix(x, s_c, al, U, E, oracle.NCHW)
+    xf = inputs.bf16_bits_to_f32(x).astype(np.float64)
+    for o in range(E - 1):
+        assert np.array_equal(y[:, o], xf[:, s_c[o, 0]])
+    # tau at its floor with a clear top logit: weight on the top channel only
+    s, w = rand_support(rng, C, E - 1, 4)
+    w[:, 0] = w.max(1) + 1.0
+    s_c, w_c, _, U, _ = oracle.prepare(C, E, s, w)
+    al = oracle.softmax(w_c, np.full((B, E - 1), 1e-3))
+    y, _ = oracle.mix(x, s_c, al, U, E, oracle.NCHW)
+    for o in range(E - 1):
+        assert np.array_equal(y[:, o], xf[:, s_c[o, 0]])
+
+
+def test_forward_coverage_every_channel_reaches_an_output():
+    wl = inputs.WORKLOADS["tiny"]
+    g = inputs.generate(wl)
+    r = oracle.forward(g["x"], g["s"], g["w"], wl.E, oracle.NCHW, a=g["a"], c=g["c"])
+    union = set(r["s"].ravel().tolist())
+    assert union | set(r["U"].tolist()) == set(range(wl.C))
+    assert not (union & set(r["U"].tolist()))
+    # perturbing any single channel changes some output (every channel contributes)
+    x = g["x"].copy()
+    base = r["y"]
+    for c in range(wl.C):
+        x2 = x.copy()
+        x2[:, c] += 1.0
+        y2 = oracle.mix(x2, r["s"], r["alpha"], r["U"], wl.E, oracle.NCHW)[0]
+        assert np.abs(y2 - base).max() > 1e-6
