@@ -1,0 +1,165 @@
+/*
+ * moce.h -- C ABI of the MI355X (gfx950) Mixture of Channel Experts forward
+ * pass (arxiv 2608.23794, "Mixture of Channel Experts: Static Sparse Supports
+ * with Input-Adaptive Mixing for Pointwise Projections").
+ *
+ * A MoCE layer replaces a pointwise projection from C input channels to E <= C
+ * outputs (Sec. 3.1): E-1 routed experts, each a convex mixture of k input
+ * channels on a static support (Sec. 3.2-3.3), plus one residual output that
+ * averages the channels outside every support (Sec. 3.4, Eq. 6).
+ *
+ * Conventions shared by every entry point
+ *  - The descriptor and gate structs are host memory; every array argument is
+ *    a device pointer (hipMalloc'd or otherwise device-accessible) unless its
+ *    name ends in _host.  The caller owns all memory.  The library never
+ *    allocates device memory and keeps no pointer after a call returns.
+ *  - Every call except moce_support_prepare is asynchronous on `stream`
+ *    (0 = the null stream) and returns as soon as its kernels are enqueued.
+ *  - Layouts: MOCE_NCHW is x[B][C][H][W] and y[B][E][H][W]; MOCE_NHWC is
+ *    x[B][H][W][C] and y[B][H][W][E].  Token inputs x[B][N][C] are MOCE_NHWC
+ *    with H = N, W = 1.  y always has the layout and element type of x.
+ *  - Element types: x and y are both MOCE_F32 or both MOCE_BF16 (bfloat16 bit
+ *    patterns, 2 bytes).  Accumulation is float32 throughout; bf16 outputs are
+ *    rounded to nearest, ties to even.  d, tau, alpha and all parameters are
+ *    float32; supports are int32 channel indices.
+ *  - Output channel E-1 is the residual expert; channels 0..E-2 are the routed
+ *    experts in support-row order.
+ *  - x and y must be 16-byte aligned.
+ *  - Errors are negative moce_status codes.  Every error detectable on the host
+ *    is reported before anything is enqueued, and then no output is written.
+ *    A failed kernel launch returns MOCE_ERR_DEVICE.  The library holds no
+ *    mutable global state; calls on different streams are independent as long
+ *    as their output buffers do not overlap.
+ */
+#ifndef MOCE_H
+#define MOCE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum moce_status {
+    MOCE_OK = 0,
+    MOCE_ERR_NULL = -1,        /* a required pointer is NULL */
+    MOCE_ERR_SHAPE = -2,       /* B, C, H, W < 1; E outside [1, C]; k outside [1, C] */
+    MOCE_ERR_DTYPE = -3,       /* unknown element type or x/y types differ */
+    MOCE_ERR_LAYOUT = -4,      /* unknown layout code */
+    MOCE_ERR_SUPPORT = -5,     /* a support row is invalid (moce_support_prepare) */
+    MOCE_ERR_GATE = -6,        /* unknown gate kind, or tau_min/tau_max invalid */
+    MOCE_ERR_WORKSPACE = -7,   /* workspace NULL or smaller than required */
+    MOCE_ERR_ALIGN = -8,       /* x or y not 16-byte aligned */
+    MOCE_ERR_DEVICE = -9,      /* a HIP call or kernel launch failed */
+    MOCE_ERR_UNSUPPORTED = -10 /* the shape exceeds a documented size limit */
+} moce_status;
+
+enum { MOCE_F32 = 0, MOCE_BF16 = 1 };
+enum { MOCE_NCHW = 0, MOCE_NHWC = 1 };
+
+/* Gate kinds.  Both read the k descriptors of an expert's support in
+ * canonical order (descending routing logit), so gate position i is the
+ * expert's i-th most preferred channel (Sec. 3.3).
+ *  MOCE_GATE_SOFTPLUS_LINEAR: tau[b][o] = softplus(c[o] + sum_i a[o][i] d[b][s[o][i]]) + 1e-3,
+ *     a per-expert linear gate (a: [E-1][k], c: [E-1]).
+ *  MOCE_GATE_MLP_SIGMOID: the paper's gate (Sec. 3.3 Eq. 3): one two-layer MLP
+ *     of hidden width k shared by all experts of the layer,
+ *     h = ReLU(W1 z + b1), g = w2 . h + b2,
+ *     tau = tau_min + (tau_max - tau_min) sigmoid(g)
+ *     (W1: [k][k] row-major, row j feeds hidden unit j; b1, w2: [k]). */
+enum { MOCE_GATE_SOFTPLUS_LINEAR = 0, MOCE_GATE_MLP_SIGMOID = 1 };
+
+typedef struct moce_desc {
+    int64_t B, C, H, W;   /* x is B images of C channels over H*W positions */
+    int32_t E;            /* outputs: E-1 routed experts + 1 residual, 1 <= E <= C */
+    int32_t k;            /* support size, 1 <= k <= C */
+    int32_t x_dtype;      /* MOCE_F32 or MOCE_BF16 */
+    int32_t y_dtype;      /* must equal x_dtype */
+    int32_t layout;       /* MOCE_NCHW or MOCE_NHWC */
+    int32_t reserved;     /* set to 0 */
+} moce_desc;
+
+typedef struct moce_gate_params {
+    int32_t kind;         /* MOCE_GATE_* */
+    int32_t reserved;     /* set to 0 */
+    const float* a;       /* softplus-linear: [E-1][k] slopes, canonical positions */
+    const float* c;       /* softplus-linear: [E-1] offsets */
+    const float* W1;      /* MLP: [k][k] */
+    const float* b1;      /* MLP: [k] */
+    const float* w2;      /* MLP: [k] */
+    float b2;             /* MLP: output bias */
+    float tau_min;        /* MLP: lower temperature bound, > 0 */
+    float tau_max;        /* MLP: upper temperature bound, >= tau_min */
+} moce_gate_params;
+
+/* Static support preparation (Sec. 3.2 Eq. 2: supports fixed at inference;
+ * Sec. 3.3: gate input order; Sec. 3.4: the uncovered set U).
+ *
+ * In:  s[E-1][k] int32 channel indices and w[E-1][k] float32 selected routing
+ *      logits, one row per routed expert, in any order.
+ * Out: s_out, w_out [E-1][k]: each row sorted by logit descending, equal
+ *      logits by ascending channel (the canonical order every other entry
+ *      point expects); covered[C] uint8: 1 if the channel is in some support;
+ *      U[C] int32: the uncovered channels ascending in U[0..nU-1] (the rest
+ *      is left unspecified); info[2] int32 device scratch receiving
+ *      {nU, first bad expert or -1}; *nU_host and *bad_expert_host receive the
+ *      same two values.
+ * A row is invalid if a channel lies outside [0, C), repeats within the row,
+ * or its logit is not finite; the call then returns MOCE_ERR_SUPPORT with
+ * *bad_expert_host = the lowest invalid expert (outputs other than info and
+ * the two host values are unspecified).  s_out/w_out may not alias s/w.
+ * This call synchronises `stream` once (it is a once-per-model step).
+ * Limits: C <= 2^24, k <= 4096. */
+moce_status moce_support_prepare(const moce_desc* desc, const int32_t* s, const float* w,
+                                 int32_t* s_out, float* w_out, uint8_t* covered, int32_t* U,
+                                 int32_t* info, int32_t* nU_host, int32_t* bad_expert_host,
+                                 hipStream_t stream);
+
+/* Global average pooling descriptor z = GAP(x) (Sec. 3.3):
+ * d[b][c] = (1 / (H W)) sum over positions of x[b][c][.]; d is [B][C] float32. */
+moce_status moce_pool(const moce_desc* desc, const void* x, float* d, hipStream_t stream);
+
+/* Temperatures (Sec. 3.3, Eq. 3 or the softplus-linear form) and mixing
+ * coefficients (Eq. 4): tau[b][o] and, if alpha != NULL,
+ * alpha[b][o][i] = exp(w[o][i] / tau[b][o]) / sum_j exp(w[o][j] / tau[b][o]).
+ * d is [B][C]; s, w are prepared rows; tau is [B][E-1]; alpha is [B][E-1][k].
+ * Does nothing when E == 1.  Limits for MOCE_GATE_MLP_SIGMOID: k <= 256. */
+moce_status moce_gate(const moce_desc* desc, const float* d, const int32_t* s, const float* w,
+                      const moce_gate_params* gate, float* tau, float* alpha, hipStream_t stream);
+
+/* Routed outputs (Sec. 3.3 Eq. 5) and residual output (Sec. 3.4 Eq. 6):
+ * y[b][o][p] = sum_i alpha[b][o][i] x[b][s[o][i]][p] for o < E-1, and
+ * y[b][E-1][p] = (1/nU) sum_{c in U} x[b][c][p], or 0 when nU == 0.
+ * s: prepared [E-1][k]; alpha: [B][E-1][k]; U: [nU] uncovered channels with
+ * 0 <= nU <= C (U may be NULL when nU == 0).  y is fully overwritten. */
+moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, const float* alpha,
+                     const int32_t* U, int32_t nU, void* y, hipStream_t stream);
+
+/* Bytes of device workspace moce_forward needs for `desc` (0 on an invalid
+ * descriptor).  The workspace holds the descriptor d and the temperatures. */
+size_t moce_forward_workspace_bytes(const moce_desc* desc);
+
+/* The whole layer (Secs. 3.3-3.4): pooling, temperatures, mixing
+ * coefficients, routed experts and residual, equal to moce_pool + moce_gate +
+ * moce_mix.  s, w: prepared rows; U, nU: as returned by moce_support_prepare;
+ * ws: device workspace of at least moce_forward_workspace_bytes(desc) bytes,
+ * 256-byte aligned, owned by the caller; its contents on entry are ignored and
+ * on return unspecified.  Concurrent calls must use distinct workspaces. */
+moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
+                         const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
+                         void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Static string naming a status code. */
+const char* moce_status_str(int status);
+
+/* ABI version of this header: 1. */
+int moce_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOCE_H */

@@ -1,0 +1,218 @@
+// C ABI of libmoce: host-side validation, workspace layout and dispatch to
+// the kernels of prepare.hip, pool.hip, gate.hip and mix.hip.  Every check that
+// can fail on the host runs before anything is enqueued.
+#include <climits>
+#include <cmath>
+#include <cstring>
+
+#include "moce_internal.h"
+
+using moce::Shape;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+moce_status check_desc(const moce_desc* d, Shape* sh) {
+  if (!d) return MOCE_ERR_NULL;
+  if (d->B < 1 || d->C < 1 || d->H < 1 || d->W < 1) return MOCE_ERR_SHAPE;
+  if (d->E < 1 || (int64_t)d->E > d->C || d->k < 1 || (int64_t)d->k > d->C) return MOCE_ERR_SHAPE;
+  if (d->x_dtype != MOCE_F32 && d->x_dtype != MOCE_BF16) return MOCE_ERR_DTYPE;
+  if (d->y_dtype != d->x_dtype) return MOCE_ERR_DTYPE;
+  if (d->layout != MOCE_NCHW && d->layout != MOCE_NHWC) return MOCE_ERR_LAYOUT;
+  // index arithmetic: positions, channels and per-image element counts fit int32
+  if (d->H > INT_MAX || d->W > INT_MAX || d->C > INT_MAX) return MOCE_ERR_UNSUPPORTED;
+  const int64_t HW = d->H * d->W;
+  if (d->H > INT_MAX / d->W) return MOCE_ERR_UNSUPPORTED;
+  if (d->C > (int64_t)INT_MAX / HW) return MOCE_ERR_UNSUPPORTED;
+  if (d->B > ((int64_t)1 << 40) / (d->C * HW)) return MOCE_ERR_UNSUPPORTED;
+  if ((int64_t)d->E * d->k > INT_MAX) return MOCE_ERR_UNSUPPORTED;
+  sh->B = d->B;
+  sh->C = d->C;
+  sh->HW = HW;
+  sh->E = d->E;
+  sh->R = d->E - 1;
+  sh->k = d->k;
+  sh->elem = d->x_dtype;
+  sh->layout = d->layout;
+  return MOCE_OK;
+}
+
+moce_status check_gate(const Shape& sh, const moce_gate_params* g) {
+  if (!g) return MOCE_ERR_NULL;
+  if (g->kind == MOCE_GATE_SOFTPLUS_LINEAR) {
+    if (sh.R > 0 && (!g->a || !g->c)) return MOCE_ERR_NULL;
+    return MOCE_OK;
+  }
+  if (g->kind == MOCE_GATE_MLP_SIGMOID) {
+    if (sh.R > 0 && (!g->W1 || !g->b1 || !g->w2)) return MOCE_ERR_NULL;
+    if (!std::isfinite(g->tau_min) || !std::isfinite(g->tau_max) || !std::isfinite(g->b2) ||
+        g->tau_min <= 0.f || g->tau_max < g->tau_min)
+      return MOCE_ERR_GATE;
+    if (sh.k > 256) return MOCE_ERR_UNSUPPORTED;
+    return MOCE_OK;
+  }
+  return MOCE_ERR_GATE;
+}
+
+moce_status device_status(hipError_t e) { return e == hipSuccess ? MOCE_OK : MOCE_ERR_DEVICE; }
+
+size_t elem_bytes(const Shape& sh) { return sh.elem == MOCE_F32 ? 4 : 2; }
+
+// Forward workspace: d [B][C], tau [B][R], lse [B][R], counters
+// (per-image pool counts [B], 8 queue tickets, an error word), the fused
+// kernel's support plan, and for NCHW the coefficients alpha [B][R][k] of the
+// staged path; every region starts on a 256-byte boundary.
+struct WsLayout {
+  size_t d, tau, lse, counters, plan, alpha, total;
+};
+WsLayout ws_layout(const Shape& sh) {
+  WsLayout l{};
+  size_t off = 0;
+  l.d = off;
+  off += round_up((size_t)sh.B * sh.C * sizeof(float));
+  l.tau = off;
+  off += round_up((size_t)sh.B * sh.R * sizeof(float));
+  l.lse = off;
+  off += round_up((size_t)sh.B * sh.R * sizeof(float));
+  l.counters = off;
+  off += round_up((size_t)(sh.B + 8 + 1) * sizeof(int));
+  l.plan = off;
+  if (moce::fused_eligible(sh)) off += round_up(moce::fused_plan_bytes(sh));
+  l.alpha = off;
+  if (sh.layout == MOCE_NCHW) off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
+  l.total = off;
+  return l;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moce_abi_version(void) { return 1; }
+
+const char* moce_status_str(int status) {
+  switch (status) {
+    case MOCE_OK: return "MOCE_OK";
+    case MOCE_ERR_NULL: return "MOCE_ERR_NULL: a required pointer is NULL";
+    case MOCE_ERR_SHAPE: return "MOCE_ERR_SHAPE: invalid B, C, H, W, E or k";
+    case MOCE_ERR_DTYPE: return "MOCE_ERR_DTYPE: unknown or mismatched element type";
+    case MOCE_ERR_LAYOUT: return "MOCE_ERR_LAYOUT: unknown layout";
+    case MOCE_ERR_SUPPORT: return "MOCE_ERR_SUPPORT: invalid support row";
+    case MOCE_ERR_GATE: return "MOCE_ERR_GATE: invalid gate kind or parameters";
+    case MOCE_ERR_WORKSPACE: return "MOCE_ERR_WORKSPACE: workspace missing or too small";
+    case MOCE_ERR_ALIGN: return "MOCE_ERR_ALIGN: pointer not aligned";
+    case MOCE_ERR_DEVICE: return "MOCE_ERR_DEVICE: HIP call or kernel launch failed";
+    case MOCE_ERR_UNSUPPORTED: return "MOCE_ERR_UNSUPPORTED: shape exceeds a size limit";
+    default: return "unknown moce_status";
+  }
+}
+
+moce_status moce_support_prepare(const moce_desc* desc, const int32_t* s, const float* w,
+                                 int32_t* s_out, float* w_out, uint8_t* covered, int32_t* U,
+                                 int32_t* info, int32_t* nU_host, int32_t* bad_expert_host,
+                                 hipStream_t stream) {
+  Shape sh;
+  moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  if (!covered || !U || !info || !nU_host || !bad_expert_host) return MOCE_ERR_NULL;
+  if (sh.R > 0 && (!s || !w || !s_out || !w_out)) return MOCE_ERR_NULL;
+  if (sh.C > (1 << 24) || sh.k > 4096) return MOCE_ERR_UNSUPPORTED;
+  if (sh.R > 0 && (static_cast<const void*>(s) == s_out || static_cast<const void*>(w) == w_out))
+    return MOCE_ERR_NULL;
+  hipError_t e = moce::launch_prepare(sh, s, w, s_out, w_out, covered, U, info, stream);
+  if (e != hipSuccess) return MOCE_ERR_DEVICE;
+  int32_t host[2] = {0, 0};
+  e = hipMemcpyAsync(host, info, sizeof host, hipMemcpyDeviceToHost, stream);
+  if (e != hipSuccess) return MOCE_ERR_DEVICE;
+  e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return MOCE_ERR_DEVICE;
+  *nU_host = host[0];
+  *bad_expert_host = host[1];
+  return host[1] >= 0 ? MOCE_ERR_SUPPORT : MOCE_OK;
+}
+
+moce_status moce_pool(const moce_desc* desc, const void* x, float* d, hipStream_t stream) {
+  Shape sh;
+  moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  if (!x || !d) return MOCE_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(d, 4)) return MOCE_ERR_ALIGN;
+  return device_status(moce::launch_pool(sh, x, d, stream));
+}
+
+moce_status moce_gate(const moce_desc* desc, const float* d, const int32_t* s, const float* w,
+                      const moce_gate_params* gate, float* tau, float* alpha, hipStream_t stream) {
+  Shape sh;
+  moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  st = check_gate(sh, gate);
+  if (st != MOCE_OK) return st;
+  if (sh.R == 0) return MOCE_OK;
+  if (!d || !s || !w || !tau) return MOCE_ERR_NULL;
+  return device_status(moce::launch_gate(sh, d, s, w, *gate, tau, alpha, nullptr, stream));
+}
+
+moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, const float* alpha,
+                     const int32_t* U, int32_t nU, void* y, hipStream_t stream) {
+  Shape sh;
+  moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  if (!x || !y) return MOCE_ERR_NULL;
+  if (sh.R > 0 && (!s || !alpha)) return MOCE_ERR_NULL;
+  if (nU < 0 || (int64_t)nU > sh.C) return MOCE_ERR_SHAPE;
+  if (nU > 0 && !U) return MOCE_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(y, 16)) return MOCE_ERR_ALIGN;
+  return device_status(moce::launch_mix(sh, x, s, alpha, nullptr, nullptr, nullptr, U, nU, y, stream));
+}
+
+size_t moce_forward_workspace_bytes(const moce_desc* desc) {
+  Shape sh;
+  if (check_desc(desc, &sh) != MOCE_OK) return 0;
+  return ws_layout(sh).total;
+}
+
+moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
+                         const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  Shape sh;
+  moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  st = check_gate(sh, gate);
+  if (st != MOCE_OK) return st;
+  if (!x || !y) return MOCE_ERR_NULL;
+  if (sh.R > 0 && (!s || !w)) return MOCE_ERR_NULL;
+  if (nU < 0 || (int64_t)nU > sh.C) return MOCE_ERR_SHAPE;
+  if (nU > 0 && !U) return MOCE_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(y, 16)) return MOCE_ERR_ALIGN;
+  const WsLayout l = ws_layout(sh);
+  if (!ws || ws_bytes < l.total) return MOCE_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return MOCE_ERR_ALIGN;
+
+  char* base = static_cast<char*>(ws);
+  float* d = reinterpret_cast<float*>(base + l.d);
+  float* tau = reinterpret_cast<float*>(base + l.tau);
+  float* lse = reinterpret_cast<float*>(base + l.lse);
+  float* alpha = sh.layout == MOCE_NCHW ? reinterpret_cast<float*>(base + l.alpha) : nullptr;
+
+  if (gate->kind == MOCE_GATE_SOFTPLUS_LINEAR && moce::fused_eligible(sh)) {
+    int* counters = reinterpret_cast<int*>(base + l.counters);
+    const moce::FusedWs fw{d, tau, lse, counters, counters + sh.B, counters + sh.B + 8,
+                           reinterpret_cast<int32_t*>(base + l.plan)};
+    return device_status(moce::launch_fused(sh, x, s, w, *gate, U, nU, y, fw, stream));
+  }
+  hipError_t e = moce::launch_pool(sh, x, d, stream);
+  if (e != hipSuccess) return MOCE_ERR_DEVICE;
+  if (sh.R > 0) {
+    e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, alpha ? nullptr : lse, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+  }
+  e = moce::launch_mix(sh, x, s, alpha, w, tau, lse, U, nU, y, stream);
+  return device_status(e);
+}
+
+}  // extern "C"

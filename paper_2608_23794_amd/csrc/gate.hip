@@ -1,0 +1,101 @@
+// Temperatures (Sec. 3.3) and mixing coefficients (Sec. 3.3 Eq. 4).
+//
+// One wavefront per (image, routed expert).  Lanes span the k support
+// positions: each gathers the descriptor of its channel, the wave reduces the
+// gate's pre-activation, and the same lanes then form the softmax of the
+// selected logits over the temperature.  Optionally writes the coefficients
+// alpha[b][o][i] and/or the log-partition lse[b][o] = log sum_j exp(w_j / tau),
+// from which a consumer can rebuild alpha_i = exp(w_i / tau - lse).
+#include "moce_internal.h"
+
+namespace moce {
+namespace {
+
+constexpr int kGateWaves = 4;
+
+__device__ __forceinline__ void softmax_epilogue(const float* __restrict__ wo, int k, float t, int lane,
+                                                 float* __restrict__ alpha_row, float* __restrict__ lse_out) {
+  float m = -INFINITY;
+  for (int i = lane; i < k; i += kWave) m = fmaxf(m, wo[i] / t);
+  m = wave_max(m);
+  float z = 0.f;
+  for (int i = lane; i < k; i += kWave) z += expf(wo[i] / t - m);
+  z = wave_sum(z);
+  if (alpha_row) {
+    for (int i = lane; i < k; i += kWave) alpha_row[i] = expf(wo[i] / t - m) / z;
+  }
+  if (lse_out && lane == 0) *lse_out = m + logf(z);
+}
+
+__global__ void __launch_bounds__(kGateWaves * kWave)
+k_gate_softplus(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
+                const float* __restrict__ a, const float* __restrict__ c, float* __restrict__ tau,
+                float* __restrict__ alpha, float* __restrict__ lse, int64_t B, int64_t C, int R, int k) {
+  const int lane = threadIdx.x & 63;
+  const int64_t item = (int64_t)blockIdx.x * kGateWaves + (threadIdx.x >> 6);
+  if (item >= B * R) return;
+  const int64_t b = item / R;
+  const int o = (int)(item % R);
+  const int32_t* so = s + (int64_t)o * k;
+  const float* ao = a + (int64_t)o * k;
+  const float* db = d + b * C;
+  float g = 0.f;
+  for (int i = lane; i < k; i += kWave) g += ao[i] * db[so[i]];
+  g = wave_sum(g) + c[o];
+  const float t = softplusf(g) + 1e-3f;
+  if (lane == 0) tau[item] = t;
+  softmax_epilogue(w + (int64_t)o * k, k, t, lane, alpha ? alpha + item * k : nullptr,
+                   lse ? lse + item : nullptr);
+}
+
+// The paper's shared gate: h = ReLU(W1 z + b1), g = w2 . h + b2,
+// tau = tau_min + (tau_max - tau_min) sigmoid(g).  k <= 256 (4 hidden units
+// per lane at most).
+__global__ void __launch_bounds__(kGateWaves * kWave)
+k_gate_mlp(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
+           const float* __restrict__ W1, const float* __restrict__ b1, const float* __restrict__ w2,
+           float b2, float tau_min, float tau_max, float* __restrict__ tau, float* __restrict__ alpha,
+           float* __restrict__ lse, int64_t B, int64_t C, int R, int k) {
+  __shared__ float zs[kGateWaves][256];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int64_t item = (int64_t)blockIdx.x * kGateWaves + wv;
+  const bool active = item < B * R;  // every wave reaches the barrier below
+  const int64_t b = active ? item / R : 0;
+  const int o = active ? (int)(item % R) : 0;
+  const int32_t* so = s + (int64_t)o * k;
+  for (int i = lane; i < k; i += kWave) zs[wv][i] = d[b * C + so[i]];
+  __syncthreads();
+  if (!active) return;
+  float g = 0.f;
+  for (int j = lane; j < k; j += kWave) {
+    const float* row = W1 + (int64_t)j * k;
+    float h = b1[j];
+    for (int i = 0; i < k; ++i) h += row[i] * zs[wv][i];
+    g += w2[j] * fmaxf(h, 0.f);
+  }
+  g = wave_sum(g) + b2;
+  const float t = tau_min + (tau_max - tau_min) / (1.f + expf(-g));
+  if (lane == 0) tau[item] = t;
+  softmax_epilogue(w + (int64_t)o * k, k, t, lane, alpha ? alpha + item * k : nullptr,
+                   lse ? lse + item : nullptr);
+}
+
+}  // namespace
+
+hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const float* w,
+                       const moce_gate_params& g, float* tau, float* alpha, float* lse, hipStream_t st) {
+  if (sh.R == 0) return hipSuccess;
+  const int64_t items = sh.B * sh.R;
+  const unsigned blocks = (unsigned)((items + kGateWaves - 1) / kGateWaves);
+  if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR) {
+    hipLaunchKernelGGL(k_gate_softplus, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
+                       tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
+  } else {
+    hipLaunchKernelGGL(k_gate_mlp, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.W1, g.b1, g.w2,
+                       g.b2, g.tau_min, g.tau_max, tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace moce

@@ -1,0 +1,94 @@
+// Internal declarations shared by the HIP translation units of libmoce.
+// Device helpers for bfloat16 handling and wave64 reductions, plus the
+// launchers that the C ABI layer (api.hip) dispatches to.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/moce.h"
+
+namespace moce {
+
+constexpr int kWave = 64;
+
+// ---- bfloat16 <-> float32 ------------------------------------------------
+// bf16 values travel as their 16-bit patterns (uint16_t).  Widening is exact:
+// the pattern becomes the upper half of a float32.
+__device__ __forceinline__ float bf16_lo(uint32_t pair) { return __uint_as_float(pair << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t pair) { return __uint_as_float(pair & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// float32 -> bf16, round to nearest even (the hardware conversion on gfx950).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// ---- wave64 reductions ---------------------------------------------------
+template <int WIDTH = kWave>
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = WIDTH / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, WIDTH);
+  return v;
+}
+template <int WIDTH = kWave>
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = WIDTH / 2; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, WIDTH));
+  return v;
+}
+__device__ __forceinline__ int wave_min_int(int v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off, kWave));
+  return v;
+}
+
+// softplus(t) = log(1 + e^t) without overflow in either direction.
+__device__ __forceinline__ float softplusf(float t) {
+  return fmaxf(t, 0.f) + log1pf(expf(-fabsf(t)));
+}
+
+// ---- launch parameters derived from a validated descriptor ---------------
+struct Shape {
+  int64_t B, C, HW;
+  int E, R, k;       // R = E - 1 routed experts
+  int elem;          // MOCE_F32 / MOCE_BF16
+  int layout;        // MOCE_NCHW / MOCE_NHWC
+};
+
+// ---- launchers (return hipSuccess or the launch error) --------------------
+hipError_t launch_prepare(const Shape& sh, const int32_t* s, const float* w, int32_t* s_out,
+                          float* w_out, uint8_t* covered, int32_t* U, int32_t* info,
+                          hipStream_t st);
+hipError_t launch_pool(const Shape& sh, const void* x, float* d, hipStream_t st);
+// alpha and lse are optional outputs (nullptr: not written).
+hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const float* w,
+                       const moce_gate_params& g, float* tau, float* alpha, float* lse, hipStream_t st);
+// alpha != nullptr: coefficients are read from alpha[B][R][k]; otherwise
+// they are rebuilt as exp(w[o][i] / tau[b][o] - lse[b][o]).
+hipError_t launch_mix(const Shape& sh, const void* x, const int32_t* s, const float* alpha,
+                      const float* w, const float* tau, const float* lse, const int32_t* U, int nU,
+                      void* y, hipStream_t st);
+
+// Fused NCHW bf16 forward (fused.hip).  Workspace regions it needs:
+struct FusedWs {
+  float* d;        // [B][C]
+  float* tau;      // [B][R]
+  float* lse;      // [B][R]
+  int* pool_done;  // [B]
+  int* tickets;    // [8]
+  int* err;        // [1]
+  int32_t* plan;   // fused_plan_bytes(sh) bytes
+};
+// Whether the shape runs on the fused kernel (otherwise the staged path).
+bool fused_eligible(const Shape& sh);
+size_t fused_lds_bytes(const Shape& sh);
+size_t fused_plan_bytes(const Shape& sh);
+hipError_t launch_fused(const Shape& sh, const void* x, const int32_t* s, const float* w,
+                        const moce_gate_params& g, const int32_t* U, int nU, void* y, const FusedWs& ws,
+                        hipStream_t st);
+
+}  // namespace moce

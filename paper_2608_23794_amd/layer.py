@@ -1,0 +1,137 @@
+"""A MoCE layer held on the GPU, driven through the C ABI.
+
+``MoceLayer`` owns the device copies of a layer's parameters (support rows,
+selected logits, gate parameters), prepares the supports once with
+``moce_support_prepare`` and then forwards batches with ``moce_forward`` or
+the individual ``moce_pool`` / ``moce_gate`` / ``moce_mix`` calls.  Torch
+provides device memory and the current stream; every step of the layer runs in
+libmoce's HIP kernels.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import binding as mb
+
+_DT = {"f32": mb.MOCE_F32, "bf16": mb.MOCE_BF16}
+_LAYOUT = {"nchw": mb.MOCE_NCHW, "nhwc": mb.MOCE_NHWC}
+_TORCH_DT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def _dev(a, dtype, device) -> torch.Tensor:
+    return torch.as_tensor(np.ascontiguousarray(a), dtype=dtype).to(device)
+
+
+class MoceLayer:
+    def __init__(self, C: int, E: int, k: int, H: int, W: int, dtype: str, layout: str,
+                 s: np.ndarray, w: np.ndarray, gate: str = "softplus", a=None, c=None,
+                 W1=None, b1=None, w2=None, b2: float = 0.0, tau_min: float = 0.2, tau_max: float = 6.0,
+                 device: str = "cuda"):
+        self.C, self.E, self.k, self.H, self.W = C, E, k, H, W
+        self.R = E - 1
+        self.dtype, self.layout, self.device = dtype, layout, device
+        i32, f32 = torch.int32, torch.float32
+        R = self.R
+        self.s = _dev(np.asarray(s, np.int32).reshape(R, k), i32, device)
+        self.w = _dev(np.asarray(w, np.float32).reshape(R, k), f32, device)
+        self.s_c = torch.empty((R, k), dtype=i32, device=device)
+        self.w_c = torch.empty((R, k), dtype=f32, device=device)
+        self.covered = torch.empty(C, dtype=torch.uint8, device=device)
+        self.U = torch.empty(C, dtype=i32, device=device)
+        self.info = torch.empty(2, dtype=i32, device=device)
+        self._keep = []
+        if gate == "softplus":
+            self.a = _dev(np.asarray(a, np.float32).reshape(R, k), f32, device)
+            self.c = _dev(np.asarray(c, np.float32).reshape(R), f32, device)
+            self.gate = mb.make_gate(mb.MOCE_GATE_SOFTPLUS_LINEAR, a=self.a, c=self.c)
+        elif gate == "mlp":
+            self.W1 = _dev(np.asarray(W1, np.float32).reshape(k, k), f32, device)
+            self.b1 = _dev(np.asarray(b1, np.float32).reshape(k), f32, device)
+            self.w2 = _dev(np.asarray(w2, np.float32).reshape(k), f32, device)
+            self.gate = mb.make_gate(mb.MOCE_GATE_MLP_SIGMOID, W1=self.W1, b1=self.b1, w2=self.w2,
+                                     b2=float(b2), tau_min=float(tau_min), tau_max=float(tau_max))
+        else:
+            raise ValueError(gate)
+        self.status, self.nU, self.bad_expert = self.prepare(check=False)
+
+    # -- construction helpers ------------------------------------------------
+    @classmethod
+    def from_workload(cls, wl, params: dict, layout: Optional[str] = None, gate: str = "softplus",
+                      device: str = "cuda") -> "MoceLayer":
+        return cls(wl.C, wl.E, wl.k, wl.H, wl.W, wl.dtype, layout or wl.layouts[0], params["s"], params["w"],
+                   gate=gate, a=params.get("a"), c=params.get("c"), W1=params.get("W1"),
+                   b1=params.get("b1"), w2=params.get("w2"), b2=float(params.get("b2", 0.0)),
+                   tau_min=float(params.get("tau_min", 0.2)), tau_max=float(params.get("tau_max", 6.0)),
+                   device=device)
+
+    def desc(self, B: int) -> mb.moce_desc:
+        return mb.make_desc(B, self.C, self.H, self.W, self.E, self.k, _DT[self.dtype], _LAYOUT[self.layout])
+
+    @property
+    def torch_dtype(self):
+        return _TORCH_DT[self.dtype]
+
+    def y_shape(self, B: int):
+        return (B, self.E, self.H, self.W) if self.layout == "nchw" else (B, self.H, self.W, self.E)
+
+    def _stream(self):
+        return torch.cuda.current_stream(self.device)
+
+    # -- the C ABI -------------------------------------------------------------
+    def prepare(self, check: bool = True):
+        return mb.moce_support_prepare(self.desc(1), self.s, self.w, self.s_c, self.w_c, self.covered, self.U,
+                                       self.info, self._stream(), check=check)
+
+    def pool(self, x: torch.Tensor, d: Optional[torch.Tensor] = None) -> torch.Tensor:
+        B = x.shape[0]
+        if d is None:
+            d = torch.empty((B, self.C), dtype=torch.float32, device=self.device)
+        mb.moce_pool(self.desc(B), x, d, self._stream())
+        return d
+
+    def gate_tau(self, d: torch.Tensor, with_alpha: bool = True):
+        B = d.shape[0]
+        tau = torch.empty((B, self.R), dtype=torch.float32, device=self.device)
+        alpha = torch.empty((B, self.R, self.k), dtype=torch.float32, device=self.device) if with_alpha else None
+        mb.moce_gate(self.desc(B), d, self.s_c, self.w_c, self.gate, tau, alpha, self._stream())
+        return tau, alpha
+
+    def mix(self, x: torch.Tensor, alpha: torch.Tensor, y: Optional[torch.Tensor] = None) -> torch.Tensor:
+        B = x.shape[0]
+        if y is None:
+            y = torch.empty(self.y_shape(B), dtype=x.dtype, device=self.device)
+        mb.moce_mix(self.desc(B), x, self.s_c, alpha, self.U if self.nU else None, self.nU, y, self._stream())
+        return y
+
+    def workspace_bytes(self, B: int) -> int:
+        return mb.moce_forward_workspace_bytes(self.desc(B))
+
+    def new_workspace(self, B: int) -> torch.Tensor:
+        return torch.empty(max(self.workspace_bytes(B), 1), dtype=torch.uint8, device=self.device)
+
+    def forward(self, x: torch.Tensor, y: Optional[torch.Tensor] = None,
+                ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+        B = x.shape[0]
+        if y is None:
+            y = torch.empty(self.y_shape(B), dtype=x.dtype, device=self.device)
+        if ws is None:
+            ws = self.new_workspace(B)
+        mb.moce_forward(self.desc(B), x, self.s_c, self.w_c, self.gate, self.U if self.nU else None, self.nU,
+                        y, ws, ws.numel(), self._stream())
+        return y
+
+
+def to_device_x(x: np.ndarray, dtype: str, device: str = "cuda") -> torch.Tensor:
+    """Uploads f32 values or bf16 bit patterns (uint16) as a float32/bfloat16 tensor."""
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(device)
+    bits = np.ascontiguousarray(x, np.uint16).view(np.int16)
+    return torch.from_numpy(bits).to(device).view(torch.bfloat16)
+
+
+def to_host_f64(y: torch.Tensor) -> np.ndarray:
+    """Exact float64 copy of a float32 or bfloat16 device tensor."""
+    return y.float().cpu().numpy().astype(np.float64)

@@ -1,0 +1,185 @@
+"""The C ABI library: it loads, exports every entry point include/moce.h
+declares, and rejects invalid arguments on the host before any GPU work.
+
+Every call here fails host-side validation, so nothing reaches the GPU; the
+pointers are placeholders that are never dereferenced.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_23794_amd import binding as mb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moce.h")
+
+FAKE = 0x10000  # 64 KiB-aligned placeholder address, never dereferenced
+FAKE_UNALIGNED = 0x10008
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^[A-Za-z_][\w \*]*?\b(moce_\w+)\s*\(", text, flags=re.M)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(mb.LIB_PATH):
+        from paper_2608_23794_amd import build
+        build.build()
+    return mb.load()
+
+
+def test_header_declares_the_binding_entry_points():
+    assert sorted(declared_functions()) == sorted(mb.ENTRY_POINTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", mb.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\b(moce_\w+)\b", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_abi_version_and_status_strings(lib):
+    assert mb.moce_abi_version() == 1
+    for code, name in mb.STATUS.items():
+        assert mb.moce_status_str(code).startswith(name)
+    assert mb.moce_status_str(12345) == "unknown moce_status"
+
+
+def good_desc(**kw):
+    d = dict(B=2, C=64, H=8, W=8, E=16, k=8, dtype=mb.MOCE_BF16, layout=mb.MOCE_NCHW)
+    d.update(kw)
+    return mb.make_desc(d["B"], d["C"], d["H"], d["W"], d["E"], d["k"], d["dtype"], d["layout"])
+
+
+BAD_DESCS = [
+    (dict(B=0), -2),
+    (dict(C=0), -2), (dict(H=0), -2), (dict(W=-1), -2),
+    (dict(E=0), -2), (dict(E=65), -2), (dict(k=0), -2), (dict(k=65), -2),
+    (dict(dtype=7), -3), (dict(layout=2), -4),
+    (dict(H=1 << 31), -10), (dict(C=1 << 20, H=1 << 11, W=1 << 11), -10),
+]
+
+
+def _call_pool(desc, x=FAKE, d=FAKE):
+    return mb.raw_status("moce_pool", ctypes.byref(desc), x, d, None)
+
+
+def _call_mix(desc, x=FAKE, s=FAKE, alpha=FAKE, U=FAKE, nU=0, y=FAKE):
+    return mb.raw_status("moce_mix", ctypes.byref(desc), x, s, alpha, U, nU, y, None)
+
+
+def _call_gate(desc, gate, d=FAKE, s=FAKE, w=FAKE, tau=FAKE, alpha=FAKE):
+    g = ctypes.byref(gate) if gate is not None else None
+    return mb.raw_status("moce_gate", ctypes.byref(desc), d, s, w, g, tau, alpha, None)
+
+
+def _call_forward(desc, gate, x=FAKE, s=FAKE, w=FAKE, U=FAKE, nU=0, y=FAKE, ws=FAKE, ws_bytes=1 << 30):
+    g = ctypes.byref(gate) if gate is not None else None
+    return mb.raw_status("moce_forward", ctypes.byref(desc), x, s, w, g, U, nU, y, ws, ws_bytes, None)
+
+
+def _call_prepare(desc, s=FAKE, w=FAKE, s_out=FAKE + 256, w_out=FAKE + 512, covered=FAKE, U=FAKE, info=FAKE,
+                  nU=True, bad=True):
+    n = ctypes.c_int32(0)
+    b = ctypes.c_int32(0)
+    return mb.raw_status("moce_support_prepare", ctypes.byref(desc), s, w, s_out, w_out, covered, U, info,
+                         ctypes.byref(n) if nU else None, ctypes.byref(b) if bad else None, None)
+
+
+@pytest.mark.parametrize("change,code", [(c, s) for c, s in BAD_DESCS])
+def test_descriptor_errors_every_entry_point(lib, change, code):
+    desc = good_desc(**change)
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+    assert _call_pool(desc) == code
+    assert _call_mix(desc) == code
+    assert _call_gate(desc, gate) == code
+    assert _call_forward(desc, gate) == code
+    assert _call_prepare(desc) == code
+    assert lib.moce_forward_workspace_bytes(ctypes.byref(desc)) == 0
+
+
+def test_mismatched_x_and_y_types(lib):
+    desc = good_desc()
+    desc.y_dtype = mb.MOCE_F32
+    assert _call_pool(desc) == -3
+
+
+def test_null_descriptor(lib):
+    assert mb.raw_status("moce_pool", None, FAKE, FAKE, None) == -1
+    assert lib.moce_forward_workspace_bytes(None) == 0
+
+
+def test_null_pointers(lib):
+    desc = good_desc()
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+    assert _call_pool(desc, x=None) == -1
+    assert _call_pool(desc, d=None) == -1
+    assert _call_mix(desc, x=None) == -1
+    assert _call_mix(desc, s=None) == -1
+    assert _call_mix(desc, alpha=None) == -1
+    assert _call_mix(desc, y=None) == -1
+    assert _call_mix(desc, U=None, nU=3) == -1
+    assert _call_gate(desc, gate, d=None) == -1
+    assert _call_gate(desc, gate, tau=None) == -1
+    assert _call_gate(desc, None) == -1
+    assert _call_gate(desc, mb.make_gate(a=None, c=FAKE)) == -1
+    assert _call_gate(desc, mb.make_gate(mb.MOCE_GATE_MLP_SIGMOID, W1=None, b1=FAKE, w2=FAKE)) == -1
+    assert _call_forward(desc, gate, x=None) == -1
+    assert _call_forward(desc, gate, w=None) == -1
+    assert _call_forward(desc, gate, U=None, nU=2) == -1
+    assert _call_forward(desc, None) == -1
+    assert _call_prepare(desc, covered=None) == -1
+    assert _call_prepare(desc, info=None) == -1
+    assert _call_prepare(desc, nU=False) == -1
+    assert _call_prepare(desc, bad=False) == -1
+    assert _call_prepare(desc, s_out=FAKE) == -1  # s_out aliases s
+
+
+def test_alignment_and_residual_count(lib):
+    desc = good_desc()
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+    assert _call_pool(desc, x=FAKE_UNALIGNED) == -8
+    assert _call_mix(desc, y=FAKE_UNALIGNED) == -8
+    assert _call_forward(desc, gate, x=FAKE_UNALIGNED) == -8
+    assert _call_forward(desc, gate, ws=FAKE + 64) == -8
+    assert _call_mix(desc, nU=-1) == -2
+    assert _call_mix(desc, nU=65) == -2
+    assert _call_forward(desc, gate, nU=65) == -2
+
+
+def test_gate_parameter_errors(lib):
+    desc = good_desc()
+    assert _call_gate(desc, mb.make_gate(kind=9, a=FAKE, c=FAKE)) == -6
+    mlp = dict(kind=mb.MOCE_GATE_MLP_SIGMOID, W1=FAKE, b1=FAKE, w2=FAKE)
+    assert _call_gate(desc, mb.make_gate(**mlp, tau_min=0.0)) == -6
+    assert _call_gate(desc, mb.make_gate(**mlp, tau_min=2.0, tau_max=1.0)) == -6
+    assert _call_gate(desc, mb.make_gate(**mlp, tau_max=float("inf"))) == -6
+    assert _call_gate(desc, mb.make_gate(**mlp, b2=float("nan"))) == -6
+    big = good_desc(C=512, k=300)
+    assert _call_gate(big, mb.make_gate(**mlp)) == -10
+
+
+def test_workspace_size_and_errors(lib):
+    desc = good_desc()
+    need = lib.moce_forward_workspace_bytes(ctypes.byref(desc))
+    # d [2][64] + tau [2][15] + lse [2][15] + counters [2 + 8 + 1] + alpha [2][15][8],
+    # each rounded up to 256 bytes
+    assert need == 512 + 256 + 256 + 256 + 1024
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+    assert _call_forward(desc, gate, ws=None) == -7
+    assert _call_forward(desc, gate, ws_bytes=need - 1) == -7
+    nhwc = good_desc(layout=mb.MOCE_NHWC)
+    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 256 + 256
+
+
+def test_prepare_limits(lib):
+    assert _call_prepare(good_desc(C=1 << 25, H=1, W=1, E=2, k=4097)) == -10

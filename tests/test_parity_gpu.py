@@ -1,0 +1,356 @@
+"""GPU parity: the HIP library, called through its C ABI, against the CPU oracle.
+
+Integer outputs (canonical supports, coverage mask, uncovered list and count,
+the first bad expert) must match bit for bit.  Float outputs must satisfy
+
+* descriptor d:  |d - d_ref| <= 1e-5 * mean|x| over the plane;
+* temperature:   |tau - tau_ref| <= 1e-5 * tau_ref;
+* coefficients:  |alpha - alpha_ref| <= 1e-5 * max_i alpha_ref (per row);
+* outputs y:     |y - y_ref| <= rtol * M, M = sum_i alpha_i |x_i| (the oracle's
+  magnitude), rtol = 1e-5 for float32 and 1e-2 for bfloat16 outputs; bfloat16
+  outputs must in addition be within one rounding of the float32 result,
+  |y - y_ref| <= 2^-8 |y_ref| + 1e-5 * M.
+
+Inputs come from the seeded workload generator; nothing the GPU computes is
+ever fed to the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_23794_amd import binding as mb
+from paper_2608_23794_amd import inputs
+from paper_2608_23794_amd.layer import MoceLayer, to_device_x, to_host_f64
+
+pytestmark = [pytest.mark.gpu, pytest.mark.usefixtures("oracle_lib")]
+
+CASES = [("tiny", "nchw"), ("tiny", "nhwc"), ("resnet50_stage1", "nchw"), ("resnet50_stage3", "nchw"),
+         ("resnet50_stage3", "nhwc"), ("resnet50_stage4", "nhwc"), ("vit_tokens", "nhwc")]
+OL = {"nchw": oracle.NCHW, "nhwc": oracle.NHWC}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    mb.load()
+    yield
+    torch.cuda.synchronize()
+
+
+_cache = {}
+
+
+def workload(name, layout):
+    key = (name, layout)
+    if key not in _cache:
+        wl = inputs.WORKLOADS[name]
+        g = inputs.generate(wl, layout)
+        ref = oracle.forward(g["x"], g["s"], g["w"], wl.E, OL[layout], a=g["a"], c=g["c"])
+        _cache.clear()
+        _cache[key] = (wl, g, ref)
+    return _cache[key]
+
+
+def abs_mean(x, layout):
+    if x.dtype == np.uint16:
+        x = x & np.uint16(0x7FFF)
+    else:
+        x = np.abs(x)
+    return oracle.pool(x, OL[layout])
+
+
+def check_d(d, d_ref, scale):
+    err = np.abs(d - d_ref) / np.maximum(scale, 1e-30)
+    assert err.max() <= 1e-5, f"d: max normalised error {err.max():.3e}"
+
+
+def check_tau_alpha(tau, tau_ref, alpha=None, alpha_ref=None):
+    e = np.abs(tau - tau_ref) / tau_ref
+    assert e.max() <= 1e-5, f"tau: max relative error {e.max():.3e}"
+    if alpha is not None:
+        rowmax = alpha_ref.max(axis=-1, keepdims=True)
+        ea = np.abs(alpha - alpha_ref) / rowmax
+        assert ea.max() <= 1e-5, f"alpha: max normalised error {ea.max():.3e}"
+
+
+def check_y(y, y_ref, mag, dtype):
+    tiny = 1e-30
+    err = np.abs(y - y_ref)
+    rtol = 1e-5 if dtype == "f32" else 1e-2
+    norm = err / np.maximum(mag, tiny)
+    worst = np.unravel_index(np.argmax(norm), norm.shape)
+    assert norm.max() <= rtol, f"y: max error/M {norm.max():.3e} at {worst}"
+    if dtype == "bf16":
+        bound = 2.0 ** -8 * np.abs(y_ref) + 1e-5 * mag + tiny
+        assert np.all(err <= bound), f"y: {int((err > bound).sum())} outputs beyond one bf16 rounding"
+    return float(norm.max())
+
+
+# --------------------------------------------------------------------------- prepare
+
+@pytest.mark.parametrize("name,layout", [CASES[i] for i in (0, 2, 3, 5, 6)])
+def test_prepare_bit_exact(name, layout):
+    wl, g, ref = workload(name, layout)
+    layer = MoceLayer.from_workload(wl, g, layout)
+    assert layer.status == 0 and layer.bad_expert == -1
+    torch.cuda.synchronize()
+    assert np.array_equal(layer.s_c.cpu().numpy(), ref["s"])
+    assert np.array_equal(layer.w_c.cpu().numpy().view(np.uint32), ref["w"].view(np.uint32))
+    assert np.array_equal(layer.covered.cpu().numpy(), ref["covered"])
+    assert layer.nU == ref["nU"]
+    assert np.array_equal(layer.U.cpu().numpy()[:layer.nU], ref["U"])
+    assert layer.info.cpu().numpy().tolist() == [ref["nU"], -1]
+    if name == "resnet50_stage3":
+        assert layer.nU == 51
+
+
+@pytest.mark.parametrize("C,E,k", [(64, 16, 8), (100, 7, 13), (32, 32, 32), (17, 3, 5), (64, 1, 4),
+                                   (1000, 3, 1000), (5000, 9, 700)])
+def test_prepare_cyclic_and_ties(C, E, k):
+    rng = np.random.default_rng(C + E + k)
+    R = E - 1
+    s = np.array([[(e * k + j) % C for j in range(k)] for e in range(R)], np.int32).reshape(R, k)
+    w = np.round(rng.standard_normal((R, k)) * 2).astype(np.float32)  # many ties
+    w[:, ::7] = -0.0
+    s_ref, w_ref, cov_ref, U_ref, nU_ref = oracle.prepare(C, E, s, w)
+    layer = MoceLayer(C, E, k, 1, 1, "f32", "nchw", s, w, a=np.zeros((R, k)), c=np.zeros(R))
+    assert layer.status == 0
+    assert np.array_equal(layer.s_c.cpu().numpy(), s_ref)
+    assert np.array_equal(layer.w_c.cpu().numpy().view(np.uint32), w_ref.view(np.uint32))
+    assert np.array_equal(layer.covered.cpu().numpy(), cov_ref)
+    assert layer.nU == nU_ref and np.array_equal(layer.U.cpu().numpy()[:nU_ref], U_ref)
+
+
+@pytest.mark.parametrize("bad", ["dup", "neg", "range", "nan", "inf", "two_rows"])
+def test_prepare_rejects_invalid_rows_like_the_oracle(bad):
+    rng = np.random.default_rng(4)
+    C, E, k = 300, 40, 24
+    R = E - 1
+    s = np.array([rng.choice(C, k, replace=False) for _ in range(R)], np.int32)
+    w = rng.standard_normal((R, k)).astype(np.float32)
+    o = 17
+    if bad == "dup":
+        s[o, 20] = s[o, 3]
+    elif bad == "neg":
+        s[o, 5] = -7
+    elif bad == "range":
+        s[o, 0] = C
+    elif bad == "nan":
+        w[o, 9] = np.nan
+    elif bad == "inf":
+        w[o, 9] = np.inf
+    else:
+        s[30, 1] = s[30, 2]
+        s[o, 4] = C + 5
+    with pytest.raises(oracle.SupportError) as ei:
+        oracle.prepare(C, E, s, w)
+    layer = MoceLayer(C, E, k, 2, 2, "f32", "nchw", s, w, a=np.zeros((R, k)), c=np.zeros(R))
+    assert layer.status == -5
+    assert layer.bad_expert == ei.value.expert == o
+
+
+# --------------------------------------------------------------------------- pool / gate / mix
+
+@pytest.mark.parametrize("name,layout", CASES)
+def test_pool(name, layout):
+    wl, g, ref = workload(name, layout)
+    layer = MoceLayer.from_workload(wl, g, layout)
+    x = to_device_x(g["x"], wl.dtype)
+    d = layer.pool(x).cpu().numpy().astype(np.float64)
+    check_d(d, ref["d"], abs_mean(g["x"], layout))
+
+
+@pytest.mark.parametrize("name", ["tiny", "resnet50_stage1", "resnet50_stage3", "resnet50_stage4", "vit_tokens"])
+def test_gate_softplus_isolated(name):
+    wl = inputs.WORKLOADS[name]
+    g = inputs.generate(wl, with_x=False)
+    d = inputs.random_descriptor(wl.B, wl.C, seed=wl.seed, signed=wl.signed)
+    s_c, w_c, _, _, _ = oracle.prepare(wl.C, wl.E, g["s"], g["w"])
+    tau_ref = oracle.gate_softplus(d, s_c, g["a"], g["c"])
+    alpha_ref = oracle.softmax(w_c, tau_ref)
+    layer = MoceLayer.from_workload(wl, g)
+    tau, alpha = layer.gate_tau(torch.from_numpy(d).cuda())
+    check_tau_alpha(tau.cpu().numpy(), tau_ref, alpha.cpu().numpy(), alpha_ref)
+
+
+@pytest.mark.parametrize("name", ["tiny", "resnet50_stage1", "resnet50_stage3"])
+def test_gate_mlp_isolated(name):
+    wl = inputs.WORKLOADS[name]
+    g = inputs.generate(wl, with_x=False)
+    d = inputs.random_descriptor(wl.B, wl.C, seed=wl.seed + 100)
+    s_c, w_c, _, _, _ = oracle.prepare(wl.C, wl.E, g["s"], g["w"])
+    tau_ref = oracle.gate_mlp(d, s_c, g["W1"], g["b1"], g["w2"], g["b2"], g["tau_min"], g["tau_max"])
+    alpha_ref = oracle.softmax(w_c, tau_ref)
+    layer = MoceLayer.from_workload(wl, g, gate="mlp")
+    tau, alpha = layer.gate_tau(torch.from_numpy(d).cuda())
+    tau = tau.cpu().numpy()
+    assert np.all(tau >= float(g["tau_min"])) and np.all(tau <= float(g["tau_max"]))
+    check_tau_alpha(tau, tau_ref, alpha.cpu().numpy(), alpha_ref)
+
+
+@pytest.mark.parametrize("name,layout", CASES)
+def test_mix_with_given_coefficients(name, layout):
+    wl, g, ref = workload(name, layout)
+    alpha32 = ref["alpha"].astype(np.float32)
+    y_ref, mag = oracle.mix(g["x"], ref["s"], alpha32.astype(np.float64), ref["U"], wl.E, OL[layout])
+    layer = MoceLayer.from_workload(wl, g, layout)
+    y = layer.mix(to_device_x(g["x"], wl.dtype), torch.from_numpy(alpha32).cuda())
+    check_y(to_host_f64(y), y_ref, mag, wl.dtype)
+
+
+@pytest.mark.parametrize("name,layout", CASES)
+def test_forward(name, layout):
+    wl, g, ref = workload(name, layout)
+    layer = MoceLayer.from_workload(wl, g, layout)
+    x = to_device_x(g["x"], wl.dtype)
+    y = layer.forward(x)
+    e = check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
+    print(f"{name}/{layout}: max |y - y_ref| / M = {e:.3e}")
+
+
+@pytest.mark.parametrize("name,layout", [("tiny", "nchw"), ("resnet50_stage3", "nchw"), ("vit_tokens", "nhwc")])
+def test_forward_mlp_gate(name, layout):
+    wl = inputs.WORKLOADS[name]
+    g = inputs.generate(wl, layout)
+    ref = oracle.forward(g["x"], g["s"], g["w"], wl.E, OL[layout], gate="mlp", W1=g["W1"], b1=g["b1"],
+                         w2=g["w2"], b2=g["b2"], tau_min=g["tau_min"], tau_max=g["tau_max"])
+    layer = MoceLayer.from_workload(wl, g, layout, gate="mlp")
+    y = layer.forward(to_device_x(g["x"], wl.dtype))
+    check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
+
+
+# --------------------------------------------------------------------------- edge cases
+
+def _custom(B, C, E, k, H, W, dtype, layout, seed, signed=False, cyclic=False, s=None, w=None):
+    rng = np.random.default_rng(seed)
+    R = E - 1
+    if s is None:
+        if cyclic:
+            s = np.array([[(e * k + j) % C for j in range(k)] for e in range(R)], np.int32).reshape(R, k)
+        else:
+            s = np.array([rng.choice(C, k, replace=False) for _ in range(R)], np.int32).reshape(R, k)
+    if w is None:
+        w = rng.standard_normal((R, k)).astype(np.float32)
+    a = (rng.standard_normal((R, k)) * k ** -0.5).astype(np.float32)
+    c = rng.standard_normal(R).astype(np.float32) * np.float32(0.5)
+    shape = (B, C, H, W) if layout == "nchw" else (B, H, W, C)
+    x = rng.standard_normal(shape).astype(np.float32)
+    if not signed:
+        x = np.maximum(x, 0)
+    if dtype == "bf16":
+        x = inputs.f32_to_bf16_bits(x)
+    return x, s, w, a, c
+
+
+EDGE = [
+    # B, C, E, k, H, W, dtype, layout, extra
+    (3, 64, 1, 4, 5, 9, "f32", "nchw", {}),            # no routed expert: y = mean over all channels
+    (2, 96, 13, 8, 7, 7, "bf16", "nchw", dict(cyclic=True)),  # |U| = 0 exactly, ragged 2-byte rows
+    (2, 40, 9, 1, 3, 11, "bf16", "nchw", {}),          # k = 1
+    (1, 24, 24, 24, 13, 5, "f32", "nchw", {}),         # E = C = k
+    (5, 200, 30, 17, 10, 10, "bf16", "nchw", dict(signed=True)),  # 8-byte rows, tail tile
+    (2, 50, 11, 7, 1, 1, "bf16", "nchw", {}),          # one position
+    (2, 700, 40, 20, 6, 6, "f32", "nchw", {}),         # tile beyond LDS: global-memory path
+    (3, 60, 10, 6, 5, 7, "bf16", "nhwc", {}),          # C*2 not a multiple of 16: scalar pooling
+    (2, 6000, 30, 40, 3, 3, "bf16", "nhwc", {}),        # tile beyond LDS: global-memory path
+    (4, 72, 9, 9, 9, 1, "f32", "nhwc", dict(signed=True)),
+    (1, 2048, 512, 128, 1, 1, "bf16", "nhwc", {}),      # single token
+]
+
+
+@pytest.mark.parametrize("B,C,E,k,H,W,dtype,layout,extra", EDGE)
+def test_forward_edge_cases(B, C, E, k, H, W, dtype, layout, extra):
+    x, s, w, a, c = _custom(B, C, E, k, H, W, dtype, layout, seed=B * 1000 + C + E + k, **extra)
+    ref = oracle.forward(x, s, w, E, OL[layout], a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, dtype, layout, s, w, a=a, c=c)
+    assert layer.nU == ref["nU"]
+    y = to_host_f64(layer.forward(to_device_x(x, dtype)))
+    check_y(y, ref["y"], ref["mag"], dtype)
+    res = y[:, E - 1] if layout == "nchw" else y[..., E - 1]
+    if ref["nU"] == 0:
+        assert np.all(res == 0.0)
+    if k == 1:  # a single channel per expert is copied exactly, even in bf16
+        routed = y[:, :E - 1] if layout == "nchw" else y[..., :E - 1]
+        rr = ref["y"][:, :E - 1] if layout == "nchw" else ref["y"][..., :E - 1]
+        assert np.array_equal(routed, rr)
+
+
+def test_one_hot_limit_is_an_exact_copy():
+    B, C, E, k, H, W = 2, 80, 12, 6, 8, 8
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=77)
+    w[:, 0] = w.max(axis=1) + 1.0       # a clear top logit
+    a[:] = 0.0
+    c[:] = -1e4                          # tau = 1e-3
+    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    assert np.array_equal(y[:, :E - 1], ref["y"][:, :E - 1])
+
+
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+def test_forward_deterministic_and_fully_written(layout):
+    wl = inputs.WORKLOADS["resnet50_stage3"]
+    g = inputs.generate(wl, layout, batch=8)
+    layer = MoceLayer.from_workload(wl, g, layout)
+    x = to_device_x(g["x"], wl.dtype)
+    shape = layer.y_shape(8)
+    n = int(np.prod(shape))
+    guard = 4096
+    buf = torch.full((n + 2 * guard,), float("nan"), dtype=torch.bfloat16, device="cuda")
+    y = buf[guard:guard + n].view(shape)
+    layer.forward(x, y)
+    torch.cuda.synchronize()
+    first = y.clone()
+    assert not torch.isnan(first).any(), "some outputs were not written"
+    assert torch.isnan(buf[:guard]).all() and torch.isnan(buf[guard + n:]).all(), "write outside y"
+    layer.forward(x, y)
+    assert torch.equal(first.view(torch.int16), y.view(torch.int16)), "forward is not deterministic"
+
+
+def test_batch_prefix_consistency():
+    """Images are independent: the first images of a batch do not depend on the rest."""
+    wl = inputs.WORKLOADS["resnet50_stage1"]
+    g = inputs.generate(wl, batch=6)
+    layer = MoceLayer.from_workload(wl, g)
+    x = to_device_x(g["x"], wl.dtype)
+    full = layer.forward(x)
+    part = layer.forward(x[:2].contiguous())
+    assert torch.equal(full[:2].view(torch.int16), part.view(torch.int16))
+
+
+# --------------------------------------------------------------------------- fused forward (NCHW bf16)
+
+FUSED = [
+    # B, C, E, k, H, W: shapes served by the persistent fused kernel
+    (3, 256, 64, 32, 56, 56),    # fewer images than queues
+    (9, 256, 64, 32, 56, 56),    # uneven queues
+    (8, 128, 32, 16, 10, 20),    # tile of 128 positions with a ragged tail
+    (5, 64, 64, 64, 16, 24),     # E = C = k
+    (4, 96, 24, 12, 30, 30),     # channels not a multiple of the pool block
+    (2, 256, 8, 256, 16, 16),    # k = C
+]
+
+
+@pytest.mark.parametrize("B,C,E,k,H,W", FUSED)
+def test_fused_forward_shapes(B, C, E, k, H, W):
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=B + C + E + k + H)
+    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    check_y(y, ref["y"], ref["mag"], "bf16")
+
+
+def test_fused_forward_reused_workspace_sees_new_inputs():
+    """Published descriptors and temperatures of one call never leak into the next."""
+    wl = inputs.WORKLOADS["resnet50_stage1"]
+    g = inputs.generate(wl, batch=16)
+    layer = MoceLayer.from_workload(wl, g)
+    ws = layer.new_workspace(16)
+    xs = [g["x"], np.ascontiguousarray(g["x"][::-1]), inputs.f32_to_bf16_bits(
+        inputs.bf16_bits_to_f32(g["x"]) * np.float32(3.0))]
+    y = None
+    for x in xs + xs[:1]:
+        ref = oracle.forward(x, g["s"], g["w"], wl.E, oracle.NCHW, a=g["a"], c=g["c"])
+        y = layer.forward(to_device_x(x, wl.dtype), y, ws)
+        check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
