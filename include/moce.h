@@ -142,6 +142,16 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
  * descriptor).  The workspace holds the descriptor d and the temperatures. */
 size_t moce_forward_workspace_bytes(const moce_desc* desc);
 
+/* Paths moce_forward can take. */
+enum { MOCE_PATH_STAGED = 0, MOCE_PATH_FUSED = 1 };
+
+/* The path moce_forward takes for `desc` and gate kind `gate_kind` on the
+ * current device: MOCE_PATH_FUSED, the single-pass kernel (NCHW bfloat16,
+ * C <= 256, H*W a multiple of 8 and at least 128, softplus-linear gate), or
+ * MOCE_PATH_STAGED, the pool, gate and mix kernels in turn.  Both compute the
+ * same values.  A negative moce_status for an invalid descriptor or gate kind. */
+int moce_forward_path(const moce_desc* desc, int gate_kind);
+
 /* The whole layer (Secs. 3.3-3.4): pooling, temperatures, mixing
  * coefficients, routed experts and residual, equal to moce_pool + moce_gate +
  * moce_mix.  s, w: prepared rows; U, nU: as returned by moce_support_prepare;

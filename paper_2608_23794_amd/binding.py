@@ -29,7 +29,8 @@ STATUS = {
 # Every function include/moce.h declares, in declaration order.
 ENTRY_POINTS = (
     "moce_support_prepare", "moce_pool", "moce_gate", "moce_mix",
-    "moce_forward_workspace_bytes", "moce_forward", "moce_status_str", "moce_abi_version",
+    "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_status_str",
+    "moce_abi_version",
 )
 
 
@@ -76,6 +77,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_mix.argtypes = [D, P, P, P, P, I32, P, P]
     lib.moce_forward_workspace_bytes.argtypes = [D]
     lib.moce_forward_workspace_bytes.restype = SZ
+    lib.moce_forward_path.argtypes = [D, ctypes.c_int]
     lib.moce_forward.argtypes = [D, P, P, P, G, P, I32, P, P, SZ, P]
     lib.moce_status_str.argtypes = [ctypes.c_int]
     lib.moce_status_str.restype = ctypes.c_char_p
@@ -152,6 +154,17 @@ def moce_mix(desc: moce_desc, x, s, alpha, U, nU: int, y, stream=None) -> None:
 
 def moce_forward_workspace_bytes(desc: moce_desc) -> int:
     return int(load().moce_forward_workspace_bytes(ctypes.byref(desc)))
+
+
+PATH_STAGED, PATH_FUSED = 0, 1
+
+
+def moce_forward_path(desc: moce_desc, gate_kind: int) -> int:
+    """PATH_FUSED or PATH_STAGED: the path moce_forward takes on the current device."""
+    r = int(load().moce_forward_path(ctypes.byref(desc), gate_kind))
+    if r < 0:
+        raise MoceError("moce_forward_path", r)
+    return r
 
 
 def moce_forward(desc: moce_desc, x, s, w, gate: moce_gate_params, U, nU: int, y, ws, ws_bytes: int,

@@ -1,6 +1,7 @@
 // C ABI of libmoce: host-side validation, workspace layout and dispatch to
 // the kernels of prepare.hip, pool.hip, gate.hip and mix.hip.  Every check that
 // can fail on the host runs before anything is enqueued.
+#include <algorithm>
 #include <climits>
 #include <cmath>
 #include <cstring>
@@ -63,26 +64,27 @@ moce_status device_status(hipError_t e) { return e == hipSuccess ? MOCE_OK : MOC
 
 size_t elem_bytes(const Shape& sh) { return sh.elem == MOCE_F32 ? 4 : 2; }
 
-// Forward workspace: d [B][C], tau [B][R], lse [B][R], counters
-// (per-image pool counts [B], 8 queue tickets, an error word), the fused
-// kernel's support plan, and for NCHW the coefficients alpha [B][R][k] of the
-// staged path; every region starts on a 256-byte boundary.
+// Forward workspace: d [B][C] (on the fused path the per-tile channel sums
+// [B][C][nt rounded up to 4] instead), tau [B][R], lse [B][R], counters (per-image tile counts
+// [B], 8 spare words, an error word), and for NCHW the coefficients
+// alpha [B][R][k] of the staged path; every region starts on a 256-byte
+// boundary.
 struct WsLayout {
-  size_t d, tau, lse, counters, plan, alpha, total;
+  size_t d, tau, lse, counters, alpha, total;
 };
 WsLayout ws_layout(const Shape& sh) {
   WsLayout l{};
   size_t off = 0;
   l.d = off;
-  off += round_up((size_t)sh.B * sh.C * sizeof(float));
+  size_t d_floats = (size_t)sh.B * sh.C;
+  if (moce::fused_eligible(sh)) d_floats = std::max(d_floats, moce::fused_partial_floats(sh));
+  off += round_up(d_floats * sizeof(float));
   l.tau = off;
   off += round_up((size_t)sh.B * sh.R * sizeof(float));
   l.lse = off;
   off += round_up((size_t)sh.B * sh.R * sizeof(float));
   l.counters = off;
   off += round_up((size_t)(sh.B + 8 + 1) * sizeof(int));
-  l.plan = off;
-  if (moce::fused_eligible(sh)) off += round_up(moce::fused_plan_bytes(sh));
   l.alpha = off;
   if (sh.layout == MOCE_NCHW) off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
   l.total = off;
@@ -176,6 +178,14 @@ size_t moce_forward_workspace_bytes(const moce_desc* desc) {
   return ws_layout(sh).total;
 }
 
+int moce_forward_path(const moce_desc* desc, int gate_kind) {
+  Shape sh;
+  const moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  if (gate_kind != MOCE_GATE_SOFTPLUS_LINEAR && gate_kind != MOCE_GATE_MLP_SIGMOID) return MOCE_ERR_GATE;
+  return gate_kind == MOCE_GATE_SOFTPLUS_LINEAR && moce::fused_runnable(sh) ? MOCE_PATH_FUSED : MOCE_PATH_STAGED;
+}
+
 moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
                          const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y, void* ws,
                          size_t ws_bytes, hipStream_t stream) {
@@ -201,9 +211,11 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
 
   if (gate->kind == MOCE_GATE_SOFTPLUS_LINEAR && moce::fused_eligible(sh)) {
     int* counters = reinterpret_cast<int*>(base + l.counters);
-    const moce::FusedWs fw{d, tau, lse, counters, counters + sh.B, counters + sh.B + 8,
-                           reinterpret_cast<int32_t*>(base + l.plan)};
-    return device_status(moce::launch_fused(sh, x, s, w, *gate, U, nU, y, fw, stream));
+    const moce::FusedWs fw{d, tau, lse, counters, counters + sh.B + 8};
+    bool launched = false;
+    const hipError_t fe = moce::launch_fused(sh, x, s, w, *gate, U, nU, y, fw, stream, &launched);
+    if (fe != hipSuccess) return MOCE_ERR_DEVICE;
+    if (launched) return MOCE_OK;
   }
   hipError_t e = moce::launch_pool(sh, x, d, stream);
   if (e != hipSuccess) return MOCE_ERR_DEVICE;

@@ -75,20 +75,24 @@ hipError_t launch_mix(const Shape& sh, const void* x, const int32_t* s, const fl
 
 // Fused NCHW bf16 forward (fused.hip).  Workspace regions it needs:
 struct FusedWs {
-  float* d;        // [B][C]
-  float* tau;      // [B][R]
-  float* lse;      // [B][R]
-  int* pool_done;  // [B]
-  int* tickets;    // [8]
-  int* err;        // [1]
-  int32_t* plan;   // fused_plan_bytes(sh) bytes
+  float* part;   // [B][C][nt rounded up to 4] per-tile channel sums
+  float* tau;    // [B][R]
+  float* lse;    // [B][R]
+  int* arrive;   // [B] tiles whose channel sums are published
+  int* err;      // [1]
 };
-// Whether the shape runs on the fused kernel (otherwise the staged path).
+// Whether the shape can run on the fused kernel (otherwise the staged path).
 bool fused_eligible(const Shape& sh);
 size_t fused_lds_bytes(const Shape& sh);
-size_t fused_plan_bytes(const Shape& sh);
+// fused_eligible, and the current device holds enough workgroups at once.
+bool fused_runnable(const Shape& sh);
+// Floats of per-tile channel sums the fused kernel publishes.
+size_t fused_partial_floats(const Shape& sh);
+// Enqueues the fused forward; *launched is false (and nothing is enqueued)
+// when the device cannot hold enough workgroups at once, and the caller then
+// takes the staged path.
 hipError_t launch_fused(const Shape& sh, const void* x, const int32_t* s, const float* w,
                         const moce_gate_params& g, const int32_t* U, int nU, void* y, const FusedWs& ws,
-                        hipStream_t st);
+                        hipStream_t st, bool* launched);
 
 }  // namespace moce
