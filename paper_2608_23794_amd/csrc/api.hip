@@ -209,13 +209,20 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
   float* lse = reinterpret_cast<float*>(base + l.lse);
   float* alpha = sh.layout == MOCE_NCHW ? reinterpret_cast<float*>(base + l.alpha) : nullptr;
 
-  if (gate->kind == MOCE_GATE_SOFTPLUS_LINEAR && moce::fused_eligible(sh)) {
+  if (gate->kind == MOCE_GATE_SOFTPLUS_LINEAR && moce::fused_runnable(sh)) {
+    // pooling reads x plane by plane (the order HBM serves best) and leaves it
+    // in the infinity cache; the gate kernel writes tau and lse; the tile
+    // kernel then mixes, reading x back from the cache
     int* counters = reinterpret_cast<int*>(base + l.counters);
     const moce::FusedWs fw{d, tau, lse, counters, counters + sh.B + 8};
+    hipError_t e = moce::launch_pool(sh, x, d, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    e = moce::launch_gate(sh, d, s, w, *gate, tau, nullptr, lse, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
     bool launched = false;
-    const hipError_t fe = moce::launch_fused(sh, x, s, w, *gate, U, nU, y, fw, stream, &launched);
-    if (fe != hipSuccess) return MOCE_ERR_DEVICE;
-    if (launched) return MOCE_OK;
+    e = moce::launch_fused(sh, x, s, w, *gate, U, nU, y, fw, true, stream, &launched);
+    if (e != hipSuccess || !launched) return MOCE_ERR_DEVICE;
+    return MOCE_OK;
   }
   hipError_t e = moce::launch_pool(sh, x, d, stream);
   if (e != hipSuccess) return MOCE_ERR_DEVICE;

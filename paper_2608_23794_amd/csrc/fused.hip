@@ -77,6 +77,7 @@ struct FusedArgs {
   int ntp;                        // nt rounded up to a multiple of 4: row length of the channel sums
   int gsz, epl;                   // gate lanes per expert (a power of two, 8 to 64), entries per lane
   int ng;                         // gate service workgroups (the last ng of the grid)
+  int gated;                      // tau and lse are final on entry: no channel sums, no gate service
 };
 
 // LDS regions, in bytes: the tile [C][kTT] float; the coefficients [R][kq]
@@ -467,12 +468,14 @@ k_fused_nchw(FusedArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__
   auto step = [&](int n, uint4* nxt, uint4* spare) -> bool {
     const int b = n / p.nt, j = n - (n / p.nt) * p.nt;
     const int n1 = n + G, n2 = n + 2 * G;
-    if (n1 < p.ntiles) publish_tile(n1, nxt);
-    // every wave has issued its channel sums of n + G: count the tile (no
-    // return value, so nothing waits for it)
-    __syncthreads();
-    if (n1 < p.ntiles && threadIdx.x == 0)
-      __hip_atomic_fetch_add(arrive + n1 / p.nt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (!p.gated) {
+      if (n1 < p.ntiles) publish_tile(n1, nxt);
+      // every wave has issued its channel sums of n + G: count the tile (no
+      // return value, so nothing waits for it)
+      __syncthreads();
+      if (n1 < p.ntiles && threadIdx.x == 0)
+        __hip_atomic_fetch_add(arrive + n1 / p.nt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
     // one lane waits for the image's gate (on the last value the service
     // publishes, with long pauses, to keep the polling traffic small); then
     // every lane reads its own two values, which are normally there already
@@ -550,10 +553,11 @@ k_fused_nchw(FusedArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__
   uint4 bufa[4], bufb[4];
   issue_tile(p, x, n, bufa);
   if (n + G < p.ntiles) issue_tile(p, x, n + G, bufb);
-  publish_tile(n, bufa);
+  if (!p.gated) publish_tile(n, bufa);
   store_tile(bufa);
   __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(arrive + n / p.nt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  if (!p.gated && threadIdx.x == 0)
+    __hip_atomic_fetch_add(arrive + n / p.nt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   // two steps per trip, so that the two register buffers trade roles
   // without being copied
   for (;;) {
@@ -648,9 +652,10 @@ bool fused_runnable(const Shape& sh) {
 
 hipError_t launch_fused(const Shape& sh, const void* x, const int32_t* s, const float* w,
                         const moce_gate_params& g, const int32_t* U, int nU, void* y, const FusedWs& ws,
-                        hipStream_t st, bool* launched) {
+                        bool gated, hipStream_t st, bool* launched) {
   *launched = false;
   FusedArgs p;
+  p.gated = gated ? 1 : 0;
   p.B = (int)sh.B;
   p.C = (int)sh.C;
   p.HW = (int)sh.HW;
@@ -667,18 +672,21 @@ hipError_t launch_fused(const Shape& sh, const void* x, const int32_t* s, const 
 
   const size_t lds = fused_lds_bytes(sh);
   const int resident = resident_workgroups(sh, lds);
-  p.ng = (int)std::min<int64_t>(sh.B, kGateWorkgroups);
+  p.ng = gated ? 0 : (int)std::min<int64_t>(sh.B, kGateWorkgroups);
   const int mixers = std::min(resident - p.ng, p.ntiles);
   // every tile of an image must be held by a different resident workgroup
   if (mixers <= 0 || (mixers < p.nt && mixers < p.ntiles)) return hipSuccess;
   const int grid = mixers + p.ng;
 
-  const int64_t work = std::max<int64_t>((int64_t)p.B * p.C * p.ntp, sh.B * sh.R);
-  const int64_t fill_blocks = std::min<int64_t>(std::max<int64_t>((work + 255) / 256, 1), 1024);
-  hipLaunchKernelGGL(k_fused_fill, dim3((unsigned)fill_blocks), dim3(256), 0, st, p, ws.part, ws.tau, ws.lse,
-                     ws.arrive, ws.err);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  if (!gated) {
+    const int64_t work = std::max<int64_t>((int64_t)p.B * p.C * p.ntp, sh.B * sh.R);
+    const int64_t fill_blocks = std::min<int64_t>(std::max<int64_t>((work + 255) / 256, 1), 1024);
+    hipLaunchKernelGGL(k_fused_fill, dim3((unsigned)fill_blocks), dim3(256), 0, st, p, ws.part, ws.tau, ws.lse,
+                       ws.arrive, ws.err);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
 
   FusedKernel kern = pick_kernel(sh);
   const uint16_t* xp = static_cast<const uint16_t*>(x);
@@ -691,8 +699,16 @@ hipError_t launch_fused(const Shape& sh, const void* x, const int32_t* s, const 
   const float* ga = g.a;
   const float* gc = g.c;
   void* args[] = {&p, &xp, &yp, &part, &tau, &lse, &arrive, &err, &s, &w, &ga, &gc, &U};
-  e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3((unsigned)grid), dim3(kThreads), args,
-                                 (unsigned)lds, st);
+  if (gated) {
+    // no workgroup waits for another: an ordinary launch (a cooperative one
+    // costs several microseconds on each side)
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, st, p, xp, yp, part, tau, lse, arrive, err,
+                       s, w, ga, gc, U);
+    e = hipGetLastError();
+  } else {
+    e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3((unsigned)grid), dim3(kThreads), args,
+                                   (unsigned)lds, st);
+  }
   if (e == hipSuccess) *launched = true;
   return e;
 }

@@ -91,8 +91,10 @@ size_t fused_partial_floats(const Shape& sh);
 // Enqueues the fused forward; *launched is false (and nothing is enqueued)
 // when the device cannot hold enough workgroups at once, and the caller then
 // takes the staged path.
+// With gated, tau and lse in ws are final on entry (written by the gate
+// kernel) and the kernel only mixes.
 hipError_t launch_fused(const Shape& sh, const void* x, const int32_t* s, const float* w,
                         const moce_gate_params& g, const int32_t* U, int nU, void* y, const FusedWs& ws,
-                        hipStream_t st, bool* launched);
+                        bool gated, hipStream_t st, bool* launched);
 
 }  // namespace moce

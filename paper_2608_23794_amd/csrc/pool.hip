@@ -49,6 +49,34 @@ k_pool_nchw(const T* __restrict__ x, float* __restrict__ d, int64_t planes, int 
   }
 }
 
+// Planes whose length is a whole number of 16-byte vectors (so every plane
+// starts 16-byte aligned): one wave per plane, each lane issuing all U of its
+// loads of a batch (clamped to the plane) before it adds any of them, so that
+// a wave keeps U KB in flight.
+template <typename T, int U>
+__global__ void __launch_bounds__(256)
+k_pool_planes(const T* __restrict__ x, float* __restrict__ d, int64_t planes, int HW) {
+  constexpr int EPV = 16 / sizeof(T);
+  const int lane = threadIdx.x & 63;
+  const int nvec = HW / EPV;
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t pl = wave; pl < planes; pl += nwaves) {
+    const uint4* vb = reinterpret_cast<const uint4*>(x + pl * HW);
+    float sum = 0.f;
+    for (int v0 = 0; v0 < nvec; v0 += U * 64) {
+      uint4 buf[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) buf[u] = vb[min(v0 + u * 64 + lane, nvec - 1)];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (v0 + u * 64 + lane < nvec) sum += sum16<T>(buf[u]);
+    }
+    sum = wave_sum<64>(sum);
+    if (lane == 0) d[pl] = sum / (float)HW;
+  }
+}
+
 // grid B * nblk (nblk = ceil(vectors per row / 64)), block 256.  EPV channels per lane.
 template <typename T, int EPV>
 __global__ void __launch_bounds__(256)
@@ -99,6 +127,14 @@ hipError_t pool_nchw(const Shape& sh, const T* x, float* d, hipStream_t st) {
   constexpr int EPV = 16 / sizeof(T);
   const int64_t planes = sh.B * sh.C;
   const int64_t nvec = sh.HW / EPV;
+  if (sh.HW % EPV == 0 && nvec >= 256) {
+    // long aligned planes: a wave per plane with 8 loads per lane in flight,
+    // as many workgroups as planes need, at most 8 per CU and round
+    int64_t blocks = (planes + 3) / 4;
+    if (blocks > 2048) blocks = 2048;
+    hipLaunchKernelGGL((k_pool_planes<T, 8>), dim3(blocks), dim3(256), 0, st, x, d, planes, (int)sh.HW);
+    return hipGetLastError();
+  }
   int L = nvec >= 128 ? 64 : nvec >= 48 ? 32 : nvec >= 16 ? 16 : 8;
   const int64_t groups_per_block = 256 / L;
   int64_t blocks = (planes + groups_per_block - 1) / groups_per_block;
