@@ -143,13 +143,14 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
 size_t moce_forward_workspace_bytes(const moce_desc* desc);
 
 /* Paths moce_forward can take. */
-enum { MOCE_PATH_STAGED = 0, MOCE_PATH_FUSED = 1 };
+enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1 };
 
-/* The path moce_forward takes for `desc` and gate kind `gate_kind` on the
- * current device: MOCE_PATH_FUSED, the single-pass kernel (NCHW bfloat16,
- * C <= 256, H*W a multiple of 8 and at least 128, softplus-linear gate), or
- * MOCE_PATH_STAGED, the pool, gate and mix kernels in turn.  Both compute the
- * same values.  A negative moce_status for an invalid descriptor or gate kind. */
+/* The path moce_forward (and moce_mix) takes for `desc`: MOCE_PATH_TILE, the
+ * tile kernel (NCHW bfloat16, C <= 256, H*W a multiple of 8) after plane-wise
+ * pooling and the gate, or MOCE_PATH_GENERIC, the layout- and type-generic
+ * kernels.  Both compute the same values.  `gate_kind` must be a valid gate
+ * kind; it does not change the path.  A negative moce_status for an invalid
+ * descriptor or gate kind. */
 int moce_forward_path(const moce_desc* desc, int gate_kind);
 
 /* The whole layer (Secs. 3.3-3.4): pooling, temperatures, mixing

@@ -64,27 +64,20 @@ moce_status device_status(hipError_t e) { return e == hipSuccess ? MOCE_OK : MOC
 
 size_t elem_bytes(const Shape& sh) { return sh.elem == MOCE_F32 ? 4 : 2; }
 
-// Forward workspace: d [B][C] (on the fused path the per-tile channel sums
-// [B][C][nt rounded up to 4] instead), tau [B][R], lse [B][R], counters (per-image tile counts
-// [B], 8 spare words, an error word), and for NCHW the coefficients
-// alpha [B][R][k] of the staged path; every region starts on a 256-byte
-// boundary.
+// Forward workspace: d [B][C], tau [B][R], lse [B][R], and for NCHW the
+// coefficients alpha [B][R][k]; every region starts on a 256-byte boundary.
 struct WsLayout {
-  size_t d, tau, lse, counters, alpha, total;
+  size_t d, tau, lse, alpha, total;
 };
 WsLayout ws_layout(const Shape& sh) {
   WsLayout l{};
   size_t off = 0;
   l.d = off;
-  size_t d_floats = (size_t)sh.B * sh.C;
-  if (moce::fused_eligible(sh)) d_floats = std::max(d_floats, moce::fused_partial_floats(sh));
-  off += round_up(d_floats * sizeof(float));
+  off += round_up((size_t)sh.B * sh.C * sizeof(float));
   l.tau = off;
   off += round_up((size_t)sh.B * sh.R * sizeof(float));
   l.lse = off;
   off += round_up((size_t)sh.B * sh.R * sizeof(float));
-  l.counters = off;
-  off += round_up((size_t)(sh.B + 8 + 1) * sizeof(int));
   l.alpha = off;
   if (sh.layout == MOCE_NCHW) off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
   l.total = off;
@@ -169,6 +162,8 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
   if (nU < 0 || (int64_t)nU > sh.C) return MOCE_ERR_SHAPE;
   if (nU > 0 && !U) return MOCE_ERR_NULL;
   if (!aligned(x, 16) || !aligned(y, 16)) return MOCE_ERR_ALIGN;
+  if (sh.R > 0 && moce::tilemix_eligible(sh))
+    return device_status(moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream));
   return device_status(moce::launch_mix(sh, x, s, alpha, nullptr, nullptr, nullptr, U, nU, y, stream));
 }
 
@@ -183,7 +178,7 @@ int moce_forward_path(const moce_desc* desc, int gate_kind) {
   const moce_status st = check_desc(desc, &sh);
   if (st != MOCE_OK) return st;
   if (gate_kind != MOCE_GATE_SOFTPLUS_LINEAR && gate_kind != MOCE_GATE_MLP_SIGMOID) return MOCE_ERR_GATE;
-  return gate_kind == MOCE_GATE_SOFTPLUS_LINEAR && moce::fused_runnable(sh) ? MOCE_PATH_FUSED : MOCE_PATH_STAGED;
+  return sh.R > 0 && moce::tilemix_eligible(sh) ? MOCE_PATH_TILE : MOCE_PATH_GENERIC;
 }
 
 moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
@@ -209,20 +204,15 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
   float* lse = reinterpret_cast<float*>(base + l.lse);
   float* alpha = sh.layout == MOCE_NCHW ? reinterpret_cast<float*>(base + l.alpha) : nullptr;
 
-  if (gate->kind == MOCE_GATE_SOFTPLUS_LINEAR && moce::fused_runnable(sh)) {
-    // pooling reads x plane by plane (the order HBM serves best) and leaves it
-    // in the infinity cache; the gate kernel writes tau and lse; the tile
-    // kernel then mixes, reading x back from the cache
-    int* counters = reinterpret_cast<int*>(base + l.counters);
-    const moce::FusedWs fw{d, tau, lse, counters, counters + sh.B + 8};
+  // pooling reads x plane by plane (the order HBM serves best) and leaves it
+  // in the infinity cache; the gate kernel writes tau and the coefficients;
+  // the mix then reads x back from the cache
+  if (sh.R > 0 && moce::tilemix_eligible(sh)) {
     hipError_t e = moce::launch_pool(sh, x, d, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
-    e = moce::launch_gate(sh, d, s, w, *gate, tau, nullptr, lse, stream);
+    e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, nullptr, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
-    bool launched = false;
-    e = moce::launch_fused(sh, x, s, w, *gate, U, nU, y, fw, true, stream, &launched);
-    if (e != hipSuccess || !launched) return MOCE_ERR_DEVICE;
-    return MOCE_OK;
+    return device_status(moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream));
   }
   hipError_t e = moce::launch_pool(sh, x, d, stream);
   if (e != hipSuccess) return MOCE_ERR_DEVICE;

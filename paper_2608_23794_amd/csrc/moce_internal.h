@@ -73,28 +73,11 @@ hipError_t launch_mix(const Shape& sh, const void* x, const int32_t* s, const fl
                       const float* w, const float* tau, const float* lse, const int32_t* U, int nU,
                       void* y, hipStream_t st);
 
-// Fused NCHW bf16 forward (fused.hip).  Workspace regions it needs:
-struct FusedWs {
-  float* part;   // [B][C][nt rounded up to 4] per-tile channel sums
-  float* tau;    // [B][R]
-  float* lse;    // [B][R]
-  int* arrive;   // [B] tiles whose channel sums are published
-  int* err;      // [1]
-};
-// Whether the shape can run on the fused kernel (otherwise the staged path).
-bool fused_eligible(const Shape& sh);
-size_t fused_lds_bytes(const Shape& sh);
-// fused_eligible, and the current device holds enough workgroups at once.
-bool fused_runnable(const Shape& sh);
-// Floats of per-tile channel sums the fused kernel publishes.
-size_t fused_partial_floats(const Shape& sh);
-// Enqueues the fused forward; *launched is false (and nothing is enqueued)
-// when the device cannot hold enough workgroups at once, and the caller then
-// takes the staged path.
-// With gated, tau and lse in ws are final on entry (written by the gate
-// kernel) and the kernel only mixes.
-hipError_t launch_fused(const Shape& sh, const void* x, const int32_t* s, const float* w,
-                        const moce_gate_params& g, const int32_t* U, int nU, void* y, const FusedWs& ws,
-                        bool gated, hipStream_t st, bool* launched);
+// Tile gather-mix for NCHW bfloat16 with C <= 256 (tilemix.hip), from the
+// coefficients alpha [B][R][k].
+bool tilemix_eligible(const Shape& sh);
+size_t tilemix_lds_bytes(const Shape& sh);
+hipError_t launch_tilemix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
+                          int nU, void* y, hipStream_t st);
 
 }  // namespace moce

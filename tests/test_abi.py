@@ -169,20 +169,15 @@ def test_gate_parameter_errors(lib):
 
 
 def test_workspace_size_and_errors(lib):
-    staged = good_desc(dtype=mb.MOCE_F32)
-    # d [2][64] + tau [2][15] + lse [2][15] + counters [2 + 8 + 1] + alpha [2][15][8],
-    # each rounded up to 256 bytes
-    assert lib.moce_forward_workspace_bytes(ctypes.byref(staged)) == 512 + 256 + 256 + 256 + 1024
     desc = good_desc()
     need = lib.moce_forward_workspace_bytes(ctypes.byref(desc))
-    # a shape the single-pass kernel serves: its per-tile channel sums
-    # [2][64][1 tile, rounded up to 4] replace d
-    assert need == 2048 + 256 + 256 + 256 + 1024
+    # d [2][64] + tau [2][15] + lse [2][15] + alpha [2][15][8], each rounded up to 256 bytes
+    assert need == 512 + 256 + 256 + 1024
     gate = mb.make_gate(a=FAKE, c=FAKE)
     assert _call_forward(desc, gate, ws=None) == -7
     assert _call_forward(desc, gate, ws_bytes=need - 1) == -7
     nhwc = good_desc(layout=mb.MOCE_NHWC)
-    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 256 + 256
+    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 256
 
 
 def test_prepare_limits(lib):

@@ -319,46 +319,48 @@ def test_batch_prefix_consistency():
     assert torch.equal(full[:2].view(torch.int16), part.view(torch.int16))
 
 
-# --------------------------------------------------------------------------- fused forward (NCHW bf16)
-
-FUSED = [
-    # B, C, E, k, H, W: shapes served by the single-pass fused kernel
-    (3, 256, 64, 32, 56, 56),    # fewer tiles than resident workgroups
-    (24, 256, 64, 32, 56, 56),   # three rounds of tiles, the last one partial
-    (8, 128, 32, 16, 10, 20),    # two tiles per image, the second ragged (72 positions)
-    (5, 64, 64, 64, 16, 24),     # E = C = k
+# --------------------------------------------------------------------------- tile kernel (NCHW bf16)
+TILED = [
+    # B, C, E, k, H, W: shapes served by the tile kernel
+    (3, 256, 64, 32, 56, 56),    # a few images
+    (24, 256, 64, 32, 56, 56),   # several images per workgroup run
+    (8, 128, 32, 16, 10, 20),    # 200 positions: four tiles, the last ragged (8 positions)
+    (5, 64, 64, 64, 16, 24),     # E = C = k, two expert passes
     (4, 96, 24, 12, 28, 30),     # channels not a multiple of 64, ragged last tile
     (2, 256, 8, 256, 16, 16),    # k = C (runtime support length)
-    (2, 64, 16, 8, 128, 128),    # 128 tiles per image
+    (2, 64, 16, 8, 128, 128),    # 256 tiles per image
+    (3, 200, 200, 4, 8, 8),      # E = C: 199 routed experts, seven passes, one tile per image
+    (2, 64, 2, 5, 8, 8),         # one routed expert, k not a multiple of 4
 ]
 
 
-@pytest.mark.parametrize("B,C,E,k,H,W", FUSED)
-def test_fused_forward_shapes(B, C, E, k, H, W):
+@pytest.mark.parametrize("B,C,E,k,H,W", TILED)
+def test_tile_forward_shapes(B, C, E, k, H, W):
     x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=B + C + E + k + H)
     ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
     layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
-    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_FUSED
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_TILE
     y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
     check_y(y, ref["y"], ref["mag"], "bf16")
 
 
 def test_forward_path_choice():
-    """Shapes outside the fused kernel's limits take the staged path."""
+    """Shapes outside the tile kernel's limits take the generic kernels."""
     def path(B, C, E, k, H, W, dtype="bf16", layout="nchw", gate=mb.MOCE_GATE_SOFTPLUS_LINEAR):
         d = mb.make_desc(B, C, H, W, E, k, mb.MOCE_BF16 if dtype == "bf16" else mb.MOCE_F32,
                          mb.MOCE_NCHW if layout == "nchw" else mb.MOCE_NHWC)
         return mb.moce_forward_path(d, gate)
-    assert path(64, 256, 64, 32, 56, 56) == mb.PATH_FUSED
-    assert path(64, 256, 64, 32, 56, 56, gate=mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_STAGED
-    assert path(2, 64, 16, 8, 8, 8, dtype="f32") == mb.PATH_STAGED
-    assert path(64, 1024, 256, 64, 14, 14, layout="nhwc") == mb.PATH_STAGED
-    assert path(4, 512, 64, 32, 16, 16) == mb.PATH_STAGED       # C > 256
-    assert path(4, 96, 24, 12, 30, 30) == mb.PATH_STAGED        # H*W not a multiple of 8
+    assert path(64, 256, 64, 32, 56, 56) == mb.PATH_TILE
+    assert path(64, 256, 64, 32, 56, 56, gate=mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_TILE
+    assert path(2, 64, 16, 8, 8, 8, dtype="f32") == mb.PATH_GENERIC
+    assert path(64, 1024, 256, 64, 14, 14, layout="nhwc") == mb.PATH_GENERIC
+    assert path(4, 512, 64, 32, 16, 16) == mb.PATH_GENERIC       # C > 256
+    assert path(4, 96, 24, 12, 30, 30) == mb.PATH_GENERIC        # H*W not a multiple of 8
+    assert path(4, 64, 1, 8, 8, 8) == mb.PATH_GENERIC            # no routed expert
 
 
-def test_fused_forward_reused_workspace_sees_new_inputs():
-    """Published descriptors and temperatures of one call never leak into the next."""
+def test_forward_reused_workspace_sees_new_inputs():
+    """Descriptors and coefficients of one call never leak into the next."""
     wl = inputs.WORKLOADS["resnet50_stage1"]
     g = inputs.generate(wl, batch=16)
     layer = MoceLayer.from_workload(wl, g)
