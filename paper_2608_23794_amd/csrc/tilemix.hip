@@ -180,23 +180,45 @@ k_tilemix(TileArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, 
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rkq = p.R * p.kq;
 
-  // byte offsets of the support rows in the LDS tile (padding: row 0)
-  for (int e = threadIdx.x; e < rkq; e += kThreads) {
-    const int o = e / p.kq, i = e - (e / p.kq) * p.kq;
-    const int32_t sv = s[min((int64_t)o * p.k + i, (int64_t)p.R * p.k - 1)];
-    sofs[e] = (uint16_t)((i < p.k ? sv : 0) * kRowBytes);
-  }
-  // coefficients of the first image
-  int cur = t0 / p.nt;
-  for (int e = threadIdx.x; e < rkq; e += kThreads) al[e] = alpha_entry(p, alpha, cur, e);
-
+  // The first two tiles' loads go out first; the support offsets and the
+  // first image's coefficients are then read with all loads issued before
+  // any is used, so the prologue costs about one memory round trip.
   uint4 bufa[4], bufb[4];
   issue_tile(p, x, t0, bufa);
   if (t0 + 1 < t1) issue_tile(p, x, t0 + 1, bufb);
+  int cur = t0 / p.nt;
+  const bool pre = rkq <= kASlots * kThreads;  // a full table fits kASlots values per thread
+  if (pre) {
+    int32_t sv[kASlots];
+    float av[kASlots];
+#pragma unroll
+    for (int q = 0; q < kASlots; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      const int o = e / p.kq, i = e - (e / p.kq) * p.kq;
+      sv[q] = s[min((int64_t)o * p.k + i, (int64_t)p.R * p.k - 1)];
+      av[q] = alpha[min((int64_t)cur * p.R * p.k + (int64_t)o * p.k + i, (int64_t)p.B * p.R * p.k - 1)];
+    }
+#pragma unroll
+    for (int q = 0; q < kASlots; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      const int o = e / p.kq, i = e - (e / p.kq) * p.kq;
+      if (e < rkq) {
+        const bool valid = o < p.R && i < p.k;
+        sofs[e] = (uint16_t)((valid ? sv[q] : 0) * kRowBytes);
+        al[e] = valid ? av[q] : 0.f;
+      }
+    }
+  } else {
+    for (int e = threadIdx.x; e < rkq; e += kThreads) {
+      const int o = e / p.kq, i = e - (e / p.kq) * p.kq;
+      const int32_t sv = s[min((int64_t)o * p.k + i, (int64_t)p.R * p.k - 1)];
+      sofs[e] = (uint16_t)((i < p.k ? sv : 0) * kRowBytes);
+      al[e] = alpha_entry(p, alpha, cur, e);
+    }
+  }
   store_tile(p, bufa, tile);
   __syncthreads();
 
-  const bool pre = rkq <= kASlots * kThreads;  // next image's coefficients fit the registers
   float an[kASlots];
   const int gq = lane >> 4, l4 = lane & 15;
   const char* base = reinterpret_cast<const char*>(tile) + l4 * 16;
