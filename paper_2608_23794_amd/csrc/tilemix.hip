@@ -1,12 +1,8 @@
 // Gather-mix of the routed experts (Eq. 5) and the residual output (Eq. 6)
 // for NCHW bfloat16 inputs with C <= 256, given the coefficients alpha.
 //
-// Tiles.  Image b is cut into nt = ceil(HW / 64) tiles of 64 positions by all
-// C channels.  A 512-thread workgroup holds one tile in LDS, widened to
-// float32, and every routed expert reads its k support rows from there: the
-// gather costs one 16-byte LDS read per support entry and lane (4 positions),
-// so each loaded channel row serves every expert whose support contains it.
-// Two workgroups share a CU (about 77 KB of LDS each).
+// The tile and the expert mix are those of tile_common.h; two workgroups share
+// a CU (about 77 KB of LDS each).
 //
 // Schedule.  Workgroup g of G takes the contiguous run of tiles
 // [g * ntiles / G, (g + 1) * ntiles / G), which mostly lies in one image, so
@@ -19,146 +15,14 @@
 // until the next tile has been written to LDS, and only then are they
 // stored, so that the compiler's wait for the next tile's data counts exactly
 // the operations issued after it and never drains the loads still in flight.
-//
-// Mixing.  Each quarter wave computes one expert (or the residual) for the 64
-// positions of the tile, each lane 4 consecutive positions.  The byte offsets
-// of an expert's support rows are 16-bit values in LDS read four at a time,
-// and so are the coefficients.
 #include <algorithm>
 
-#include "moce_internal.h"
+#include "tile_common.h"
 
 namespace moce {
 namespace {
 
-constexpr int kThreads = 512;
-constexpr int kWaves = kThreads / 64;
-constexpr int kTT = 64;             // positions per tile
-constexpr int kRowBytes = kTT * 4;  // bytes of one channel row of the LDS tile
-constexpr int kPerCU = 2;           // workgroups per CU
-constexpr int kMaxLds = 80 * 1024 - 1024;
-constexpr int kASlots = 4;          // coefficients per thread prefetched in registers
-constexpr int kExpertsPerPass = 4 * kWaves;
-
-struct TileArgs {
-  int B, C, HW, E, R, k, kq, nU;  // kq: k rounded up to a multiple of 4
-  int nt, ntiles;                 // tiles per image, tiles in the batch
-};
-
-// LDS regions in bytes: tile [C][kTT] float, coefficients [R][kq] float,
-// support row offsets [R][kq] uint16.
-struct TileLds {
-  size_t alpha, sofs, total;
-};
-
-__host__ __device__ inline TileLds tile_lds(int C, int R, int kq) {
-  TileLds l;
-  l.alpha = (size_t)C * kTT * 4;
-  l.sofs = l.alpha + (size_t)R * kq * 4;
-  l.total = l.sofs + (((size_t)R * kq * 2 + 15) & ~(size_t)15);
-  return l;
-}
-
-// Issues the global loads of tile n into buf (4 x 16 bytes per thread): thread
-// t reads 8 positions of channel (t >> 3) + 64u in round u.  Every round
-// loads (rows past C repeat row C - 1, positions past the image repeat its
-// last vector), so the loads are straight-line code; the surplus is never
-// written to an output.
-__device__ __forceinline__ void issue_tile(const TileArgs& p, const uint16_t* __restrict__ x, int n, uint4* buf) {
-  const int b = n / p.nt, j = n - (n / p.nt) * p.nt;
-  const int p0 = j * kTT;
-  const int vvalid = min(kTT, p.HW - p0) / 8;
-  const uint16_t* xb = x + (int64_t)b * p.C * p.HW + p0;
-  const int qv = threadIdx.x & 7;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int c = (threadIdx.x >> 3) + u * 64;
-    buf[u] = *reinterpret_cast<const uint4*>(xb + (int64_t)min(c, p.C - 1) * p.HW + min(qv, vvalid - 1) * 8);
-  }
-}
-
-// Widens tile data into the LDS tile (channels < C).
-__device__ __forceinline__ void store_tile(const TileArgs& p, const uint4* buf, float* tile) {
-  const int qv = threadIdx.x & 7;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int c = (threadIdx.x >> 3) + u * 64;
-    if (u * 64 < p.C && c < p.C) {
-      float4* dst = reinterpret_cast<float4*>(tile + c * kTT + qv * 8);
-      dst[0] = make_float4(bf16_lo(buf[u].x), bf16_hi(buf[u].x), bf16_lo(buf[u].y), bf16_hi(buf[u].y));
-      dst[1] = make_float4(bf16_lo(buf[u].z), bf16_hi(buf[u].z), bf16_lo(buf[u].w), bf16_hi(buf[u].w));
-    }
-  }
-}
-
-// Coefficient e of image b in the padded [R][kq] layout (0 for padding),
-// read from alpha [B][R][k].
-__device__ __forceinline__ float alpha_entry(const TileArgs& p, const float* __restrict__ alpha, int b, int e) {
-  const int o = e / p.kq, i = e - (e / p.kq) * p.kq;
-  const int64_t rk = (int64_t)p.R * p.k;
-  const float v = alpha[min((int64_t)b * rk + (int64_t)o * p.k + i, (int64_t)p.B * rk - 1)];
-  return (o < p.R && i < p.k) ? v : 0.f;
-}
-
-// y[o][p0 + 4 l .. +3] of one routed expert from lane l of a quarter wave: K
-// (or kq, when K == 0) support entries, each a 16-byte read of the LDS tile at
-// the entry's 16-bit byte offset plus the lane's own.  Padding entries have
-// coefficient 0 and row 0.
-template <int K>
-__device__ __forceinline__ float4 mix_expert(const uint16_t* ofs, const float* al, const char* base, int kq) {
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  const int n = K > 0 ? K : kq;
-  // the offsets and coefficients of the next four entries are read while the
-  // rows of the current four are in flight (the last step reads its own again)
-  uint2 of = *reinterpret_cast<const uint2*>(ofs);
-  float4 a = *reinterpret_cast<const float4*>(al);
-  auto step4 = [&](int i) {
-    const int inext = min(i + 4, n - 4);
-    const uint2 of_n = *reinterpret_cast<const uint2*>(ofs + inext);
-    const float4 a_n = *reinterpret_cast<const float4*>(al + inext);
-    // keep the two reads above ahead of the row reads below
-    __builtin_amdgcn_sched_barrier(0);
-    const float4 v0 = *reinterpret_cast<const float4*>(base + (of.x & 0xffffu));
-    const float4 v1 = *reinterpret_cast<const float4*>(base + (of.x >> 16));
-    const float4 v2 = *reinterpret_cast<const float4*>(base + (of.y & 0xffffu));
-    const float4 v3 = *reinterpret_cast<const float4*>(base + (of.y >> 16));
-#define MOCE_FMA4(A, V) \
-    acc.x = fmaf(A, V.x, acc.x); acc.y = fmaf(A, V.y, acc.y); acc.z = fmaf(A, V.z, acc.z); acc.w = fmaf(A, V.w, acc.w)
-    MOCE_FMA4(a.x, v0); MOCE_FMA4(a.y, v1); MOCE_FMA4(a.z, v2); MOCE_FMA4(a.w, v3);
-#undef MOCE_FMA4
-    of = of_n;
-    a = a_n;
-  };
-  if constexpr (K > 0) {
-#pragma unroll 2
-    for (int i = 0; i < K; i += 4) step4(i);
-  } else {
-    for (int i = 0; i < n; i += 4) step4(i);
-  }
-  return acc;
-}
-
-// The residual output for lane l of a quarter wave: mean of the tile rows of
-// the uncovered channels U, exactly 0 when U is empty.
-__device__ __forceinline__ float4 residual(const int32_t* __restrict__ U, int nU, const char* base) {
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int u = 0; u < nU; ++u) {
-    const float4 v = *reinterpret_cast<const float4*>(base + U[u] * kRowBytes);
-    acc.x += v.x;
-    acc.y += v.y;
-    acc.z += v.z;
-    acc.w += v.w;
-  }
-  if (nU > 0) {
-    const float n = (float)nU;
-    acc = make_float4(acc.x / n, acc.y / n, acc.z / n, acc.w / n);
-  }
-  return acc;
-}
-
-__device__ __forceinline__ uint2 pack_bf16x4(float4 v) {
-  return make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
-}
+using namespace tile;
 
 // K: kq when fixed (else 0); NP: passes of kExpertsPerPass experts covering
 // the R routed experts and the residual (else 0: a runtime loop).
@@ -296,15 +160,134 @@ k_tilemix(TileArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, 
   }
 }
 
+// Register-resident variant (tile_common.h) for k <= 16 NR and
+// R + 1 <= NP * kExpertsPerPass: the lanes hold the coefficients and support
+// row offsets, and LDS holds only the tile.  Same schedule as k_tilemix; the
+// next image's coefficients are prefetched into registers one step ahead,
+// and padding entries are zeroed where the values are used, not right after
+// the loads.
+template <int NR, int NP>
+__global__ void __launch_bounds__(kThreads, 2 * kPerCU)
+k_tilemix_regs(TileArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, const int32_t* __restrict__ s,
+               const float* __restrict__ alpha, const int32_t* __restrict__ U) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* tile = reinterpret_cast<float*>(smem);  // [C][kTT]
+
+  const int G = gridDim.x;
+  const int t0 = (int)((int64_t)blockIdx.x * p.ntiles / G);
+  const int t1 = (int)((int64_t)(blockIdx.x + 1) * p.ntiles / G);
+  if (t0 >= t1) return;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int gq = lane >> 4, l4 = lane & 15;
+
+  uint4 bufa[4], bufb[4];
+  issue_tile(p, x, t0, bufa);
+  if (t0 + 1 < t1) issue_tile(p, x, t0 + 1, bufb);
+
+  // entry m of pass q: expert 4 wv + q kExpertsPerPass + gq, support position l4 + 16 m
+  int ofs[NP][NR], eoff[NP][NR];
+  uint32_t valid = 0;
+#pragma unroll
+  for (int q = 0; q < NP; ++q)
+#pragma unroll
+    for (int m = 0; m < NR; ++m) {
+      const int o = 4 * wv + q * kExpertsPerPass + gq, i = l4 + kRowLanes * m;
+      const bool v = o < p.R && i < p.k;
+      valid |= (uint32_t)v << (q * NR + m);
+      eoff[q][m] = v ? o * p.k + i : 0;
+      ofs[q][m] = s[eoff[q][m]];
+    }
+  float a[NP][NR], an[NP][NR];
+  auto load_alpha = [&](int b, float (&dst)[NP][NR]) {
+    const float* ab = alpha + (int64_t)b * p.R * p.k;
+#pragma unroll
+    for (int q = 0; q < NP; ++q)
+#pragma unroll
+      for (int m = 0; m < NR; ++m) dst[q][m] = ab[eoff[q][m]];
+  };
+  auto take_alpha = [&]() {
+#pragma unroll
+    for (int q = 0; q < NP; ++q)
+#pragma unroll
+      for (int m = 0; m < NR; ++m) a[q][m] = (valid >> (q * NR + m)) & 1 ? an[q][m] : 0.f;
+  };
+  int cur = t0 / p.nt;
+  load_alpha(cur, an);
+#pragma unroll
+  for (int q = 0; q < NP; ++q)
+#pragma unroll
+    for (int m = 0; m < NR; ++m) ofs[q][m] = (valid >> (q * NR + m)) & 1 ? ofs[q][m] * kRowBytes : 0;
+  take_alpha();
+  store_tile(p, bufa, tile);
+  __syncthreads();
+  const char* base = reinterpret_cast<const char*>(tile) + l4 * 16;
+
+  auto step = [&](int n, uint4* nxt, uint4* spare) {
+    const int b = n / p.nt, j = n - (n / p.nt) * p.nt;
+    const int n1 = n + 1, n2 = n + 2;
+    if (b != cur) {
+      take_alpha();
+      cur = b;
+    }
+    if (n1 < t1 && n1 / p.nt != b) load_alpha(n1 / p.nt, an);
+    if (n2 < t1) issue_tile(p, x, n2, spare);
+
+    const int p0 = j * kTT;
+    const bool store = l4 * 4 < min(kTT, p.HW - p0);  // H*W is a multiple of 8: all four positions or none
+    uint16_t* yb = y + (int64_t)b * p.E * p.HW + p0 + l4 * 4;
+    float4 res[NP];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const int o = 4 * wv + q * kExpertsPerPass + gq;
+      res[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (o < p.R)
+        res[q] = mix_expert_regs<NR>(a[q], ofs[q], base);
+      else if (o == p.R)
+        res[q] = residual(U, p.nU, base);
+    }
+    __syncthreads();  // every wave is done with the LDS tile
+    if (n1 < t1) store_tile(p, nxt, tile);
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const int o = 4 * wv + q * kExpertsPerPass + gq;
+      if (store && o <= p.R) *reinterpret_cast<uint2*>(yb + (int64_t)o * p.HW) = pack_bf16x4(res[q]);
+    }
+    __syncthreads();
+  };
+
+  for (int n = t0;;) {
+    step(n, bufb, bufa);
+    if (++n >= t1) break;
+    step(n, bufa, bufb);
+    if (++n >= t1) break;
+  }
+}
+
 int rounded_k(const Shape& sh) { return (sh.k + 3) & ~3; }
 
 int64_t tiles_per_image(const Shape& sh) { return (sh.HW + kTT - 1) / kTT; }
 
 using TileKernel = void (*)(TileArgs, const uint16_t*, uint16_t*, const int32_t*, const float*, const int32_t*);
 
+int expert_passes(const Shape& sh) { return (sh.R + 1 + kExpertsPerPass - 1) / kExpertsPerPass; }
+
+// register rows per expert for the register-resident kernel, 0 when it does not apply
+int regs_rows(const Shape& sh) {
+  if (sh.k > 4 * kRowLanes || expert_passes(sh) > 2) return 0;
+  return (sh.k + kRowLanes - 1) / kRowLanes;
+}
+
 TileKernel pick_kernel(const Shape& sh) {
+  const int nr = regs_rows(sh), np = expert_passes(sh);
+  if (nr > 0) {
+    static const TileKernel regs[4][2] = {{k_tilemix_regs<1, 1>, k_tilemix_regs<1, 2>},
+                                          {k_tilemix_regs<2, 1>, k_tilemix_regs<2, 2>},
+                                          {k_tilemix_regs<3, 1>, k_tilemix_regs<3, 2>},
+                                          {k_tilemix_regs<4, 1>, k_tilemix_regs<4, 2>}};
+    return regs[nr - 1][np - 1];
+  }
   const int kq = rounded_k(sh);
-  const int np = (sh.R + 1 + kExpertsPerPass - 1) / kExpertsPerPass;
   if (kq == 32 && np == 1) return k_tilemix<32, 1>;
   if (kq == 32 && np == 2) return k_tilemix<32, 2>;
   if (kq == 64 && np == 2) return k_tilemix<64, 2>;
@@ -313,7 +296,10 @@ TileKernel pick_kernel(const Shape& sh) {
 
 }  // namespace
 
-size_t tilemix_lds_bytes(const Shape& sh) { return tile_lds((int)sh.C, sh.R, rounded_k(sh)).total; }
+size_t tilemix_lds_bytes(const Shape& sh) {
+  if (regs_rows(sh) > 0) return (size_t)sh.C * kRowBytes;
+  return tile_lds((int)sh.C, sh.R, rounded_k(sh)).total;
+}
 
 bool tilemix_eligible(const Shape& sh) {
   if (sh.layout != MOCE_NCHW || sh.elem != MOCE_BF16 || sh.R < 1) return false;

@@ -220,6 +220,18 @@ def test_forward_mlp_gate(name, layout):
     check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
 
 
+def test_forward_mlp_gate_tile_path():
+    """The MLP gate on a tile shape: plane-wise pooling, the gate kernel, then the tile kernel."""
+    wl = inputs.WORKLOADS["resnet50_stage1"]
+    g = inputs.generate(wl, batch=5)
+    ref = oracle.forward(g["x"], g["s"], g["w"], wl.E, oracle.NCHW, gate="mlp", W1=g["W1"], b1=g["b1"],
+                         w2=g["w2"], b2=g["b2"], tau_min=g["tau_min"], tau_max=g["tau_max"])
+    layer = MoceLayer.from_workload(wl, g, gate="mlp")
+    assert mb.moce_forward_path(layer.desc(5), mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_TILE
+    y = layer.forward(to_device_x(g["x"], wl.dtype))
+    check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
+
+
 # --------------------------------------------------------------------------- edge cases
 
 def _custom(B, C, E, k, H, W, dtype, layout, seed, signed=False, cyclic=False, s=None, w=None):
