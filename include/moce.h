@@ -143,13 +143,21 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
 size_t moce_forward_workspace_bytes(const moce_desc* desc);
 
 /* Paths moce_forward can take. */
-enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1 };
+enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1, MOCE_PATH_MFMA = 2 };
 
-/* The path moce_forward (and moce_mix) takes for `desc`: MOCE_PATH_TILE, the
- * tile kernel (NCHW bfloat16, C <= 256, H*W a multiple of 8) after plane-wise
- * pooling and the gate, or MOCE_PATH_GENERIC, the layout- and type-generic
- * kernels.  Both compute the same values.  `gate_kind` must be a valid gate
- * kind; it does not change the path.  A negative moce_status for an invalid
+/* The path moce_forward (and moce_mix) takes for `desc`, after plane-wise
+ * pooling and the gate:
+ *  MOCE_PATH_MFMA: the routed and residual outputs of an image as one dense
+ *     bf16 matrix product on the matrix cores, the coefficients split into
+ *     bf16 parts that sum to them exactly (NCHW bfloat16, E-1 >= 1, C a
+ *     multiple of 32 up to 256, E <= 64, H*W a multiple of 8);
+ *  MOCE_PATH_TILE: the tile gather kernel (NCHW bfloat16, C <= 256, H*W a
+ *     multiple of 8);
+ *  MOCE_PATH_GENERIC: the layout- and type-generic kernels.
+ * All compute the same values up to float32 rounding order; the MFMA path
+ * requires distinct channels within each support row, as
+ * moce_support_prepare guarantees.  `gate_kind` must be a valid gate kind;
+ * it does not change the path.  A negative moce_status for an invalid
  * descriptor or gate kind. */
 int moce_forward_path(const moce_desc* desc, int gate_kind);
 

@@ -156,11 +156,11 @@ def moce_forward_workspace_bytes(desc: moce_desc) -> int:
     return int(load().moce_forward_workspace_bytes(ctypes.byref(desc)))
 
 
-PATH_GENERIC, PATH_TILE = 0, 1
+PATH_GENERIC, PATH_TILE, PATH_MFMA = 0, 1, 2
 
 
 def moce_forward_path(desc: moce_desc, gate_kind: int) -> int:
-    """PATH_TILE or PATH_GENERIC: the kernels moce_forward and moce_mix use for desc."""
+    """PATH_MFMA, PATH_TILE or PATH_GENERIC: the kernels moce_forward and moce_mix use for desc."""
     r = int(load().moce_forward_path(ctypes.byref(desc), gate_kind))
     if r < 0:
         raise MoceError("moce_forward_path", r)

@@ -14,7 +14,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["api.hip", "prepare.hip", "pool.hip", "gate.hip", "mix.hip", "tilemix.hip"]
+SOURCES = ["api.hip", "prepare.hip", "pool.hip", "gate.hip", "mix.hip", "tilemix.hip", "mfmamix.hip"]
 LIB = os.path.join(HERE, "libmoce.so")
 OBJDIR = os.path.join(HERE, "_build")
 

@@ -162,6 +162,8 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
   if (nU < 0 || (int64_t)nU > sh.C) return MOCE_ERR_SHAPE;
   if (nU > 0 && !U) return MOCE_ERR_NULL;
   if (!aligned(x, 16) || !aligned(y, 16)) return MOCE_ERR_ALIGN;
+  if (moce::mfmamix_eligible(sh))
+    return device_status(moce::launch_mfmamix(sh, x, s, alpha, U, nU, y, stream));
   if (sh.R > 0 && moce::tilemix_eligible(sh))
     return device_status(moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream));
   return device_status(moce::launch_mix(sh, x, s, alpha, nullptr, nullptr, nullptr, U, nU, y, stream));
@@ -178,6 +180,7 @@ int moce_forward_path(const moce_desc* desc, int gate_kind) {
   const moce_status st = check_desc(desc, &sh);
   if (st != MOCE_OK) return st;
   if (gate_kind != MOCE_GATE_SOFTPLUS_LINEAR && gate_kind != MOCE_GATE_MLP_SIGMOID) return MOCE_ERR_GATE;
+  if (moce::mfmamix_eligible(sh)) return MOCE_PATH_MFMA;
   return sh.R > 0 && moce::tilemix_eligible(sh) ? MOCE_PATH_TILE : MOCE_PATH_GENERIC;
 }
 
@@ -207,6 +210,13 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
   // pooling reads x plane by plane (the order HBM serves best) and leaves it
   // in the infinity cache; the gate kernel writes tau and the coefficients;
   // the mix then reads x back from the cache
+  if (moce::mfmamix_eligible(sh)) {
+    hipError_t e = moce::launch_pool(sh, x, d, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, nullptr, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    return device_status(moce::launch_mfmamix(sh, x, s, alpha, U, nU, y, stream));
+  }
   if (sh.R > 0 && moce::tilemix_eligible(sh)) {
     hipError_t e = moce::launch_pool(sh, x, d, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;

@@ -80,4 +80,11 @@ size_t tilemix_lds_bytes(const Shape& sh);
 hipError_t launch_tilemix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
                           int nU, void* y, hipStream_t st);
 
+// Mixing as a dense bf16 product on the matrix cores (mfmamix.hip), for NCHW
+// bfloat16 with R >= 1, C a multiple of 32 up to 256, E <= 64 and H*W a
+// multiple of 8; supports must hold distinct channels (prepared rows).
+bool mfmamix_eligible(const Shape& sh);
+hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
+                          int nU, void* y, hipStream_t st);
+
 }  // namespace moce

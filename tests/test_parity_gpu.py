@@ -220,14 +220,14 @@ def test_forward_mlp_gate(name, layout):
     check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
 
 
-def test_forward_mlp_gate_tile_path():
-    """The MLP gate on a tile shape: plane-wise pooling, the gate kernel, then the tile kernel."""
+def test_forward_mlp_gate_mfma_path():
+    """The MLP gate on the stage-1 shape: plane-wise pooling, the gate kernel, then the MFMA mix."""
     wl = inputs.WORKLOADS["resnet50_stage1"]
     g = inputs.generate(wl, batch=5)
     ref = oracle.forward(g["x"], g["s"], g["w"], wl.E, oracle.NCHW, gate="mlp", W1=g["W1"], b1=g["b1"],
                          w2=g["w2"], b2=g["b2"], tau_min=g["tau_min"], tau_max=g["tau_max"])
     layer = MoceLayer.from_workload(wl, g, gate="mlp")
-    assert mb.moce_forward_path(layer.desc(5), mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_TILE
+    assert mb.moce_forward_path(layer.desc(5), mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_MFMA
     y = layer.forward(to_device_x(g["x"], wl.dtype))
     check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
 
@@ -331,18 +331,83 @@ def test_batch_prefix_consistency():
     assert torch.equal(full[:2].view(torch.int16), part.view(torch.int16))
 
 
+# --------------------------------------------------------------------------- MFMA mix (NCHW bf16)
+MFMA = [
+    # B, C, E, k, H, W: shapes served by the dense matrix-core mix
+    (3, 256, 64, 32, 56, 56),    # a few images
+    (24, 256, 64, 32, 56, 56),   # several images per workgroup range (rebuilds of A_b mid-range)
+    (8, 128, 32, 16, 10, 20),    # 200 positions: four tiles, the last ragged (8 positions); E = 32
+    (5, 64, 64, 64, 16, 24),     # E = C = k
+    (4, 96, 24, 12, 28, 30),     # three load rounds, ragged last tile, half the expert waves idle
+    (2, 256, 8, 256, 16, 16),    # k = C
+    (2, 64, 16, 8, 128, 128),    # 256 tiles per image
+    (2, 64, 2, 5, 8, 8),         # one routed expert, k not a multiple of 4
+    (3, 256, 64, 64, 8, 8),      # R k = 4032 coefficients: more than the register prefetch holds
+    (2, 32, 32, 3, 4, 6),        # C = 32 (one load round), fewer tiles than CUs
+    (2, 64, 40, 3, 4, 6),        # E above 32: the second expert half partly filled
+    (1, 160, 40, 20, 2, 4),      # eight positions in a single partial tile
+    (2, 192, 48, 9, 7, 8),
+    (3, 224, 20, 30, 6, 12),
+]
+
+
+@pytest.mark.parametrize("B,C,E,k,H,W", MFMA)
+def test_mfma_forward_shapes(B, C, E, k, H, W):
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=B + C + E + k + H, signed=(C % 64 == 32))
+    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_MFMA
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    check_y(y, ref["y"], ref["mag"], "bf16")
+    res = y[:, E - 1]
+    if ref["nU"] == 0:
+        assert np.all(res == 0.0)
+
+
+def test_mfma_residual_only_uncovered():
+    """Cyclic supports that leave exactly the top channels uncovered: the residual row is their mean."""
+    B, C, E, k, H, W = 2, 64, 9, 6, 8, 8
+    s = np.array([[(e * k + j) % 48 for j in range(k)] for e in range(E - 1)], np.int32)
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=5, s=s)
+    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
+    assert ref["nU"] == 16
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_MFMA
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    check_y(y, ref["y"], ref["mag"], "bf16")
+
+
+def test_mfma_exact_copies():
+    """k = 1 and the one-hot limit give coefficients of exactly 1: the routed outputs are copies of
+    channels, bit for bit, through the split-coefficient products."""
+    B, C, E, H, W = 2, 64, 12, 8, 8
+    x, s, w, a, c = _custom(B, C, E, 1, H, W, "bf16", "nchw", seed=91, signed=True)
+    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
+    layer = MoceLayer(C, E, 1, H, W, "bf16", "nchw", s, w, a=a, c=c)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_MFMA
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    assert np.array_equal(y[:, :E - 1], ref["y"][:, :E - 1])
+    k = 6
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=77, signed=True)
+    w[:, 0] = w.max(axis=1) + 1.0
+    a[:] = 0.0
+    c[:] = -1e4
+    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    assert np.array_equal(y[:, :E - 1], ref["y"][:, :E - 1])
+
+
 # --------------------------------------------------------------------------- tile kernel (NCHW bf16)
 TILED = [
-    # B, C, E, k, H, W: shapes served by the tile kernel
-    (3, 256, 64, 32, 56, 56),    # a few images
-    (24, 256, 64, 32, 56, 56),   # several images per workgroup run
-    (8, 128, 32, 16, 10, 20),    # 200 positions: four tiles, the last ragged (8 positions)
-    (5, 64, 64, 64, 16, 24),     # E = C = k, two expert passes
-    (4, 96, 24, 12, 28, 30),     # channels not a multiple of 64, ragged last tile
-    (2, 256, 8, 256, 16, 16),    # k = C (runtime support length)
-    (2, 64, 16, 8, 128, 128),    # 256 tiles per image
+    # B, C, E, k, H, W: shapes served by the tile gather kernel (C not a multiple of 32 or E > 64)
     (3, 200, 200, 4, 8, 8),      # E = C: 199 routed experts, seven passes, one tile per image
-    (2, 64, 2, 5, 8, 8),         # one routed expert, k not a multiple of 4
+    (3, 240, 64, 32, 56, 56),    # stage-1 sized, C not a multiple of 32
+    (8, 120, 32, 16, 10, 20),    # 200 positions: four tiles, the last ragged (8 positions)
+    (5, 80, 80, 64, 16, 24),     # E = C, two expert passes
+    (4, 88, 24, 12, 28, 30),     # ragged last tile
+    (2, 256, 96, 16, 16, 16),    # E above the MFMA path's 64
+    (2, 48, 2, 5, 8, 8),         # one routed expert, k not a multiple of 4
 ]
 
 
@@ -357,13 +422,15 @@ def test_tile_forward_shapes(B, C, E, k, H, W):
 
 
 def test_forward_path_choice():
-    """Shapes outside the tile kernel's limits take the generic kernels."""
+    """The MFMA mix where its limits allow, then the tile kernel, then the generic kernels."""
     def path(B, C, E, k, H, W, dtype="bf16", layout="nchw", gate=mb.MOCE_GATE_SOFTPLUS_LINEAR):
         d = mb.make_desc(B, C, H, W, E, k, mb.MOCE_BF16 if dtype == "bf16" else mb.MOCE_F32,
                          mb.MOCE_NCHW if layout == "nchw" else mb.MOCE_NHWC)
         return mb.moce_forward_path(d, gate)
-    assert path(64, 256, 64, 32, 56, 56) == mb.PATH_TILE
-    assert path(64, 256, 64, 32, 56, 56, gate=mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_TILE
+    assert path(64, 256, 64, 32, 56, 56) == mb.PATH_MFMA
+    assert path(64, 256, 64, 32, 56, 56, gate=mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_MFMA
+    assert path(4, 240, 64, 32, 16, 16) == mb.PATH_TILE          # C not a multiple of 32
+    assert path(4, 256, 65, 32, 16, 16) == mb.PATH_TILE          # E > 64
     assert path(2, 64, 16, 8, 8, 8, dtype="f32") == mb.PATH_GENERIC
     assert path(64, 1024, 256, 64, 14, 14, layout="nhwc") == mb.PATH_GENERIC
     assert path(4, 512, 64, 32, 16, 16) == mb.PATH_GENERIC       # C > 256
