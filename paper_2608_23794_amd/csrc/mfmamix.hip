@@ -8,22 +8,26 @@
 // C entries per row (1/8 for the ResNet-50 stage-1 layer), but the matrix
 // cores multiply a dense bf16 tile far faster than the vector ALUs run the
 // gather-and-FMA form, so the kernel builds A_b densely and evaluates
-// y^T = x^T A_b^T with 32x32x16 bf16 MFMAs, which leaves it bound by HBM.
+// y^T = x^T A_b^T with 16x16x32 bf16 MFMAs, which leaves it bound by memory.
 //
 // Exactness.  x is bf16 already.  Each float32 coefficient is split into bf16
 // parts hi + mid + lo that sum to it exactly, one MFMA per part: bf16 x bf16
 // products are exact in float32 and the MFMA accumulates in float32, so the
 // result is the float32 gather form up to the order of the additions.
 //
-// Work split.  A workgroup of 4 waves occupies one CU and walks a contiguous
-// range of tiles (64 positions x all C channels of one image).  Wave w
-// computes positions 32 (w & 1) .. +31 of the tile for experts 32 (w >> 1) ..
-// +31.  Each wave holds its 32 rows of A_b (all channels, every part) in
-// registers as MFMA B operands, rebuilt when the image changes; the x tile is
-// held in LDS as bf16 and read as MFMA A operands with the transposing LDS
-// read, which turns the position-contiguous rows into channel-contiguous
-// operands.  Three tiles are in flight in registers while one is multiplied.
+// Work split.  Two workgroups of 4 waves share a CU, so that one multiplies
+// while the other loads, stores and synchronises.  A workgroup walks a
+// contiguous range of tiles (64 positions x all C channels of one image);
+// wave w computes experts 16 w .. 16 w + 15 at all 64 positions.  Each wave
+// holds its 16 rows of A_b (all channels, every part) in registers as MFMA B
+// operands, rebuilt when the image changes.  The x tile is held in LDS as
+// bf16, double-buffered, and read as MFMA A operands with the transposing LDS
+// read, which turns position-contiguous channel rows into channel-contiguous
+// operands.  A_b is assembled in whichever tile buffer is free at that moment.
+// Results leave through a small per-wave LDS area so that every store
+// instruction writes whole 128-byte rows of y.
 #include <algorithm>
+#include <type_traits>
 
 #include "moce_internal.h"
 
@@ -32,32 +36,47 @@ namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
-typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 #define MOCE_LDS __attribute__((address_space(3)))
 
 constexpr int kThreads = 256;
-constexpr int kTile = 64;          // positions per tile
-constexpr int kRow = kTile * 2;    // bytes of one channel row of an LDS tile
-constexpr int kMaxE = 64;          // rows of A_b
+constexpr int kTile = 64;               // positions per tile
+constexpr int kRow = kTile * 2;         // bytes of one channel row of an LDS tile
+constexpr int kMaxE = 64;               // rows of A_b
 constexpr int kMaxC = 256;
-constexpr int kPre = 8;            // coefficient entries per thread fetched into registers
+constexpr int kPre = 8;                 // coefficient entries per thread fetched into registers
+constexpr int kExpertsPerWave = 16;
+constexpr int kOutRow = kRow + 16;      // bytes per row of a wave's output area (padded)
+constexpr int kOutWave = kExpertsPerWave * kOutRow;
+// s_waitcnt operand waiting for every vector memory access (vmcnt 0, the
+// LDS/scalar and export counters left at their maxima)
+constexpr int kVmDrain = 0x0f70;
 
 struct MixArgs {
   int C, HW, E, R, k, nU, nt, ntiles;
 };
 
-// LDS: two x tiles [C][kTile] bf16, then the staging rows of A_b
-// [kMaxE][C + 8] bf16 (the 8-element pad spreads the rows over the banks).
-__host__ __device__ inline int stage_row(int C) { return C + 8; }
-__host__ __device__ inline size_t mfma_lds(int C) {
-  return (size_t)2 * C * kRow + (size_t)kMaxE * stage_row(C) * 2;
-}
+// LDS: two x tiles [C][kTile] bf16, then the four waves' output areas.
+__host__ __device__ inline size_t mfma_lds(int C) { return (size_t)2 * C * kRow + (size_t)4 * kOutWave; }
 
-// Chunk q (16 bytes = 8 positions) of channel row c is stored at chunk
-// q ^ swz(c), so that the 8 rows x 64 bytes one transposing read touches
-// fall evenly on the LDS banks.
-__device__ __forceinline__ int swz(int c) { return ((c >> 1) & 1) << 2; }
+// Chunk q (16 bytes = 8 positions) of channel row c of a tile is stored at
+// chunk q ^ (2 ((c >> 3) & 3)): the 16 rows x 32 bytes that one transposing
+// read touches then fall on the LDS banks two deep, the least possible.
+__device__ __forceinline__ int tile_swz(int c) { return ((c >> 3) & 3) << 1; }
+
+// Byte offset of A_b[o][c] in the staging area [kMaxE][C] bf16, whose 16-byte
+// chunks are rotated by 4 (o & 3) within the row so that the operand reads
+// (16 rows x 64 bytes) spread over the banks.
+__device__ __forceinline__ int stage_off(int o, int c, int C) {
+  const int nch = C >> 3;
+  int ch = (c >> 3) + 4 * (o & 3);
+  ch = ch >= nch ? ch - nch : ch;
+  ch = ch >= nch ? ch - nch : ch;
+  ch = ch >= nch ? ch - nch : ch;
+  return o * C * 2 + ch * 16 + (c & 7) * 2;
+}
 
 // Global loads of tile n (NR rounds of 16 bytes per thread): thread t reads
 // positions 8 (t & 7) .. +7 of channel (t >> 3) + 32 u.  Positions past the
@@ -73,10 +92,11 @@ __device__ __forceinline__ void load_tile(const MixArgs& p, const uint16_t* __re
   for (int u = 0; u < NR; ++u) buf[u] = *reinterpret_cast<const u32x4*>(src + (int64_t)u * 32 * p.HW);
 }
 
+// Thread t's chunks go to rows (t >> 3) + 32 u: one wave writes 8 whole rows.
 template <int NR>
 __device__ __forceinline__ void store_tile(const u32x4 (&buf)[NR], unsigned char* dst, int tid) {
   const int c = tid >> 3, q = tid & 7;
-  unsigned char* d = dst + c * kRow + ((q ^ swz(c)) << 4);
+  unsigned char* d = dst + c * kRow + ((q ^ tile_swz(c)) << 4);
 #pragma unroll
   for (int u = 0; u < NR; ++u) *reinterpret_cast<u32x4*>(d + u * 32 * kRow) = buf[u];
 }
@@ -92,62 +112,63 @@ __device__ __forceinline__ uint16_t coef_part(float a, int part) {
   return f32_to_bf16(r1 - bf16_to_f32(mid));
 }
 
-// Coefficients of one image fetched into registers ahead of the rebuild:
-// entry e = tid + 256 r of alpha[b] (the flattened [R][k] block).
-struct CoefFetch {
-  float a[kPre];
-};
-
-__device__ __forceinline__ void fetch_coefs(const MixArgs& p, const float* __restrict__ alpha, int b, CoefFetch& f,
-                                            int tid) {
+// Entries tid + 256 r of alpha[b] (the flattened [R][k] block), fetched
+// ahead of a rebuild.
+__device__ __forceinline__ void fetch_coefs(const MixArgs& p, const float* __restrict__ alpha, int b,
+                                            float (&a)[kPre], int tid) {
   const int nent = p.R * p.k;
   const float* ab = alpha + (int64_t)b * nent;
 #pragma unroll
-  for (int r = 0; r < kPre; ++r) f.a[r] = ab[min(tid + kThreads * r, nent - 1)];
+  for (int r = 0; r < kPre; ++r) a[r] = ab[min(tid + kThreads * r, nent - 1)];
 }
 
-// Rebuilds the wave's rows of A_b in registers: zero the staging rows, then
-// per part scatter the coefficients (and 1/nU at the uncovered channels) and
-// read the MFMA B operands.  slot[r] is the staging index of entry
-// tid + 256 r; entries past kPre * 256 are read here directly.
-template <int NS, int NKS>
-__device__ __forceinline__ void build_coefs(const MixArgs& p, int b, const int32_t* __restrict__ s, const float* __restrict__ alpha,
-                            int uch, const CoefFetch& f, const int (&slot)[kPre], uint16_t* stage,
-                            bf16x8 (&bfr)[NS][NKS], int tid, int orow, int khalf) {
-  const int rs = stage_row(p.C);
+// Rebuilds the wave's rows of A_b in registers, assembling A_b in the tile
+// buffer `stage` (free while this runs): zero it, then per part scatter the
+// coefficients alpha[b] (a: the first kPre * 256 of them, fetched ahead; the
+// rest are read here) and 1/nU at the uncovered channels, and read the MFMA B
+// operands.  The staging offset of entry e = tid + 256 r (below 2^15) is the
+// 16-bit half r & 1 of slot[r >> 1].  Ends with a barrier, after which the
+// buffer may be overwritten.
+template <int NS, int NR>
+__device__ __forceinline__ void build_coefs(const MixArgs& p, int b, const int32_t* __restrict__ s,
+                                            const float* __restrict__ alpha, const float (&a)[kPre], int uch,
+                                            const uint32_t (&slot)[kPre / 2], unsigned char* stage,
+                                            bf16x8 (&bfr)[NS][NR], int tid, int orow, int kq) {
   const int nent = p.R * p.k;
   const float* ab = alpha + (int64_t)b * nent;
   const float inv = p.nU > 0 ? 1.f / (float)p.nU : 0.f;
-  uint4* z = reinterpret_cast<uint4*>(stage);
-  const int nz = kMaxE * rs / 8;
-  for (int i = tid; i < nz; i += kThreads) z[i] = make_uint4(0u, 0u, 0u, 0u);
+  u32x4* z = reinterpret_cast<u32x4*>(stage);
+  const int nz = kMaxE * p.C / 8;
+  for (int i = tid; i < nz; i += kThreads) z[i] = u32x4{0u, 0u, 0u, 0u};
+  const int ures = stage_off(p.R, uch, p.C);
 #pragma unroll
   for (int part = 0; part < NS; ++part) {
     __syncthreads();  // zeroing (or the previous part's operand reads) done
 #pragma unroll
     for (int r = 0; r < kPre; ++r)
-      if (tid + kThreads * r < nent) stage[slot[r]] = coef_part(f.a[r], part);
+      if (tid + kThreads * r < nent)
+        *reinterpret_cast<uint16_t*>(stage + ((slot[r >> 1] >> (16 * (r & 1))) & 0xffffu)) = coef_part(a[r], part);
     for (int e = tid + kThreads * kPre; e < nent; e += kThreads)
-      stage[(e / p.k) * rs + s[e]] = coef_part(ab[e], part);
-    if (tid < p.nU) stage[p.R * rs + uch] = coef_part(inv, part);
+      *reinterpret_cast<uint16_t*>(stage + stage_off(e / p.k, s[e], p.C)) = coef_part(ab[e], part);
+    if (tid < p.nU) *reinterpret_cast<uint16_t*>(stage + ures) = coef_part(inv, part);
     __syncthreads();
-    const uint16_t* row = stage + orow * rs + khalf * 8;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-      bfr[part][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(row + ks * 16));
+    for (int ks = 0; ks < NR; ++ks)
+      bfr[part][ks] =
+          __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(stage + stage_off(orow, 32 * ks + 8 * kq, p.C)));
   }
+  __syncthreads();
 }
 
 __device__ __forceinline__ bf16x4 tr_read(const unsigned char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MOCE_LDS bf16x4*)(MOCE_LDS unsigned char*)p);
 }
 
-// NR = C / 32 load rounds, NS coefficient parts.
+// NR = C / 32 load rounds (and channel steps of 32), NS coefficient parts.
 template <int NR, int NS>
-__global__ void __launch_bounds__(kThreads, 1)
+__global__ void __launch_bounds__(kThreads, 2)
 k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, const int32_t* __restrict__ s,
           const float* __restrict__ alpha, const int32_t* __restrict__ U) {
-  constexpr int NKS = 2 * NR;  // channel steps of 16
   extern __shared__ __align__(16) unsigned char smem[];
   const int G = gridDim.x;
   const int t0 = (int)((int64_t)blockIdx.x * p.ntiles / G);
@@ -156,106 +177,150 @@ k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, c
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int mb = wv & 1, nb = wv >> 1;
   const int tileb = p.C * kRow;
-  uint16_t* stage = reinterpret_cast<uint16_t*>(smem + 2 * tileb);
-  const int rs = stage_row(p.C);
+  unsigned char* outw = smem + 2 * tileb + wv * kOutWave;
+  const int orow = kExpertsPerWave * wv + (lane & 15);  // this lane's expert (operand row, output column)
+  const int g = lane >> 4, sl = lane & 15;
 
-  // coefficients and static scatter slots first, so that waiting for them
-  // does not wait for the tiles
-  int cur = t0 / p.nt;
-  CoefFetch f;
-  fetch_coefs(p, alpha, cur, f, tid);
-  int slot[kPre];
+  // static scatter offsets, the uncovered channel and the first image's
+  // coefficients are read before any tile is requested (every workgroup
+  // starting at once would otherwise queue these small reads behind
+  // megabytes of tile requests); the first rebuild then runs while tile t0
+  // is in flight
+  uint32_t slot[kPre / 2] = {};
   const int nent = p.R * p.k;
 #pragma unroll
   for (int r = 0; r < kPre; ++r) {
     const int e = min(tid + kThreads * r, nent - 1);
-    slot[r] = (e / p.k) * rs + s[e];
+    slot[r >> 1] |= (uint32_t)stage_off(e / p.k, s[e], p.C) << (16 * (r & 1));
   }
   // uncovered channel tid (U may be null when nU == 0: s is read instead)
   const int uv = *(p.nU > 0 ? U + min(tid, p.nU - 1) : s);
   const int uch = p.nU > 0 ? uv : 0;
+  int b = t0 / p.nt, j = t0 - b * p.nt;
+  float a[kPre];
+  fetch_coefs(p, alpha, b, a, tid);
+  __builtin_amdgcn_s_waitcnt(kVmDrain);
+  __builtin_amdgcn_sched_barrier(0);
 
-  u32x4 st0[NR], st1[NR], st2[NR];
-  // issue order t0, t0 + 1, t0 + 2 (the loop below relies on loads
-  // completing in that order)
+  // issue order t0, t0 + 1 (the loop below relies on loads completing in
+  // that order)
+  u32x4 st0[NR], st1[NR];
   load_tile(p, x, t0, st0, tid);
+  __builtin_amdgcn_sched_barrier(0);
+  bf16x8 bfr[NS][NR];
+  build_coefs<NS, NR>(p, b, s, alpha, a, uch, slot, smem + tileb, bfr, tid, orow, g);
   __builtin_amdgcn_sched_barrier(0);
   load_tile(p, x, min(t0 + 1, t1 - 1), st1, tid);
   __builtin_amdgcn_sched_barrier(0);
-  load_tile(p, x, min(t0 + 2, t1 - 1), st2, tid);
-  __builtin_amdgcn_sched_barrier(0);
-
-  bf16x8 bfr[NS][NKS];
-  build_coefs<NS, NKS>(p, cur, s, alpha, uch, f, slot, stage, bfr, tid, 32 * nb + (lane & 31), lane >> 5);
-  store_tile(st0, smem, tid);
+  store_tile(st0, smem, tid);  // tile t0 into buffer 0
   __syncthreads();
 
-  // transposing-read offset of this lane for channel step 0, first half:
-  // 16-lane group g reads channels 8 (g >> 1) + 4 h + (l >> 2) at positions
-  // 32 mb + 16 (g & 1) + 4 (l & 3) .. +3 (l = lane & 15)
-  const int g = lane >> 4, sl = lane & 15;
-  const int trow = 8 * (g >> 1) + (sl >> 2);
-  const int tq = 4 * mb + 2 * (g & 1) + ((sl & 3) >> 1);
-  const int troff = trow * kRow + ((tq ^ (((sl >> 3) & 1) << 2)) << 4) + 8 * (sl & 1);
-  const int o = 32 * nb + (lane & 31);
+  // transposing reads: 16-lane group g reads channels 8 g + 4 h + (l >> 2)
+  // (+ 32 ks) at positions 16 pb + 4 (l & 3) .. +3, l = lane & 15
+  const int trow = (8 * g + (sl >> 2)) * kRow + 8 * (sl & 1);
+  int troff[4];
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb) troff[pb] = trow + (((2 * pb + ((sl & 3) >> 1)) ^ (2 * g)) << 4);
+  // this thread's destination of tile rows (tid >> 3) + 32 u
+  const int stoff = (tid >> 3) * kRow + (((tid & 7) ^ tile_swz(tid >> 3)) << 4);
 
-  auto step = [&](int n, u32x4(&refill)[NR], const u32x4(&next)[NR]) __attribute__((always_inline)) {
-    const int b = n / p.nt, j = n - (n / p.nt) * p.nt;
-    if (b != cur) {
-      build_coefs<NS, NKS>(p, b, s, alpha, uch, f, slot, stage, bfr, tid, 32 * nb + (lane & 31), lane >> 5);
-      cur = b;
+  // results of the previous tile, bf16: expert orow at positions 16 pb + 4 g
+  // .. +3 of tile (pb_img, pj); written through the wave's output area so
+  // that lane i stores 16 bytes of row i >> 3 (+8)
+  u32x2 prev[4];
+  int pb_img = b, pj = j;
+  auto emit = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) *reinterpret_cast<u32x2*>(outw + sl * kOutRow + 32 * pb + 8 * g) = prev[pb];
+    const int pos = pj * kTile + 8 * (lane & 7);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = (lane >> 3) + 8 * h;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(outw + r * kOutRow + (lane & 7) * 16);
+      const int o = kExpertsPerWave * wv + r;
+      if (o < p.E && pos < p.HW) *reinterpret_cast<u32x4*>(y + ((int64_t)pb_img * p.E + o) * p.HW + pos) = v;
     }
-    const int n1 = n + 1;
-    if (n1 < t1 && n1 / p.nt != b) fetch_coefs(p, alpha, n1 / p.nt, f, tid);
-    load_tile(p, x, min(n + 3, t1 - 1), refill, tid);
-    __builtin_amdgcn_sched_barrier(0);  // the loads go out before the products
-
-    const unsigned char* tb = smem + ((n - t0) & 1) * tileb + troff;
-    bf16x8 xa[NKS];
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const bf16x4 lo = tr_read(tb + ks * 16 * kRow);
-      const bf16x4 hi = tr_read(tb + ks * 16 * kRow + 4 * kRow);
-      xa[ks] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    }
-    f32x16 acc0 = {}, acc1 = {};
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-      for (int part = 0; part < NS; ++part) {
-        if (((ks * NS + part) & 1) == 0)
-          acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[ks], bfr[part][ks], acc0, 0, 0, 0);
-        else
-          acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[ks], bfr[part][ks], acc1, 0, 0, 0);
-      }
-
-    // the next tile into the other buffer (its last readers passed the
-    // barrier that ended the previous step)
-    store_tile(next, smem + ((n - t0 + 1) & 1) * tileb, tid);
-
-    // lane holds expert o at positions 32 mb + 8 q + 4 (lane >> 5) .. +3
-    const int pb = j * kTile + 32 * mb + 4 * (lane >> 5);
-    uint16_t* yo = y + ((int64_t)b * p.E + o) * p.HW + pb;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float v0 = acc0[4 * q] + acc1[4 * q], v1 = acc0[4 * q + 1] + acc1[4 * q + 1];
-      const float v2 = acc0[4 * q + 2] + acc1[4 * q + 2], v3 = acc0[4 * q + 3] + acc1[4 * q + 3];
-      if (o < p.E && pb + 8 * q < p.HW)
-        *reinterpret_cast<uint2*>(yo + 8 * q) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
-    }
-    __syncthreads();
   };
 
-  for (int n = t0;;) {
-    step(n, st0, st1);
-    if (++n >= t1) break;
-    step(n, st1, st2);
-    if (++n >= t1) break;
-    step(n, st2, st0);
-    if (++n >= t1) break;
+  // Tile n: the previous tile's results leave, tile n + 2 is requested into
+  // the registers tile n came through, and the products of tile n run with
+  // tile n + 1 written into the other buffer a row chunk per channel step
+  // (waiting for tile n + 1 only).  The other buffer is free: the barrier
+  // that ended the previous step (or the rebuild) follows the last reads of
+  // tile n - 1.
+  auto step = [&](int n, auto first, u32x4(&refill)[NR], const u32x4(&next)[NR]) __attribute__((always_inline)) {
+    if constexpr (!decltype(first)::value) emit();
+    load_tile(p, x, min(n + 2, t1 - 1), refill, tid);
+    unsigned char* other = smem + ((n - t0 + 1) & 1) * tileb + stoff;
+    const unsigned char* tb = smem + ((n - t0) & 1) * tileb;
+    f32x4 acc[4];
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) acc[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < NR; ++ks) {
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb) {
+        const unsigned char* ap = tb + troff[pb] + ks * 32 * kRow;
+        const bf16x8 xa = __builtin_shufflevector(tr_read(ap), tr_read(ap + 4 * kRow), 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+        for (int part = 0; part < NS; ++part)
+          acc[pb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, bfr[part][ks], acc[pb], 0, 0, 0);
+      }
+      *reinterpret_cast<u32x4*>(other + ks * 32 * kRow) = next[ks];
+    }
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb)
+      prev[pb] = u32x2{pack_bf16x2(acc[pb][0], acc[pb][1]), pack_bf16x2(acc[pb][2], acc[pb][3])};
+    pb_img = b;
+    pj = j;
+    __syncthreads();  // tile n + 1 visible; every read of tile n done
+  };
+
+  // tiles t0 + 1 ..: one image at a time, A_b rebuilt unconditionally at the
+  // start of each image's run, so that the operand registers are never merged
+  // across a conditional rebuild
+  auto run = [&](int n, int te) __attribute__((always_inline)) {
+#pragma unroll 2
+    for (; n < te; ++n, ++j) {
+      step(n, std::false_type{}, st0, st1);
+      // tile n + 2 now sits in st0 and tile n + 1 has left st1
+      u32x4 sw[NR];
+#pragma unroll
+      for (int u = 0; u < NR; ++u) sw[u] = st0[u];
+#pragma unroll
+      for (int u = 0; u < NR; ++u) st0[u] = st1[u];
+#pragma unroll
+      for (int u = 0; u < NR; ++u) st1[u] = sw[u];
+    }
+  };
+
+  step(t0, std::true_type{}, st0, st1);
+  {
+    u32x4 sw[NR];
+#pragma unroll
+    for (int u = 0; u < NR; ++u) sw[u] = st0[u];
+#pragma unroll
+    for (int u = 0; u < NR; ++u) st0[u] = st1[u];
+#pragma unroll
+    for (int u = 0; u < NR; ++u) st1[u] = sw[u];
   }
+  ++j;
+  int n = t0 + 1;
+  run(n, min(t1, (b + 1) * p.nt));
+  n = min(t1, (b + 1) * p.nt);
+  while (n < t1) {
+    // next image: this workgroup stalls on the coefficient loads, the other
+    // one on the CU keeps it busy
+    ++b;
+    j = 0;
+    fetch_coefs(p, alpha, b, a, tid);
+    build_coefs<NS, NR>(p, b, s, alpha, a, uch, slot, smem + ((n - t0 + 1) & 1) * tileb, bfr, tid, orow, g);
+    const int te = min(t1, (b + 1) * p.nt);
+    run(n, te);
+    n = te;
+  }
+  emit();
 }
 
 using MfmaKernel = void (*)(MixArgs, const uint16_t*, uint16_t*, const int32_t*, const float*, const int32_t*);
@@ -268,6 +333,7 @@ MfmaKernel pick(int nr) {
 }
 
 constexpr int kParts = 3;
+constexpr int kPerCU = 2;
 
 }  // namespace
 
@@ -295,7 +361,7 @@ hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, cons
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     cus = 256;
-  const int grid = std::min(cus, p.ntiles);
+  const int grid = std::min(cus * kPerCU, p.ntiles);
   const size_t lds = mfma_lds(p.C);
   const MfmaKernel k = pick<kParts>(p.C / 32);
   static bool configured[8] = {};
