@@ -15,17 +15,21 @@
 // products are exact in float32 and the MFMA accumulates in float32, so the
 // result is the float32 gather form up to the order of the additions.
 //
-// Work split.  Two workgroups of 4 waves share a CU, so that one multiplies
-// while the other loads, stores and synchronises.  A workgroup walks a
-// contiguous range of tiles (64 positions x all C channels of one image);
-// wave w computes experts 16 w .. 16 w + 15 at all 64 positions.  Each wave
-// holds its 16 rows of A_b (all channels, every part) in registers as MFMA B
-// operands, rebuilt when the image changes.  The x tile is held in LDS as
-// bf16, double-buffered, and read as MFMA A operands with the transposing LDS
-// read, which turns position-contiguous channel rows into channel-contiguous
-// operands.  A_b is assembled in whichever tile buffer is free at that moment.
-// Results leave through a small per-wave LDS area so that every store
-// instruction writes whole 128-byte rows of y.
+// Work split.  One workgroup per CU walks a contiguous range of tiles (64
+// positions x all C channels of one image) with three kinds of waves, so
+// that no wave that computes ever waits behind the memory system.  Two loader
+// waves copy each tile straight from HBM into a ring of four LDS tile buffers
+// (global-to-LDS loads, no registers), keeping up to three tiles in flight,
+// and wait for their own copies with explicit counters.  Four consumer waves
+// only compute: wave w multiplies experts 16 w .. 16 w + 15 at all 64
+// positions, holding its 16 rows of A_b (all channels, every part) in
+// registers as MFMA B operands and reading the x tile as MFMA A operands with
+// the transposing LDS read, which turns the position-contiguous channel rows
+// into channel-contiguous operands; results go to an LDS output buffer.  Two
+// store waves write the previous tile's results from there to y, whole
+// 128-byte rows per store.  All waves meet at one barrier per tile.  When the
+// image changes each consumer wave rebuilds its own rows of A_b, 8 at a time,
+// in its own staging area, while the other waves carry on.
 #include <algorithm>
 #include <type_traits>
 
@@ -41,25 +45,47 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 #define MOCE_LDS __attribute__((address_space(3)))
 
-constexpr int kThreads = 256;
-constexpr int kTile = 64;               // positions per tile
-constexpr int kRow = kTile * 2;         // bytes of one channel row of an LDS tile
-constexpr int kMaxE = 64;               // rows of A_b
+constexpr int kConsumers = 4;                   // waves computing products
+constexpr int kLoaders = 2;                     // waves copying tiles into LDS
+constexpr int kStorers = 2;                     // waves writing results to y
+constexpr int kCThreads = 64 * kConsumers;
+constexpr int kLThreads = 64 * kLoaders;
+constexpr int kThreads = 64 * (kConsumers + kLoaders + kStorers);
+constexpr int kRing = 4;                        // LDS tile buffers
+constexpr int kTile = 64;                       // positions per tile
+constexpr int kRow = kTile * 2;                 // bytes of one channel row of an LDS tile
+constexpr int kMaxE = 64;                       // rows of A_b
+constexpr int kStageRows = 8;                   // rows of A_b a consumer wave assembles at a time
 constexpr int kMaxC = 256;
-constexpr int kPre = 8;                 // coefficient entries per thread fetched into registers
+constexpr int kPre = 8;                         // coefficient entries per consumer lane fetched ahead
+constexpr int kUPer = kMaxC / 64;               // uncovered channels per lane of the residual's wave
 constexpr int kExpertsPerWave = 16;
-constexpr int kOutRow = kRow + 16;      // bytes per row of a wave's output area (padded)
-constexpr int kOutWave = kExpertsPerWave * kOutRow;
-// s_waitcnt operand waiting for every vector memory access (vmcnt 0, the
-// LDS/scalar and export counters left at their maxima)
-constexpr int kVmDrain = 0x0f70;
+constexpr int kOutWave = kExpertsPerWave * kRow;  // one consumer wave's results for a tile
+
+// Workgroup barrier for LDS traffic: waits for this wave's own LDS (and
+// scalar) accesses, then for every wave.  Unlike __syncthreads it does not
+// wait for outstanding global-to-LDS copies (the release fence would drain
+// the whole ring of tiles in flight at every step); each copy is waited for
+// explicitly, with vm_wait, before the barrier that publishes its tile.  The
+// memory clobber keeps the compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// s_waitcnt operand that waits until at most n vector memory accesses of
+// this wave are outstanding (the LDS/scalar and export counters left at
+// their maxima)
+constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 struct MixArgs {
   int C, HW, E, R, k, nU, nt, ntiles;
 };
 
-// LDS: two x tiles [C][kTile] bf16, then the four waves' output areas.
-__host__ __device__ inline size_t mfma_lds(int C) { return (size_t)2 * C * kRow + (size_t)4 * kOutWave; }
+// LDS: the ring of x tiles [C][kTile] bf16, each consumer wave's A_b staging
+// rows [kStageRows][C] bf16, then two output buffers [E rows][kTile] bf16
+// (the consumer waves' results of alternate tiles; 16-byte chunk q of row r
+// is stored at chunk q ^ (r & 7)).
+__host__ __device__ inline size_t mfma_lds(int C) {
+  return (size_t)kRing * C * kRow + (size_t)kConsumers * kStageRows * C * 2 + (size_t)2 * kConsumers * kOutWave;
+}
 
 // Chunk q (16 bytes = 8 positions) of channel row c of a tile is stored at
 // chunk q ^ (2 ((c >> 3) & 3)): the 16 rows x 32 bytes that one transposing
@@ -78,27 +104,25 @@ __device__ __forceinline__ int stage_off(int o, int c, int C) {
   return o * C * 2 + ch * 16 + (c & 7) * 2;
 }
 
-// Global loads of tile n (NR rounds of 16 bytes per thread): thread t reads
-// positions 8 (t & 7) .. +7 of channel (t >> 3) + 32 u.  Positions past the
-// image repeat its last vector; those outputs are never stored.
+// Copies tile n into the LDS tile buffer `buf` with global-to-LDS loads, one
+// 16-byte load per loader lane and round: loader lane t (of 128) fills slot t
+// of each 2 KB block u, i.e. chunk t & 7 of row (t >> 3) + 16 u, with the 8
+// positions of the tile that belong there under the swizzle.  Positions past
+// the image repeat its last vector; those outputs are never stored.
 template <int NR>
-__device__ __forceinline__ void load_tile(const MixArgs& p, const uint16_t* __restrict__ x, int n, u32x4 (&buf)[NR],
-                                          int tid) {
+__device__ __forceinline__ void copy_tile(const MixArgs& p, const uint16_t* __restrict__ x, int n, unsigned char* buf,
+                                          int lt) {
   const int b = n / p.nt, j = n - (n / p.nt) * p.nt;
   const int p0 = j * kTile;
-  const int vq = min(tid & 7, min(kTile, p.HW - p0) / 8 - 1);
-  const uint16_t* src = x + ((int64_t)b * p.C + (tid >> 3)) * p.HW + p0 + vq * 8;
+  const int qmax = min(kTile, p.HW - p0) / 8 - 1;
+  const uint16_t* src = x + ((int64_t)b * p.C + (lt >> 3)) * p.HW + p0;
+  MOCE_LDS unsigned char* dst = (MOCE_LDS unsigned char*)buf + (lt & ~63) * 16;
 #pragma unroll
-  for (int u = 0; u < NR; ++u) buf[u] = *reinterpret_cast<const u32x4*>(src + (int64_t)u * 32 * p.HW);
-}
-
-// Thread t's chunks go to rows (t >> 3) + 32 u: one wave writes 8 whole rows.
-template <int NR>
-__device__ __forceinline__ void store_tile(const u32x4 (&buf)[NR], unsigned char* dst, int tid) {
-  const int c = tid >> 3, q = tid & 7;
-  unsigned char* d = dst + c * kRow + ((q ^ tile_swz(c)) << 4);
-#pragma unroll
-  for (int u = 0; u < NR; ++u) *reinterpret_cast<u32x4*>(d + u * 32 * kRow) = buf[u];
+  for (int u = 0; u < 2 * NR; ++u) {
+    const int q = min((lt & 7) ^ tile_swz((lt >> 3) + 16 * u), qmax);
+    __builtin_amdgcn_global_load_lds((const void*)(src + (int64_t)u * 16 * p.HW + q * 8),
+                                     (MOCE_LDS void*)(dst + u * 16 * kRow), 16, 0, 0);
+  }
 }
 
 // Part `part` of the exact split a = hi + mid + lo into bf16 values (with
@@ -112,61 +136,125 @@ __device__ __forceinline__ uint16_t coef_part(float a, int part) {
   return f32_to_bf16(r1 - bf16_to_f32(mid));
 }
 
-// Entries tid + 256 r of alpha[b] (the flattened [R][k] block), fetched
-// ahead of a rebuild.
-__device__ __forceinline__ void fetch_coefs(const MixArgs& p, const float* __restrict__ alpha, int b,
-                                            float (&a)[kPre], int tid) {
+// A consumer wave's coefficients.  Entry i < 16 k of wave w is coefficient
+// i % k of expert 16 w + i / k, i.e. entry 16 w k + i of an image's flattened
+// [R][k] block; lane l handles entries l + 64 r.  slot[] holds their staging
+// slots, 16 bits each: (i / k) >> 3 << 14 (which group of 8 rows) | the byte
+// offset within the wave's staging rows, 0xffff for none.  uslot[] does the
+// same for the residual row's uncovered channels l + 64 u (only in the wave
+// holding row R).
+struct WaveCoefs {
+  float a[kPre];
+  uint32_t slot[kPre / 2];
+  uint32_t uslot[kUPer / 2];
+};
+
+__device__ __forceinline__ uint32_t half_of(uint32_t packed, int r) { return (packed >> (16 * (r & 1))) & 0xffffu; }
+
+__device__ __forceinline__ void wave_slots(const MixArgs& p, const int32_t* __restrict__ s,
+                                           const int32_t* __restrict__ U, WaveCoefs& wc, int cw, int lane) {
   const int nent = p.R * p.k;
-  const float* ab = alpha + (int64_t)b * nent;
 #pragma unroll
-  for (int r = 0; r < kPre; ++r) a[r] = ab[min(tid + kThreads * r, nent - 1)];
+  for (int r = 0; r < kPre; ++r) {
+    const int i = lane + 64 * r;
+    const int e = kExpertsPerWave * cw * p.k + i;
+    const int c = s[min(e, nent - 1)];
+    const int eo = i / p.k;
+    const uint32_t v = (i < kExpertsPerWave * p.k && e < nent)
+                           ? (uint32_t)((eo >> 3) << 14 | stage_off(eo & (kStageRows - 1), c, p.C))
+                           : 0xffffu;
+    wc.slot[r >> 1] = (r & 1) ? (wc.slot[r >> 1] | v << 16) : v;
+  }
+  const int ro = p.R - kExpertsPerWave * cw;  // the residual row within this wave's experts
+#pragma unroll
+  for (int u = 0; u < kUPer; ++u) {
+    const int ui = lane + 64 * u;
+    // U may be null when nU == 0: s is read instead
+    const int c = *(p.nU > 0 ? U + min(ui, p.nU - 1) : s);
+    const uint32_t v = (ro >= 0 && ro < kExpertsPerWave && ui < p.nU)
+                           ? (uint32_t)((ro >> 3) << 14 | stage_off(ro & (kStageRows - 1), c, p.C))
+                           : 0xffffu;
+    wc.uslot[u >> 1] = (u & 1) ? (wc.uslot[u >> 1] | v << 16) : v;
+  }
 }
 
-// Rebuilds the wave's rows of A_b in registers, assembling A_b in the tile
-// buffer `stage` (free while this runs): zero it, then per part scatter the
-// coefficients alpha[b] (a: the first kPre * 256 of them, fetched ahead; the
-// rest are read here) and 1/nU at the uncovered channels, and read the MFMA B
-// operands.  The staging offset of entry e = tid + 256 r (below 2^15) is the
-// 16-bit half r & 1 of slot[r >> 1].  Ends with a barrier, after which the
-// buffer may be overwritten.
+__device__ __forceinline__ void fetch_coefs(const MixArgs& p, const float* __restrict__ alpha, int b, WaveCoefs& wc,
+                                            int cw, int lane) {
+  const int nent = p.R * p.k;
+  const int first = kExpertsPerWave * cw * p.k;
+  const float* ab = alpha + (int64_t)b * nent;
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) wc.a[r] = ab[min(first + lane + 64 * r, nent - 1)];
+}
+
+// Rebuilds a consumer wave's rows of A_b in registers through its own
+// staging rows (8 at a time, so no other wave is involved and no barrier is
+// needed: a wave's LDS accesses take effect in order).  For each group of 8
+// rows: zero them, then per part scatter part `part` of the coefficients
+// (and 1/nU at the uncovered channels) and read the MFMA B operands of the
+// lanes whose expert is in the group.  Entries past 64 kPre are read here.
 template <int NS, int NR>
 __device__ __forceinline__ void build_coefs(const MixArgs& p, int b, const int32_t* __restrict__ s,
-                                            const float* __restrict__ alpha, const float (&a)[kPre], int uch,
-                                            const uint32_t (&slot)[kPre / 2], unsigned char* stage,
-                                            bf16x8 (&bfr)[NS][NR], int tid, int orow, int kq) {
+                                            const float* __restrict__ alpha, const WaveCoefs& wc,
+                                            unsigned char* rows, bf16x8 (&bfr)[NS][NR], int cw, int lane) {
   const int nent = p.R * p.k;
   const float* ab = alpha + (int64_t)b * nent;
   const float inv = p.nU > 0 ? 1.f / (float)p.nU : 0.f;
-  u32x4* z = reinterpret_cast<u32x4*>(stage);
-  const int nz = kMaxE * p.C / 8;
-  for (int i = tid; i < nz; i += kThreads) z[i] = u32x4{0u, 0u, 0u, 0u};
-  const int ures = stage_off(p.R, uch, p.C);
+  const int nz = kStageRows * p.C / 8;  // 16-byte chunks of the staging rows
+  const int my = lane & 15;             // this lane's expert within the wave
+  const int g = lane >> 4;
+#pragma unroll 1
+  for (int grp = 0; grp < kExpertsPerWave / kStageRows; ++grp) {
+    for (int i = lane; i < nz; i += 64) reinterpret_cast<u32x4*>(rows)[i] = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int part = 0; part < NS; ++part) {
-    __syncthreads();  // zeroing (or the previous part's operand reads) done
+    for (int part = 0; part < NS; ++part) {
 #pragma unroll
-    for (int r = 0; r < kPre; ++r)
-      if (tid + kThreads * r < nent)
-        *reinterpret_cast<uint16_t*>(stage + ((slot[r >> 1] >> (16 * (r & 1))) & 0xffffu)) = coef_part(a[r], part);
-    for (int e = tid + kThreads * kPre; e < nent; e += kThreads)
-      *reinterpret_cast<uint16_t*>(stage + stage_off(e / p.k, s[e], p.C)) = coef_part(ab[e], part);
-    if (tid < p.nU) *reinterpret_cast<uint16_t*>(stage + ures) = coef_part(inv, part);
-    __syncthreads();
+      for (int r = 0; r < kPre; ++r) {
+        const uint32_t sl = half_of(wc.slot[r >> 1], r);
+        if (sl != 0xffffu && (int)(sl >> 14) == grp)
+          *reinterpret_cast<uint16_t*>(rows + (sl & 0x3fffu)) = coef_part(wc.a[r], part);
+      }
+      for (int i = lane + 64 * kPre; i < kExpertsPerWave * p.k; i += 64) {
+        const int e = kExpertsPerWave * cw * p.k + i;
+        const int eo = i / p.k;
+        if (e < nent && (eo >> 3) == grp)
+          *reinterpret_cast<uint16_t*>(rows + stage_off(eo & (kStageRows - 1), s[e], p.C)) = coef_part(ab[e], part);
+      }
 #pragma unroll
-    for (int ks = 0; ks < NR; ++ks)
-      bfr[part][ks] =
-          __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(stage + stage_off(orow, 32 * ks + 8 * kq, p.C)));
+      for (int u = 0; u < kUPer; ++u) {
+        const uint32_t sl = half_of(wc.uslot[u >> 1], u);
+        if (sl != 0xffffu && (int)(sl >> 14) == grp)
+          *reinterpret_cast<uint16_t*>(rows + (sl & 0x3fffu)) = coef_part(inv, part);
+      }
+#pragma unroll
+      for (int ks = 0; ks < NR; ++ks) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(rows + stage_off(my & (kStageRows - 1), 32 * ks + 8 * g, p.C));
+        if ((my >> 3) == grp) bfr[part][ks] = __builtin_bit_cast(bf16x8, v);
+      }
+    }
   }
-  __syncthreads();
 }
 
 __device__ __forceinline__ bf16x4 tr_read(const unsigned char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((MOCE_LDS bf16x4*)(MOCE_LDS unsigned char*)p);
 }
 
-// NR = C / 32 load rounds (and channel steps of 32), NS coefficient parts.
+// Waits until the copies of tile n + 1 are complete, given that the copies
+// of tiles up to min(n + 3, t1 - 1) have been issued (2 NR per tile).
+template <int NR>
+__device__ __forceinline__ void wait_next_tile(int n, int t1) {
+  const int ahead = min(2, t1 - 2 - n);  // tiles issued after tile n + 1
+  if (ahead >= 2)
+    __builtin_amdgcn_s_waitcnt(vm_wait(4 * NR));
+  else if (ahead == 1)
+    __builtin_amdgcn_s_waitcnt(vm_wait(2 * NR));
+  else
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));
+}
+
+// NR = C / 32 channel steps of 32, NS coefficient parts.
 template <int NR, int NS>
-__global__ void __launch_bounds__(kThreads, 2)
+__global__ void __launch_bounds__(kThreads, 1)
 k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, const int32_t* __restrict__ s,
           const float* __restrict__ alpha, const int32_t* __restrict__ U) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -177,44 +265,40 @@ k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, c
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool consumer = wv < kConsumers;
+  const bool loader = !consumer && wv < kConsumers + kLoaders;
+  const bool storer = wv >= kConsumers + kLoaders;
   const int tileb = p.C * kRow;
-  unsigned char* outw = smem + 2 * tileb + wv * kOutWave;
-  const int orow = kExpertsPerWave * wv + (lane & 15);  // this lane's expert (operand row, output column)
+  unsigned char* ring = smem;
+  unsigned char* stage = smem + kRing * tileb;
+  unsigned char* obuf = stage + kConsumers * kStageRows * p.C * 2;  // two buffers of kConsumers * kOutWave bytes
+  const int cw = wv & (kConsumers - 1);
+  const int orow = kExpertsPerWave * cw + (lane & 15);  // consumer lane's expert (operand row, output column)
   const int g = lane >> 4, sl = lane & 15;
+  const int lt = tid - kCThreads;                        // loader lane
 
-  // static scatter offsets, the uncovered channel and the first image's
-  // coefficients are read before any tile is requested (every workgroup
-  // starting at once would otherwise queue these small reads behind
-  // megabytes of tile requests); the first rebuild then runs while tile t0
-  // is in flight
-  uint32_t slot[kPre / 2] = {};
-  const int nent = p.R * p.k;
-#pragma unroll
-  for (int r = 0; r < kPre; ++r) {
-    const int e = min(tid + kThreads * r, nent - 1);
-    slot[r >> 1] |= (uint32_t)stage_off(e / p.k, s[e], p.C) << (16 * (r & 1));
-  }
-  // uncovered channel tid (U may be null when nU == 0: s is read instead)
-  const int uv = *(p.nU > 0 ? U + min(tid, p.nU - 1) : s);
-  const int uch = p.nU > 0 ? uv : 0;
+  // Loaders request tile t0 first; consumers read the first image's
+  // coefficients, their staging slots and the uncovered channels before the
+  // rest of the tiles is requested (every workgroup starting at once would
+  // otherwise queue these small reads behind megabytes of tiles).  The
+  // consumers build their rows of A_b at the first step, like at every image
+  // change (one copy of that code keeps the kernel small in the instruction
+  // cache).
+  if (loader) copy_tile<NR>(p, x, t0, ring, lt);
   int b = t0 / p.nt, j = t0 - b * p.nt;
-  float a[kPre];
-  fetch_coefs(p, alpha, b, a, tid);
-  __builtin_amdgcn_s_waitcnt(kVmDrain);
-  __builtin_amdgcn_sched_barrier(0);
-
-  // issue order t0, t0 + 1 (the loop below relies on loads completing in
-  // that order)
-  u32x4 st0[NR], st1[NR];
-  load_tile(p, x, t0, st0, tid);
-  __builtin_amdgcn_sched_barrier(0);
+  WaveCoefs wc;
+  unsigned char* rows = stage + cw * (kStageRows * p.C * 2);
+  if (consumer) {
+    wave_slots(p, s, U, wc, cw, lane);
+    fetch_coefs(p, alpha, b, wc, cw, lane);
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));
+  }
+  lds_barrier();
+  if (loader) {
+    if (t0 + 1 < t1) copy_tile<NR>(p, x, t0 + 1, ring + tileb, lt);
+    if (t0 + 2 < t1) copy_tile<NR>(p, x, t0 + 2, ring + 2 * tileb, lt);
+  }
   bf16x8 bfr[NS][NR];
-  build_coefs<NS, NR>(p, b, s, alpha, a, uch, slot, smem + tileb, bfr, tid, orow, g);
-  __builtin_amdgcn_sched_barrier(0);
-  load_tile(p, x, min(t0 + 1, t1 - 1), st1, tid);
-  __builtin_amdgcn_sched_barrier(0);
-  store_tile(st0, smem, tid);  // tile t0 into buffer 0
-  __syncthreads();
 
   // transposing reads: 16-lane group g reads channels 8 g + 4 h + (l >> 2)
   // (+ 32 ks) at positions 16 pb + 4 (l & 3) .. +3, l = lane & 15
@@ -222,105 +306,98 @@ k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, c
   int troff[4];
 #pragma unroll
   for (int pb = 0; pb < 4; ++pb) troff[pb] = trow + (((2 * pb + ((sl & 3) >> 1)) ^ (2 * g)) << 4);
-  // this thread's destination of tile rows (tid >> 3) + 32 u
-  const int stoff = (tid >> 3) * kRow + (((tid & 7) ^ tile_swz(tid >> 3)) << 4);
+  // consumer results: row sl of the wave's block, bytes 32 pb + 8 g (chunk
+  // 2 pb + (g >> 1) before the row's swizzle)
+  unsigned char* cres = obuf + cw * kOutWave + sl * kRow + 8 * (g & 1);
 
-  // results of the previous tile, bf16: expert orow at positions 16 pb + 4 g
-  // .. +3 of tile (pb_img, pj); written through the wave's output area so
-  // that lane i stores 16 bytes of row i >> 3 (+8)
-  u32x2 prev[4];
-  int pb_img = b, pj = j;
-  auto emit = [&]() __attribute__((always_inline)) {
+  // store waves: tile (pimg, pj) of the buffer written a step earlier; lane
+  // i of store wave w writes physical chunk i & 7 of rows 8 h + (i >> 3) of
+  // consumer blocks 2 w and 2 w + 1
+  int pimg = b, pj = j;
+  auto store_results = [&](const unsigned char* ob) __attribute__((always_inline)) {
+    const int sw = wv - kConsumers - kLoaders;
 #pragma unroll
-    for (int pb = 0; pb < 4; ++pb) *reinterpret_cast<u32x2*>(outw + sl * kOutRow + 32 * pb + 8 * g) = prev[pb];
-    const int pos = pj * kTile + 8 * (lane & 7);
+    for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int r = (lane >> 3) + 8 * h;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(outw + r * kOutRow + (lane & 7) * 16);
-      const int o = kExpertsPerWave * wv + r;
-      if (o < p.E && pos < p.HW) *reinterpret_cast<u32x4*>(y + ((int64_t)pb_img * p.E + o) * p.HW + pos) = v;
-    }
+      for (int h = 0; h < 2; ++h) {
+        const int r = 8 * h + (lane >> 3);
+        const int blk = 2 * sw + c2;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(ob + blk * kOutWave + r * kRow + (lane & 7) * 16);
+        const int o = kExpertsPerWave * blk + r;
+        const int pos = pj * kTile + 8 * ((lane & 7) ^ (r & 7));
+        if (o < p.E && pos < p.HW) *reinterpret_cast<u32x4*>(y + ((int64_t)pimg * p.E + o) * p.HW + pos) = v;
+      }
   };
 
-  // Tile n: the previous tile's results leave, tile n + 2 is requested into
-  // the registers tile n came through, and the products of tile n run with
-  // tile n + 1 written into the other buffer a row chunk per channel step
-  // (waiting for tile n + 1 only).  The other buffer is free: the barrier
-  // that ended the previous step (or the rebuild) follows the last reads of
-  // tile n - 1.
-  auto step = [&](int n, auto first, u32x4(&refill)[NR], const u32x4(&next)[NR]) __attribute__((always_inline)) {
-    if constexpr (!decltype(first)::value) emit();
-    load_tile(p, x, min(n + 2, t1 - 1), refill, tid);
-    unsigned char* other = smem + ((n - t0 + 1) & 1) * tileb + stoff;
-    const unsigned char* tb = smem + ((n - t0) & 1) * tileb;
-    f32x4 acc[4];
+  for (int n = t0; n < t1; ++n, ++j) {
+    if (j == p.nt) {
+      ++b;
+      j = 0;
+    }
+    if (n == t0 || j == 0) {
+      // first tile or next image: the consumers (re)build their rows of A_b
+      // (the other waves carry on)
+      if (consumer) {
+        if (n != t0) {
+          fetch_coefs(p, alpha, b, wc, cw, lane);
+          __builtin_amdgcn_s_waitcnt(vm_wait(0));
+        }
+        build_coefs<NS, NR>(p, b, s, alpha, wc, rows, bfr, cw, lane);
+      }
+    }
+    if (n == t0) {
+      // tile t0 complete and visible (its copies ran during the build)
+      if (loader) wait_next_tile<NR>(t0 - 1, t1);
+      lds_barrier();
+    }
+    if (consumer) {
+      const unsigned char* tb = ring + ((n - t0) & (kRing - 1)) * tileb;
+      // software pipeline: the operands of channel step ks + 1 are read
+      // while the 4 NS products of step ks run, ordered so that consecutive
+      // products update different accumulators
+      auto read_step = [&](int ks, bf16x8 (&xa)[4]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int pb = 0; pb < 4; ++pb) acc[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int pb = 0; pb < 4; ++pb) {
+          const unsigned char* ap = tb + troff[pb] + ks * 32 * kRow;
+          xa[pb] = __builtin_shufflevector(tr_read(ap), tr_read(ap + 4 * kRow), 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+      };
+      f32x4 acc[4];
 #pragma unroll
-    for (int ks = 0; ks < NR; ++ks) {
+      for (int pb = 0; pb < 4; ++pb) acc[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      bf16x8 xa[2][4];
+      read_step(0, xa[0]);
 #pragma unroll
-      for (int pb = 0; pb < 4; ++pb) {
-        const unsigned char* ap = tb + troff[pb] + ks * 32 * kRow;
-        const bf16x8 xa = __builtin_shufflevector(tr_read(ap), tr_read(ap + 4 * kRow), 0, 1, 2, 3, 4, 5, 6, 7);
+      for (int ks = 0; ks < NR; ++ks) {
+        if (ks + 1 < NR) read_step(ks + 1, xa[(ks + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int part = 0; part < NS; ++part)
-          acc[pb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, bfr[part][ks], acc[pb], 0, 0, 0);
+#pragma unroll
+          for (int pb = 0; pb < 4; ++pb)
+            acc[pb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[ks & 1][pb], bfr[part][ks], acc[pb], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      *reinterpret_cast<u32x4*>(other + ks * 32 * kRow) = next[ks];
+      unsigned char* ob = cres + ((n - t0) & 1) * (kConsumers * kOutWave);
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+        *reinterpret_cast<u32x2*>(ob + (((2 * pb + (g >> 1)) ^ (sl & 7)) << 4)) =
+            u32x2{pack_bf16x2(acc[pb][0], acc[pb][1]), pack_bf16x2(acc[pb][2], acc[pb][3])};
+    } else if (loader) {
+      // tile n + 3 into the buffer tile n - 1 left (free since the last
+      // barrier), then wait until tile n + 1 is complete
+      if (n + 3 < t1) copy_tile<NR>(p, x, n + 3, ring + ((n - t0 + 3) & (kRing - 1)) * tileb, lt);
+      wait_next_tile<NR>(n, t1);
+    } else if (n > t0) {
+      store_results(obuf + ((n - 1 - t0) & 1) * (kConsumers * kOutWave));
     }
-#pragma unroll
-    for (int pb = 0; pb < 4; ++pb)
-      prev[pb] = u32x2{pack_bf16x2(acc[pb][0], acc[pb][1]), pack_bf16x2(acc[pb][2], acc[pb][3])};
-    pb_img = b;
-    pj = j;
-    __syncthreads();  // tile n + 1 visible; every read of tile n done
-  };
-
-  // tiles t0 + 1 ..: one image at a time, A_b rebuilt unconditionally at the
-  // start of each image's run, so that the operand registers are never merged
-  // across a conditional rebuild
-  auto run = [&](int n, int te) __attribute__((always_inline)) {
-#pragma unroll 2
-    for (; n < te; ++n, ++j) {
-      step(n, std::false_type{}, st0, st1);
-      // tile n + 2 now sits in st0 and tile n + 1 has left st1
-      u32x4 sw[NR];
-#pragma unroll
-      for (int u = 0; u < NR; ++u) sw[u] = st0[u];
-#pragma unroll
-      for (int u = 0; u < NR; ++u) st0[u] = st1[u];
-#pragma unroll
-      for (int u = 0; u < NR; ++u) st1[u] = sw[u];
+    if (storer) {
+      pimg = b;
+      pj = j;
     }
-  };
-
-  step(t0, std::true_type{}, st0, st1);
-  {
-    u32x4 sw[NR];
-#pragma unroll
-    for (int u = 0; u < NR; ++u) sw[u] = st0[u];
-#pragma unroll
-    for (int u = 0; u < NR; ++u) st0[u] = st1[u];
-#pragma unroll
-    for (int u = 0; u < NR; ++u) st1[u] = sw[u];
+    lds_barrier();  // tile n + 1 complete and visible; results of tile n visible; reads of tile n done
   }
-  ++j;
-  int n = t0 + 1;
-  run(n, min(t1, (b + 1) * p.nt));
-  n = min(t1, (b + 1) * p.nt);
-  while (n < t1) {
-    // next image: this workgroup stalls on the coefficient loads, the other
-    // one on the CU keeps it busy
-    ++b;
-    j = 0;
-    fetch_coefs(p, alpha, b, a, tid);
-    build_coefs<NS, NR>(p, b, s, alpha, a, uch, slot, smem + ((n - t0 + 1) & 1) * tileb, bfr, tid, orow, g);
-    const int te = min(t1, (b + 1) * p.nt);
-    run(n, te);
-    n = te;
-  }
-  emit();
+  if (storer) store_results(obuf + ((t1 - 1 - t0) & 1) * (kConsumers * kOutWave));
 }
 
 using MfmaKernel = void (*)(MixArgs, const uint16_t*, uint16_t*, const int32_t*, const float*, const int32_t*);
@@ -333,7 +410,6 @@ MfmaKernel pick(int nr) {
 }
 
 constexpr int kParts = 3;
-constexpr int kPerCU = 2;
 
 }  // namespace
 
@@ -361,7 +437,7 @@ hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, cons
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     cus = 256;
-  const int grid = std::min(cus * kPerCU, p.ntiles);
+  const int grid = std::min(cus, p.ntiles);
   const size_t lds = mfma_lds(p.C);
   const MfmaKernel k = pick<kParts>(p.C / 32);
   static bool configured[8] = {};
