@@ -88,9 +88,12 @@ __host__ __device__ inline size_t mfma_lds(int C) {
 }
 
 // Chunk q (16 bytes = 8 positions) of channel row c of a tile is stored at
-// chunk q ^ (2 ((c >> 3) & 3)): the 16 rows x 32 bytes that one transposing
-// read touches then fall on the LDS banks two deep, the least possible.
-__device__ __forceinline__ int tile_swz(int c) { return ((c >> 3) & 3) << 1; }
+// chunk q ^ tile_swz(c).  One transposing read fetches 8 bytes per lane from
+// rows 8 g + 4 h + (l >> 2) (+ 32 ks) of 16-lane group g, two chunks per row;
+// with 64 banks of 4 bytes, rows of equal parity collide unless their chunks
+// differ, so the swizzle takes bits 1 and 3 of the row: the 16 lanes of a
+// group, and the 32 of two neighbouring groups, then fall on distinct banks.
+__device__ __forceinline__ int tile_swz(int c) { return (((c >> 1) & 1) << 1) | (((c >> 3) & 1) << 2); }
 
 // Byte offset of A_b[o][c] in the staging area [kMaxE][C] bf16, whose 16-byte
 // chunks are rotated by 4 (o & 3) within the row so that the operand reads
@@ -305,7 +308,7 @@ k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, c
   const int trow = (8 * g + (sl >> 2)) * kRow + 8 * (sl & 1);
   int troff[4];
 #pragma unroll
-  for (int pb = 0; pb < 4; ++pb) troff[pb] = trow + (((2 * pb + ((sl & 3) >> 1)) ^ (2 * g)) << 4);
+  for (int pb = 0; pb < 4; ++pb) troff[pb] = trow + (((2 * pb + ((sl & 3) >> 1)) ^ tile_swz(8 * g + (sl >> 2))) << 4);
   // consumer results: row sl of the wave's block, bytes 32 pb + 8 g (chunk
   // 2 pb + (g >> 1) before the row's swizzle)
   unsigned char* cres = obuf + cw * kOutWave + sl * kRow + 8 * (g & 1);
