@@ -48,6 +48,43 @@ k_gate_softplus(const float* __restrict__ d, const int32_t* __restrict__ s, cons
                    lse ? lse + item : nullptr);
 }
 
+// The same for k <= W (W = 32 or 64): segments of W lanes, one per (image,
+// expert), 64 / W per wave, lane i of a segment holding support position i.
+// Every input of a position is read up front (the selected logit too), so the
+// only dependent reads are the descriptor gathers; the exponentials are
+// formed once and reused for the coefficients.
+template <int W>
+__global__ void __launch_bounds__(kGateWaves * kWave)
+k_gate_softplus_seg(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
+                    const float* __restrict__ a, const float* __restrict__ c, float* __restrict__ tau,
+                    float* __restrict__ alpha, float* __restrict__ lse, int64_t B, int64_t C, int R, int k) {
+  constexpr int kSeg = kWave / W;
+  const int lane = threadIdx.x & 63;
+  const int i = lane & (W - 1);
+  const int64_t item = ((int64_t)blockIdx.x * kGateWaves + (threadIdx.x >> 6)) * kSeg + lane / W;
+  const bool live = item < B * R;
+  const int64_t it = live ? item : B * R - 1;
+  const int64_t b = it / R;
+  const int o = (int)(it % R);
+  const bool in = i < k;
+  const int64_t e = (int64_t)o * k + (in ? i : 0);
+  const int ch = s[e];
+  const float av = a[e];
+  const float wv = w[e];
+  const float co = c[o];
+  float g = in ? av * d[b * C + ch] : 0.f;
+  g = wave_sum<W>(g) + co;
+  const float t = softplusf(g) + 1e-3f;
+  const float z = wv / t;
+  const float m = wave_max<W>(in ? z : -INFINITY);
+  const float ex = in ? expf(z - m) : 0.f;
+  const float zs = wave_sum<W>(ex);
+  if (!live) return;
+  if (i == 0) tau[item] = t;
+  if (alpha && in) alpha[item * k + i] = ex / zs;
+  if (lse && i == 0) lse[item] = m + logf(zs);
+}
+
 // The paper's shared gate: h = ReLU(W1 z + b1), g = w2 . h + b2,
 // tau = tau_min + (tau_max - tau_min) sigmoid(g).  k <= 256 (4 hidden units
 // per lane at most).
@@ -88,7 +125,14 @@ hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const 
   if (sh.R == 0) return hipSuccess;
   const int64_t items = sh.B * sh.R;
   const unsigned blocks = (unsigned)((items + kGateWaves - 1) / kGateWaves);
-  if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR) {
+  if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 32) {
+    const unsigned b32 = (unsigned)((items + 2 * kGateWaves - 1) / (2 * kGateWaves));
+    hipLaunchKernelGGL(k_gate_softplus_seg<32>, dim3(b32), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
+                       tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
+  } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 64) {
+    hipLaunchKernelGGL(k_gate_softplus_seg<64>, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
+                       tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
+  } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR) {
     hipLaunchKernelGGL(k_gate_softplus, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
                        tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
   } else {
