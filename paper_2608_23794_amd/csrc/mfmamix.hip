@@ -255,53 +255,58 @@ __device__ __forceinline__ void wait_next_tile(int n, int t1) {
     __builtin_amdgcn_s_waitcnt(vm_wait(0));
 }
 
-// NR = C / 32 channel steps of 32, NS coefficient parts.
-template <int NR, int NS>
-__global__ void __launch_bounds__(kThreads, 1)
-k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, const int32_t* __restrict__ s,
-          const float* __restrict__ alpha, const int32_t* __restrict__ U) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int G = gridDim.x;
-  const int t0 = (int)((int64_t)blockIdx.x * p.ntiles / G);
-  const int t1 = (int)((int64_t)(blockIdx.x + 1) * p.ntiles / G);
-  if (t0 >= t1) return;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool consumer = wv < kConsumers;
-  const bool loader = !consumer && wv < kConsumers + kLoaders;
-  const bool storer = wv >= kConsumers + kLoaders;
-  const int tileb = p.C * kRow;
-  unsigned char* ring = smem;
-  unsigned char* stage = smem + kRing * tileb;
-  unsigned char* obuf = stage + kConsumers * kStageRows * p.C * 2;  // two buffers of kConsumers * kOutWave bytes
-  const int cw = wv & (kConsumers - 1);
-  const int orow = kExpertsPerWave * cw + (lane & 15);  // consumer lane's expert (operand row, output column)
-  const int g = lane >> 4, sl = lane & 15;
-  const int lt = tid - kCThreads;                        // loader lane
+// ---- one workgroup's pass over the tiles [t0, t1) -------------------------
+//
+// The three roles run separate loops (so that the registers one of them
+// needs never constrain another) with the same barrier sequence: the
+// prologue's barrier, at the first tile a barrier once tile t0 is in LDS, and
+// one barrier at the end of every tile.
+struct Run {
+  MixArgs p;
+  int t0, t1;          // tiles b * nt + j of the pass
+  int tid, lane, wv;
+  int tileb;           // bytes of one LDS tile buffer
+  unsigned char* ring;   // kRing tile buffers
+  unsigned char* stage;  // the consumer waves' staging rows
+  unsigned char* obuf;   // two output buffers of kConsumers * kOutWave bytes
+};
 
-  // Loaders request tile t0 first; consumers read the first image's
-  // coefficients, their staging slots and the uncovered channels before the
-  // rest of the tiles is requested (every workgroup starting at once would
-  // otherwise queue these small reads behind megabytes of tiles).  The
-  // consumers build their rows of A_b at the first step, like at every image
-  // change (one copy of that code keeps the kernel small in the instruction
-  // cache).
-  if (loader) copy_tile<NR>(p, x, t0, ring, lt);
-  int b = t0 / p.nt, j = t0 - b * p.nt;
+__device__ __forceinline__ Run make_run(const MixArgs& p, int t0, int t1, unsigned char* smem) {
+  Run r;
+  r.p = p;
+  r.t0 = t0;
+  r.t1 = t1;
+  r.tid = threadIdx.x;
+  r.lane = r.tid & 63;
+  r.wv = __builtin_amdgcn_readfirstlane(r.tid >> 6);
+  r.tileb = p.C * kRow;
+  r.ring = smem;
+  r.stage = smem + kRing * r.tileb;
+  r.obuf = r.stage + kConsumers * kStageRows * p.C * 2;
+  return r;
+}
+
+__device__ __forceinline__ unsigned char* out_buffer(const Run& r, int n) {
+  return r.obuf + ((n - r.t0) & 1) * (kConsumers * kOutWave);
+}
+
+// Consumer waves: the staging slots and the coefficients of the first image
+// are read before the prologue's barrier,
+// and the wave's rows of A_b are rebuilt at the first tile and at every image
+// change.
+template <int NR, int NS>
+__device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __restrict__ s,
+                                             const int32_t* __restrict__ U, const float* __restrict__ alpha) {
+  const MixArgs& p = r.p;
+  const int lane = r.lane, cw = r.wv;
+  const int g = lane >> 4, sl = lane & 15;
+  int b = r.t0 / p.nt, j = r.t0 - b * p.nt;
   WaveCoefs wc;
-  unsigned char* rows = stage + cw * (kStageRows * p.C * 2);
-  if (consumer) {
-    wave_slots(p, s, U, wc, cw, lane);
-    fetch_coefs(p, alpha, b, wc, cw, lane);
-    __builtin_amdgcn_s_waitcnt(vm_wait(0));
-  }
+  unsigned char* rows = r.stage + cw * (kStageRows * p.C * 2);
+  wave_slots(p, s, U, wc, cw, lane);
+  fetch_coefs(p, alpha, b, wc, cw, lane);
+  __builtin_amdgcn_s_waitcnt(vm_wait(0));
   lds_barrier();
-  if (loader) {
-    if (t0 + 1 < t1) copy_tile<NR>(p, x, t0 + 1, ring + tileb, lt);
-    if (t0 + 2 < t1) copy_tile<NR>(p, x, t0 + 2, ring + 2 * tileb, lt);
-  }
-  bf16x8 bfr[NS][NR];
 
   // transposing reads: 16-lane group g reads channels 8 g + 4 h + (l >> 2)
   // (+ 32 ks) at positions 16 pb + 4 (l & 3) .. +3, l = lane & 15
@@ -309,98 +314,158 @@ k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, c
   int troff[4];
 #pragma unroll
   for (int pb = 0; pb < 4; ++pb) troff[pb] = trow + (((2 * pb + ((sl & 3) >> 1)) ^ tile_swz(8 * g + (sl >> 2))) << 4);
-  // consumer results: row sl of the wave's block, bytes 32 pb + 8 g (chunk
-  // 2 pb + (g >> 1) before the row's swizzle)
-  unsigned char* cres = obuf + cw * kOutWave + sl * kRow + 8 * (g & 1);
+  // results: row sl of the wave's block, bytes 32 pb + 8 g (chunk 2 pb +
+  // (g >> 1) before the row's swizzle)
+  const int cres = cw * kOutWave + sl * kRow + 8 * (g & 1);
 
-  // store waves: tile (pimg, pj) of the buffer written a step earlier; lane
-  // i of store wave w writes physical chunk i & 7 of rows 8 h + (i >> 3) of
-  // consumer blocks 2 w and 2 w + 1
-  int pimg = b, pj = j;
-  auto store_results = [&](const unsigned char* ob) __attribute__((always_inline)) {
-    const int sw = wv - kConsumers - kLoaders;
-#pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int r = 8 * h + (lane >> 3);
-        const int blk = 2 * sw + c2;
-        const u32x4 v = *reinterpret_cast<const u32x4*>(ob + blk * kOutWave + r * kRow + (lane & 7) * 16);
-        const int o = kExpertsPerWave * blk + r;
-        const int pos = pj * kTile + 8 * ((lane & 7) ^ (r & 7));
-        if (o < p.E && pos < p.HW) *reinterpret_cast<u32x4*>(y + ((int64_t)pimg * p.E + o) * p.HW + pos) = v;
-      }
-  };
-
-  for (int n = t0; n < t1; ++n, ++j) {
+  bf16x8 bfr[NS][NR];
+  for (int n = r.t0; n < r.t1; ++n, ++j) {
     if (j == p.nt) {
       ++b;
       j = 0;
     }
-    if (n == t0 || j == 0) {
-      // first tile or next image: the consumers (re)build their rows of A_b
-      // (the other waves carry on)
-      if (consumer) {
-        if (n != t0) {
-          fetch_coefs(p, alpha, b, wc, cw, lane);
-          __builtin_amdgcn_s_waitcnt(vm_wait(0));
-        }
-        build_coefs<NS, NR>(p, b, s, alpha, wc, rows, bfr, cw, lane);
+    if (n == r.t0 || j == 0) {
+      // first tile or next image: rebuild this wave's rows of A_b.  The old
+      // operands are dead from here (each lane's are rewritten by one of the
+      // build's passes); a constant frees their registers meanwhile.
+#pragma unroll
+      for (int part = 0; part < NS; ++part)
+#pragma unroll
+        for (int ks = 0; ks < NR; ++ks) bfr[part][ks] = bf16x8{};
+      if (n != r.t0) {
+        fetch_coefs(p, alpha, b, wc, cw, lane);
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
       }
+      build_coefs<NS, NR>(p, b, s, alpha, wc, rows, bfr, cw, lane);
     }
-    if (n == t0) {
-      // tile t0 complete and visible (its copies ran during the build)
-      if (loader) wait_next_tile<NR>(t0 - 1, t1);
+    if (n == r.t0) lds_barrier();  // tile t0 in LDS
+
+    const unsigned char* tb = r.ring + ((n - r.t0) & (kRing - 1)) * r.tileb;
+    // software pipeline: the operands of channel step ks + 1 are read while
+    // the 4 NS products of step ks run, ordered so that consecutive products
+    // update different accumulators
+    auto read_step = [&](int ks, bf16x8 (&xa)[4]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb) {
+        const unsigned char* ap = tb + troff[pb] + ks * 32 * kRow;
+        xa[pb] = __builtin_shufflevector(tr_read(ap), tr_read(ap + 4 * kRow), 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    };
+    f32x4 acc[4];
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) acc[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bf16x8 xa[2][4];
+    read_step(0, xa[0]);
+#pragma unroll
+    for (int ks = 0; ks < NR; ++ks) {
+      if (ks + 1 < NR) read_step(ks + 1, xa[(ks + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int part = 0; part < NS; ++part)
+#pragma unroll
+        for (int pb = 0; pb < 4; ++pb)
+          acc[pb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[ks & 1][pb], bfr[part][ks], acc[pb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    unsigned char* ob = out_buffer(r, n) + cres;
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb)
+      *reinterpret_cast<u32x2*>(ob + (((2 * pb + (g >> 1)) ^ (sl & 7)) << 4)) =
+          u32x2{pack_bf16x2(acc[pb][0], acc[pb][1]), pack_bf16x2(acc[pb][2], acc[pb][3])};
+    lds_barrier();  // results of tile n visible; reads of tile n done
+  }
+}
+
+// Loader waves: tile t0 is requested first, before the prologue's barrier
+// (every workgroup starting at once would otherwise queue the consumers'
+// small coefficient reads behind megabytes of tiles), then up to three
+// tiles stay in flight.
+template <int NR>
+__device__ __forceinline__ void loader_run(const Run& r, const uint16_t* __restrict__ x) {
+  const MixArgs& p = r.p;
+  const int lt = r.tid - kCThreads;
+  copy_tile<NR>(p, x, r.t0, r.ring, lt);
+  lds_barrier();
+  if (r.t0 + 1 < r.t1) copy_tile<NR>(p, x, r.t0 + 1, r.ring + r.tileb, lt);
+  if (r.t0 + 2 < r.t1) copy_tile<NR>(p, x, r.t0 + 2, r.ring + 2 * r.tileb, lt);
+  for (int n = r.t0; n < r.t1; ++n) {
+    if (n == r.t0) {
+      wait_next_tile<NR>(r.t0 - 1, r.t1);  // tile t0 complete
       lds_barrier();
     }
-    if (consumer) {
-      const unsigned char* tb = ring + ((n - t0) & (kRing - 1)) * tileb;
-      // software pipeline: the operands of channel step ks + 1 are read
-      // while the 4 NS products of step ks run, ordered so that consecutive
-      // products update different accumulators
-      auto read_step = [&](int ks, bf16x8 (&xa)[4]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int pb = 0; pb < 4; ++pb) {
-          const unsigned char* ap = tb + troff[pb] + ks * 32 * kRow;
-          xa[pb] = __builtin_shufflevector(tr_read(ap), tr_read(ap + 4 * kRow), 0, 1, 2, 3, 4, 5, 6, 7);
-        }
-      };
-      f32x4 acc[4];
-#pragma unroll
-      for (int pb = 0; pb < 4; ++pb) acc[pb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      bf16x8 xa[2][4];
-      read_step(0, xa[0]);
-#pragma unroll
-      for (int ks = 0; ks < NR; ++ks) {
-        if (ks + 1 < NR) read_step(ks + 1, xa[(ks + 1) & 1]);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int part = 0; part < NS; ++part)
-#pragma unroll
-          for (int pb = 0; pb < 4; ++pb)
-            acc[pb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[ks & 1][pb], bfr[part][ks], acc[pb], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      unsigned char* ob = cres + ((n - t0) & 1) * (kConsumers * kOutWave);
-#pragma unroll
-      for (int pb = 0; pb < 4; ++pb)
-        *reinterpret_cast<u32x2*>(ob + (((2 * pb + (g >> 1)) ^ (sl & 7)) << 4)) =
-            u32x2{pack_bf16x2(acc[pb][0], acc[pb][1]), pack_bf16x2(acc[pb][2], acc[pb][3])};
-    } else if (loader) {
-      // tile n + 3 into the buffer tile n - 1 left (free since the last
-      // barrier), then wait until tile n + 1 is complete
-      if (n + 3 < t1) copy_tile<NR>(p, x, n + 3, ring + ((n - t0 + 3) & (kRing - 1)) * tileb, lt);
-      wait_next_tile<NR>(n, t1);
-    } else if (n > t0) {
-      store_results(obuf + ((n - 1 - t0) & 1) * (kConsumers * kOutWave));
-    }
-    if (storer) {
-      pimg = b;
-      pj = j;
-    }
-    lds_barrier();  // tile n + 1 complete and visible; results of tile n visible; reads of tile n done
+    // tile n + 3 into the buffer tile n - 1 left (free since the last
+    // barrier), then wait until tile n + 1 is complete
+    if (n + 3 < r.t1) copy_tile<NR>(p, x, n + 3, r.ring + ((n - r.t0 + 3) & (kRing - 1)) * r.tileb, lt);
+    wait_next_tile<NR>(n, r.t1);
+    lds_barrier();  // tile n + 1 complete and visible
   }
-  if (storer) store_results(obuf + ((t1 - 1 - t0) & 1) * (kConsumers * kOutWave));
+}
+
+// Store waves: the results of each tile go out during the next tile's step,
+// the last tile's after the loop.
+__device__ __forceinline__ void store_run(const Run& r, uint16_t* __restrict__ y) {
+  const MixArgs& p = r.p;
+  const int lane = r.lane;
+  const int sw = r.wv - kConsumers - kLoaders;
+  int b = r.t0 / p.nt, j = r.t0 - b * p.nt;
+  lds_barrier();
+
+  // results of tile (pimg, pj) from its output buffer: lane i of store wave w
+  // writes physical chunk i & 7 of rows 8 h + (i >> 3) of consumer blocks
+  // 2 w and 2 w + 1
+  int pimg = b, pj = j;
+  auto store_results = [&](const unsigned char* ob) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int rr = 8 * h + (lane >> 3);
+        const int blk = 2 * sw + c2;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(ob + blk * kOutWave + rr * kRow + (lane & 7) * 16);
+        const int o = kExpertsPerWave * blk + rr;
+        const int pos = pj * kTile + 8 * ((lane & 7) ^ (rr & 7));
+        if (o < p.E && pos < p.HW) *reinterpret_cast<u32x4*>(y + ((int64_t)pimg * p.E + o) * p.HW + pos) = v;
+      }
+  };
+
+  for (int n = r.t0; n < r.t1; ++n, ++j) {
+    if (j == p.nt) {
+      ++b;
+      j = 0;
+    }
+    if (n == r.t0) lds_barrier();  // tile t0 in LDS
+    if (n > r.t0) store_results(out_buffer(r, n - 1));
+    pimg = b;
+    pj = j;
+    lds_barrier();  // results of tile n visible
+  }
+  store_results(out_buffer(r, r.t1 - 1));
+}
+
+template <int NR, int NS>
+__device__ __forceinline__ void run_tiles(const Run& r, const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                                          const int32_t* __restrict__ s, const int32_t* __restrict__ U,
+                                          const float* __restrict__ alpha) {
+  if (r.wv < kConsumers)
+    consumer_run<NR, NS>(r, s, U, alpha);
+  else if (r.wv < kConsumers + kLoaders)
+    loader_run<NR>(r, x);
+  else
+    store_run(r, y);
+}
+
+// NR = C / 32 channel steps of 32, NS coefficient parts.  One contiguous
+// range of tiles per workgroup.
+template <int NR, int NS>
+__global__ void __launch_bounds__(kThreads, 1)
+k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, const int32_t* __restrict__ s,
+          const float* __restrict__ alpha, const int32_t* __restrict__ U) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int t0 = (int)((int64_t)blockIdx.x * p.ntiles / gridDim.x);
+  const int t1 = (int)((int64_t)(blockIdx.x + 1) * p.ntiles / gridDim.x);
+  if (t0 >= t1) return;
+  const Run r = make_run(p, t0, t1, smem);
+  run_tiles<NR, NS>(r, x, y, s, U, alpha);
 }
 
 using MfmaKernel = void (*)(MixArgs, const uint16_t*, uint16_t*, const int32_t*, const float*, const int32_t*);
@@ -424,8 +489,9 @@ bool mfmamix_eligible(const Shape& sh) {
   return true;
 }
 
-hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
-                          int nU, void* y, hipStream_t st) {
+namespace {
+
+MixArgs mix_args(const Shape& sh, int nU) {
   MixArgs p;
   p.C = (int)sh.C;
   p.HW = (int)sh.HW;
@@ -435,20 +501,38 @@ hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, cons
   p.nU = nU;
   p.nt = (int)((sh.HW + kTile - 1) / kTile);
   p.ntiles = (int)(sh.B * p.nt);
-  if (p.ntiles == 0) return hipSuccess;
+  return p;
+}
+
+int cu_count() {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     cus = 256;
-  const int grid = std::min(cus, p.ntiles);
+  return cus;
+}
+
+// Raises the dynamic LDS limit of kernel k (once per kernel).
+template <typename K>
+hipError_t allow_lds(K k, size_t lds, bool& done) {
+  if (done) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e == hipSuccess) done = true;
+  return e;
+}
+
+}  // namespace
+
+hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
+                          int nU, void* y, hipStream_t st) {
+  const MixArgs p = mix_args(sh, nU);
+  if (p.ntiles == 0) return hipSuccess;
+  const int grid = std::min(cu_count(), p.ntiles);
   const size_t lds = mfma_lds(p.C);
   const MfmaKernel k = pick<kParts>(p.C / 32);
   static bool configured[8] = {};
-  if (!configured[p.C / 32 - 1]) {
-    const hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    configured[p.C / 32 - 1] = true;
-  }
+  const hipError_t e = allow_lds(k, lds, configured[p.C / 32 - 1]);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, st, p, static_cast<const uint16_t*>(x),
                      static_cast<uint16_t*>(y), s, alpha, U);
   return hipGetLastError();

@@ -348,6 +348,8 @@ MFMA = [
     (1, 160, 40, 20, 2, 4),      # eight positions in a single partial tile
     (2, 192, 48, 9, 7, 8),
     (3, 224, 20, 30, 6, 12),
+    (600, 64, 16, 2, 8, 8),      # one tile per image: a rebuild of A_b at every tile of a range
+    (300, 32, 32, 1, 4, 16),     # k = 1
 ]
 
 
