@@ -43,7 +43,37 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-context", action="store_true")
+    # after the measurements, copy this many MiB device to device five times:
+    # a plain copy kernel of known size against which hardware byte counters
+    # (rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE) are calibrated
+    p.add_argument("--copy-probe-mib", type=int, default=0)
     return p.parse_args()
+
+
+def measured_traffic(kernel: str):
+    """HBM-side bytes per launch of `kernel` from the committed rocprofv3 byte
+    counters (calibrated against a plain copy), or None when the kernel's
+    sources have changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "mix_resnet50_stage1_hbm_bytes.md")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for ln in open(path):
+        k, sep, v = ln.partition(":")
+        if sep and k.strip() in ("kernel", "sources", "sources_sha256", "traffic_bytes"):
+            rec[k.strip()] = v.strip()
+    if rec.get("kernel") != kernel or "sources" not in rec:
+        return None
+    h = hashlib.sha256()
+    for f in rec["sources"].split():
+        fp = os.path.join(ROOT, f)
+        if not os.path.exists(fp):
+            return None
+        h.update(open(fp, "rb").read())
+    if h.hexdigest() != rec.get("sources_sha256"):
+        return None
+    return int(rec["traffic_bytes"])
 
 
 def event_time_ms(fn, n, stream):
@@ -148,7 +178,9 @@ def main():
         "rotation_sets": nsets,
         "kernels_us": {n: round(v[0] * 1e3, 2) for n, v in kernels.items()},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("k_mfmamix<8, 3>")
+                     if dom == "mix" and path == mb.PATH_MFMA and wl.name == "resnet50_stage1" else None,
                      "algorithmic_bytes": dom_bytes},
     }
 
@@ -186,6 +218,13 @@ def main():
                                 "cores": oracle.threads(), "kind": "oracle",
                                 "sample": f"{passes} full-batch forward passes of {wl.name} (B={B}), "
                                           f"{per_pass * 1e3:.1f} ms each, os.cpu_count()={os.cpu_count()}"}
+    if args.copy_probe_mib > 0:
+        n = args.copy_probe_mib * 2 ** 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
     print(json.dumps(line), flush=True)
 
 
