@@ -22,23 +22,43 @@ def test_more_than_one_gpu_is_refused():
 
 
 def _tree(tmp_path, edit=None):
-    for f in (PROFILE,) + SOURCES:
+    """A copy of the sources with a counter record taken for exactly these sources, then `edit` appended to."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in SOURCES:
         dst = tmp_path / f
         dst.parent.mkdir(parents=True, exist_ok=True)
         shutil.copy(os.path.join(ROOT, f), dst)
+        h.update(open(dst, "rb").read())
+    lines = []
+    for ln in open(os.path.join(ROOT, PROFILE)):
+        if ln.startswith("sources_sha256:"):
+            ln = f"sources_sha256: {h.hexdigest()}\n"
+        lines.append(ln)
+    (tmp_path / PROFILE).parent.mkdir(parents=True, exist_ok=True)
+    (tmp_path / PROFILE).write_text("".join(lines))
     if edit:
         with open(tmp_path / edit, "a") as fh:
             fh.write("\n// edited\n")
     return str(tmp_path)
 
 
-def test_traffic_record_matches_current_sources():
+def test_traffic_record_is_the_calibrated_counters():
+    """The reported figure is the record's calibrated sum while the sources hash to its value (null after a
+    change to the kernel, until the counters are taken again)."""
+    import hashlib
     rec = {}
     for ln in open(os.path.join(ROOT, PROFILE)):
         k, sep, v = ln.partition(":")
         if sep:
             rec[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for f in rec["sources"].split():
+        h.update(open(os.path.join(ROOT, f), "rb").read())
     t = bench.measured_traffic("k_mfmamix<8, 3>")
+    if h.hexdigest() != rec["sources_sha256"]:
+        assert t is None
+        return
     assert t == int(rec["traffic_bytes"])
     # the record is the calibrated sum of the two counters
     fetch = int(rec["fetch_kib_per_dispatch"]) * 1024 * float(rec["fetch_scale"])

@@ -453,3 +453,30 @@ def test_forward_reused_workspace_sees_new_inputs():
         ref = oracle.forward(x, g["s"], g["w"], wl.E, oracle.NCHW, a=g["a"], c=g["c"])
         y = layer.forward(to_device_x(x, wl.dtype), y, ws)
         check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
+
+
+MFMA_STAGES = [
+    # B, C, E, k, H, W: moce_forward against moce_pool + moce_gate + moce_mix on the MFMA path
+    (64, 256, 64, 32, 56, 56),   # the ResNet-50 stage-1 layer
+    (5, 128, 24, 64, 12, 16),    # k = 64: 64-lane segments, two passes per group
+    (9, 32, 8, 3, 8, 8),         # C = 32, one partial expert group, k not a power of two
+    (3, 96, 40, 20, 6, 12),      # three expert groups, the last partial; ragged last tile (72 positions)
+    (2, 64, 17, 8, 4, 4),        # the residual row alone in the second group
+]
+
+
+@pytest.mark.parametrize("B,C,E,k,H,W", MFMA_STAGES)
+def test_mfma_forward_equals_stages(B, C, E, k, H, W):
+    """The whole-layer entry point gives the same bits as the three stage entry points in a row."""
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=11 * B + k, signed=(E % 2 == 1))
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_MFMA
+    xd = to_device_x(x, "bf16")
+    y = layer.forward(xd)
+    d = layer.pool(xd)
+    _, alpha = layer.gate_tau(d)
+    y_st = layer.mix(xd, alpha)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y_st.view(torch.int16))
+    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
+    check_y(to_host_f64(y), ref["y"], ref["mag"], "bf16")
