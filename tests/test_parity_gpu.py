@@ -458,7 +458,9 @@ def test_forward_reused_workspace_sees_new_inputs():
 MFMA_STAGES = [
     # B, C, E, k, H, W: moce_forward against moce_pool + moce_gate + moce_mix on the MFMA path
     (64, 256, 64, 32, 56, 56),   # the ResNet-50 stage-1 layer
-    (5, 128, 24, 64, 12, 16),    # k = 64: 64-lane segments, two passes per group
+    (24, 256, 64, 32, 56, 56),   # workgroup ranges that straddle images (a rebuild mid-range)
+    (600, 64, 16, 2, 8, 8),      # ranges over three images
+    (5, 128, 24, 64, 12, 16),    # k = 64: the gate kernel's 64-lane segments
     (9, 32, 8, 3, 8, 8),         # C = 32, one partial expert group, k not a power of two
     (3, 96, 40, 20, 6, 12),      # three expert groups, the last partial; ragged last tile (72 positions)
     (2, 64, 17, 8, 4, 4),        # the residual row alone in the second group
