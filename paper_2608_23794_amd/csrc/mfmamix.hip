@@ -17,19 +17,22 @@
 //
 // Work split.  One workgroup per CU walks a contiguous range of tiles (64
 // positions x all C channels of one image) with three kinds of waves, so
-// that no wave that computes ever waits behind the memory system.  Two loader
-// waves copy each tile straight from HBM into a ring of four LDS tile buffers
-// (global-to-LDS loads, no registers), keeping up to three tiles in flight,
-// and wait for their own copies with explicit counters.  Four consumer waves
-// only compute: wave w multiplies experts 16 w .. 16 w + 15 at all 64
-// positions, holding its 16 rows of A_b (all channels, every part) in
-// registers as MFMA B operands and reading the x tile as MFMA A operands with
-// the transposing LDS read, which turns the position-contiguous channel rows
-// into channel-contiguous operands; results go to an LDS output buffer.  Two
-// store waves write the previous tile's results from there to y, whole
-// 128-byte rows per store.  All waves meet at one barrier per tile.  When the
-// image changes each consumer wave rebuilds its own rows of A_b, 8 at a time,
-// in its own staging area, while the other waves carry on.
+// that no wave that computes ever waits behind the memory system; each kind
+// runs its own loop over the tiles, and all waves meet at one barrier per
+// tile.  Two loader waves copy each tile straight into a ring of four LDS
+// tile buffers (global-to-LDS loads, no registers; in the forward x mostly
+// comes back from the infinity cache, where the pooling kernel left it),
+// keeping up to three tiles in flight, and wait for their own copies with
+// explicit counters.  Four consumer waves only compute: wave w multiplies
+// experts 16 w .. 16 w + 15 at all 64 positions, holding its 16 rows of A_b
+// (all channels, every part) in registers as MFMA B operands and reading the
+// x tile as MFMA A operands with the transposing LDS read, which turns the
+// position-contiguous channel rows into channel-contiguous operands; results
+// go to an LDS output buffer.  Two store waves write the previous tile's
+// results from there to y, whole 128-byte rows per store.  The tile copies
+// and the stores of y carry the non-temporal hint.  When the image changes
+// each consumer wave rebuilds its own rows of A_b, 8 at a time, in its own
+// staging area, while the other waves carry on.
 #include <algorithm>
 #include <type_traits>
 
