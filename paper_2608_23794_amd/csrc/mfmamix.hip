@@ -525,15 +525,6 @@ int cu_count() {
   return cus;
 }
 
-// Raises the dynamic LDS limit of kernel k (once per kernel).
-template <typename K>
-hipError_t allow_lds(K k, size_t lds, bool& done) {
-  if (done) return hipSuccess;
-  const hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e == hipSuccess) done = true;
-  return e;
-}
-
 }  // namespace
 
 hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
@@ -543,8 +534,9 @@ hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, cons
   const int grid = std::min(cu_count(), p.ntiles);
   const size_t lds = mfma_lds(p.C);
   const MfmaKernel k = pick<kParts>(p.C / 32);
-  static bool configured[8] = {};
-  const hipError_t e = allow_lds(k, lds, configured[p.C / 32 - 1]);
+  // the dynamic LDS limit, set on the current device at every launch (the
+  // library keeps no state between calls)
+  const hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, st, p, static_cast<const uint16_t*>(x),
                      static_cast<uint16_t*>(y), s, alpha, U);
