@@ -30,8 +30,9 @@
 // position-contiguous channel rows into channel-contiguous operands; results
 // go to an LDS output buffer.  Two store waves write the previous tile's
 // results from there to y, whole 128-byte rows per store.  The tile copies
-// and the stores of y carry the non-temporal hint.  When the image changes
-// each consumer wave rebuilds its own rows of A_b, 8 at a time, in its own
+// and the stores of y carry the non-temporal hint.  At the first tile each
+// consumer wave builds its rows of A_b through the last ring buffer, still
+// free then; when the image changes it rebuilds them, 8 at a time, in its own
 // staging area, while the other waves carry on.
 #include <algorithm>
 #include <type_traits>
@@ -63,6 +64,7 @@ constexpr int kMaxC = 256;
 constexpr int kPre = 8;                         // coefficient entries per consumer lane fetched ahead
 constexpr int kUPer = kMaxC / 64;               // uncovered channels per lane of the residual's wave
 constexpr int kExpertsPerWave = 16;
+static_assert(kExpertsPerWave == 2 * kStageRows, "a rebuild takes two groups of staging rows");
 constexpr int kOutWave = kExpertsPerWave * kRow;  // one consumer wave's results for a tile
 
 // Workgroup barrier for LDS traffic: waits for this wave's own LDS (and
@@ -101,16 +103,22 @@ __host__ __device__ inline size_t mfma_lds(int C) {
 // group, and the 32 of two neighbouring groups, then fall on distinct banks.
 __device__ __forceinline__ int tile_swz(int c) { return (((c >> 1) & 1) << 1) | (((c >> 3) & 1) << 2); }
 
-// Byte offset of A_b[o][c] in the staging area [kMaxE][C] bf16, whose 16-byte
-// chunks are rotated by 4 (o & 3) within the row so that the operand reads
-// (16 rows x 64 bytes) spread over the banks.
-__device__ __forceinline__ int stage_off(int o, int c, int C) {
-  const int nch = C >> 3;
+// Byte offset of A_b[o][c] in a staging area [rows][C] bf16 (C = 32 NR),
+// whose 16-byte chunks are rotated by 4 (o & 3) within the row so that the
+// operand reads (16 rows x 64 bytes) spread over the banks.  C is a constant
+// of the kernel, so the row size and the rotation's wrap (c / 8 < C / 8 and
+// 4 (o & 3) <= 12) cost a few full-rate operations.
+template <int NR>
+__device__ __forceinline__ int stage_off(int o, int c) {
+  constexpr int nch = 4 * NR;  // 16-byte chunks per row
   int ch = (c >> 3) + 4 * (o & 3);
-  ch = ch >= nch ? ch - nch : ch;
-  ch = ch >= nch ? ch - nch : ch;
-  ch = ch >= nch ? ch - nch : ch;
-  return o * C * 2 + ch * 16 + (c & 7) * 2;
+  if constexpr ((nch & (nch - 1)) == 0) {
+    ch &= nch - 1;
+  } else {
+#pragma unroll
+    for (int t = 0; t <= 11 / nch; ++t) ch = ch >= nch ? ch - nch : ch;
+  }
+  return o * (64 * NR) + ch * 16 + (c & 7) * 2;
 }
 
 // Copies tile n into the LDS tile buffer `buf` with global-to-LDS loads, one
@@ -152,8 +160,8 @@ __device__ __forceinline__ uint16_t coef_part(float a, int part) {
 // A consumer wave's coefficients.  Entry i < 16 k of wave w is coefficient
 // i % k of expert 16 w + i / k, i.e. entry 16 w k + i of an image's flattened
 // [R][k] block; lane l handles entries l + 64 r.  slot[] holds their staging
-// slots, 16 bits each: (i / k) >> 3 << 14 (which group of 8 rows) | the byte
-// offset within the wave's staging rows, 0xffff for none.  uslot[] does the
+// slots, 16 bits each: the byte offset of the entry in a staging area of the
+// wave's 16 rows (below 32 C <= 8192), 0xffff for none.  uslot[] does the
 // same for the residual row's uncovered channels l + 64 u (only in the wave
 // holding row R).
 struct WaveCoefs {
@@ -164,29 +172,43 @@ struct WaveCoefs {
 
 __device__ __forceinline__ uint32_t half_of(uint32_t packed, int r) { return (packed >> (16 * (r & 1))) & 0xffffu; }
 
-__device__ __forceinline__ void wave_slots(const MixArgs& p, const int32_t* __restrict__ s,
-                                           const int32_t* __restrict__ U, WaveCoefs& wc, int cw, int lane) {
+// A lane's share of the wave's support indices (entries l + 64 r) and of the
+// uncovered channels (l + 64 u; U may be null when nU == 0, and s is read
+// instead).  The caller pins the results with empty asm statements, so that
+// every load is unconditional and all are issued before any is used: left to
+// itself the compiler moves each load into the branch that uses it and waits
+// for it there, one memory round trip per load.
+__device__ __forceinline__ void load_indices(const MixArgs& p, const int32_t* __restrict__ s,
+                                             const int32_t* __restrict__ U, int (&cs)[kPre], int (&cu)[kUPer], int cw,
+                                             int lane) {
   const int nent = p.R * p.k;
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) cs[r] = s[min(kExpertsPerWave * cw * p.k + lane + 64 * r, nent - 1)];
+#pragma unroll
+  for (int u = 0; u < kUPer; ++u) cu[u] = *(p.nU > 0 ? U + min(lane + 64 * u, p.nU - 1) : s);
+}
+
+template <int NR>
+__device__ __forceinline__ void wave_slots(const MixArgs& p, const int (&cs)[kPre], const int (&cu)[kUPer],
+                                           WaveCoefs& wc, int cw, int lane) {
+  const int nent = p.R * p.k;
+  const float rk = 1.f / (float)p.k;
 #pragma unroll
   for (int r = 0; r < kPre; ++r) {
     const int i = lane + 64 * r;
     const int e = kExpertsPerWave * cw * p.k + i;
-    const int c = s[min(e, nent - 1)];
-    const int eo = i / p.k;
-    const uint32_t v = (i < kExpertsPerWave * p.k && e < nent)
-                           ? (uint32_t)((eo >> 3) << 14 | stage_off(eo & (kStageRows - 1), c, p.C))
-                           : 0xffffu;
+    // i / k where it is used (i < 16 k): the float quotient of i + 1/2 is
+    // below 16 with a relative error of a few ulp, far inside its distance
+    // of at least 1 / (2 k) from an integer
+    const int eo = (int)(((float)i + 0.5f) * rk);
+    const uint32_t v = (i < kExpertsPerWave * p.k && e < nent) ? (uint32_t)stage_off<NR>(eo, cs[r]) : 0xffffu;
     wc.slot[r >> 1] = (r & 1) ? (wc.slot[r >> 1] | v << 16) : v;
   }
   const int ro = p.R - kExpertsPerWave * cw;  // the residual row within this wave's experts
 #pragma unroll
   for (int u = 0; u < kUPer; ++u) {
-    const int ui = lane + 64 * u;
-    // U may be null when nU == 0: s is read instead
-    const int c = *(p.nU > 0 ? U + min(ui, p.nU - 1) : s);
-    const uint32_t v = (ro >= 0 && ro < kExpertsPerWave && ui < p.nU)
-                           ? (uint32_t)((ro >> 3) << 14 | stage_off(ro & (kStageRows - 1), c, p.C))
-                           : 0xffffu;
+    const uint32_t v = (ro >= 0 && ro < kExpertsPerWave && lane + 64 * u < p.nU) ? (uint32_t)stage_off<NR>(ro, cu[u])
+                                                                                : 0xffffu;
     wc.uslot[u >> 1] = (u & 1) ? (wc.uslot[u >> 1] | v << 16) : v;
   }
 }
@@ -200,48 +222,112 @@ __device__ __forceinline__ void fetch_coefs(const MixArgs& p, const float* __res
   for (int r = 0; r < kPre; ++r) wc.a[r] = ab[min(first + lane + 64 * r, nent - 1)];
 }
 
-// Rebuilds a consumer wave's rows of A_b in registers through its own
-// staging rows (8 at a time, so no other wave is involved and no barrier is
-// needed: a wave's LDS accesses take effect in order).  For each group of 8
-// rows: zero them, then per part scatter part `part` of the coefficients
+// The exact split a = hi + mid + lo into bf16 parts (with two parts: hi and
+// the rounded remainder).
+template <int NS>
+__device__ __forceinline__ void split_parts(float a, uint16_t (&pt)[NS]) {
+  pt[0] = f32_to_bf16(a);
+  const float r1 = a - bf16_to_f32(pt[0]);
+  pt[1] = f32_to_bf16(r1);
+  if constexpr (NS > 2) pt[2] = f32_to_bf16(r1 - bf16_to_f32(pt[1]));
+}
+
+// Builds a consumer wave's rows of A_b in registers at the first tile,
+// through a staging area of all 16 rows (the last ring buffer, free until
+// tile t0 + 3 is requested): zero the rows, then per part scatter part
+// `part` of the coefficients (and 1/nU at the uncovered channels) and read
+// the MFMA B operands.  Every part lands on the same slots, so one zeroing
+// serves all, and a wave's LDS accesses take effect in order, so no barrier
+// is needed.  Empty slots write to `junk` (4 bytes per lane, never read)
+// rather than branch around the store.  Entries past 64 kPre are read here.
+template <int NS, int NR>
+__device__ __forceinline__ void build_first(const MixArgs& p, int b, const int32_t* __restrict__ s,
+                                            const float* __restrict__ alpha, const WaveCoefs& wc,
+                                            unsigned char* rows, unsigned char* junk, bf16x8 (&bfr)[NS][NR], int cw,
+                                            int lane) {
+  const int nent = p.R * p.k;
+  const float* ab = alpha + (int64_t)b * nent;
+  const int my = lane & 15;  // this lane's expert within the wave
+  const int g = lane >> 4;
+#pragma unroll
+  for (int q = 0; q < NR; ++q)  // 16 rows of 64 NR bytes: NR chunks per lane
+    reinterpret_cast<u32x4*>(rows)[lane + 64 * q] = u32x4{0u, 0u, 0u, 0u};
+  unsigned char* dst[kPre];
+  uint16_t pt[kPre][NS];
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) {
+    const uint32_t sl = half_of(wc.slot[r >> 1], r);
+    dst[r] = sl != 0xffffu ? rows + sl : junk + 4 * lane;
+    split_parts<NS>(wc.a[r], pt[r]);
+  }
+  unsigned char* udst[kUPer];
+#pragma unroll
+  for (int u = 0; u < kUPer; ++u) {
+    const uint32_t sl = half_of(wc.uslot[u >> 1], u);
+    udst[u] = sl != 0xffffu ? rows + sl : junk + 4 * lane;
+  }
+  uint16_t ipt[NS];
+  split_parts<NS>(p.nU > 0 ? 1.f / (float)p.nU : 0.f, ipt);
+#pragma unroll
+  for (int part = 0; part < NS; ++part) {
+#pragma unroll
+    for (int r = 0; r < kPre; ++r) *reinterpret_cast<uint16_t*>(dst[r]) = pt[r][part];
+    for (int i = lane + 64 * kPre; i < kExpertsPerWave * p.k; i += 64) {
+      const int e = kExpertsPerWave * cw * p.k + i;
+      if (e < nent) *reinterpret_cast<uint16_t*>(rows + stage_off<NR>(i / p.k, s[e])) = coef_part(ab[e], part);
+    }
+#pragma unroll
+    for (int u = 0; u < kUPer; ++u) *reinterpret_cast<uint16_t*>(udst[u]) = ipt[part];
+#pragma unroll
+    for (int ks = 0; ks < NR; ++ks)
+      bfr[part][ks] =
+          __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(rows + stage_off<NR>(my, 32 * ks + 8 * g)));
+  }
+}
+
+// Rebuilds a consumer wave's rows of A_b when the image changes, through its
+// own staging rows, 8 at a time (the ring is in use then).  For each group of
+// 8 rows: zero them, then per part scatter part `part` of the coefficients
 // (and 1/nU at the uncovered channels) and read the MFMA B operands of the
-// lanes whose expert is in the group.  Entries past 64 kPre are read here.
+// lanes whose expert is in the group.
 template <int NS, int NR>
 __device__ __forceinline__ void build_coefs(const MixArgs& p, int b, const int32_t* __restrict__ s,
                                             const float* __restrict__ alpha, const WaveCoefs& wc,
                                             unsigned char* rows, bf16x8 (&bfr)[NS][NR], int cw, int lane) {
+  constexpr int kGroupBytes = kStageRows * 64 * NR;  // 8 rows of 2 C bytes
   const int nent = p.R * p.k;
   const float* ab = alpha + (int64_t)b * nent;
   const float inv = p.nU > 0 ? 1.f / (float)p.nU : 0.f;
-  const int nz = kStageRows * p.C / 8;  // 16-byte chunks of the staging rows
-  const int my = lane & 15;             // this lane's expert within the wave
+  const int my = lane & 15;  // this lane's expert within the wave
   const int g = lane >> 4;
 #pragma unroll 1
   for (int grp = 0; grp < kExpertsPerWave / kStageRows; ++grp) {
-    for (int i = lane; i < nz; i += 64) reinterpret_cast<u32x4*>(rows)[i] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int q = 0; q < NR / 2 + (NR & 1); ++q)  // 8 rows of 64 NR bytes: 32 NR chunks
+      if (lane + 64 * q < 32 * NR) reinterpret_cast<u32x4*>(rows)[lane + 64 * q] = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int part = 0; part < NS; ++part) {
 #pragma unroll
       for (int r = 0; r < kPre; ++r) {
         const uint32_t sl = half_of(wc.slot[r >> 1], r);
-        if (sl != 0xffffu && (int)(sl >> 14) == grp)
-          *reinterpret_cast<uint16_t*>(rows + (sl & 0x3fffu)) = coef_part(wc.a[r], part);
+        if (sl != 0xffffu && ((int)sl >= kGroupBytes) == (grp == 1))
+          *reinterpret_cast<uint16_t*>(rows + sl - grp * kGroupBytes) = coef_part(wc.a[r], part);
       }
       for (int i = lane + 64 * kPre; i < kExpertsPerWave * p.k; i += 64) {
         const int e = kExpertsPerWave * cw * p.k + i;
         const int eo = i / p.k;
         if (e < nent && (eo >> 3) == grp)
-          *reinterpret_cast<uint16_t*>(rows + stage_off(eo & (kStageRows - 1), s[e], p.C)) = coef_part(ab[e], part);
+          *reinterpret_cast<uint16_t*>(rows + stage_off<NR>(eo & (kStageRows - 1), s[e])) = coef_part(ab[e], part);
       }
 #pragma unroll
       for (int u = 0; u < kUPer; ++u) {
         const uint32_t sl = half_of(wc.uslot[u >> 1], u);
-        if (sl != 0xffffu && (int)(sl >> 14) == grp)
-          *reinterpret_cast<uint16_t*>(rows + (sl & 0x3fffu)) = coef_part(inv, part);
+        if (sl != 0xffffu && ((int)sl >= kGroupBytes) == (grp == 1))
+          *reinterpret_cast<uint16_t*>(rows + sl - grp * kGroupBytes) = coef_part(inv, part);
       }
 #pragma unroll
       for (int ks = 0; ks < NR; ++ks) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(rows + stage_off(my & (kStageRows - 1), 32 * ks + 8 * g, p.C));
+        const u32x4 v = *reinterpret_cast<const u32x4*>(rows + stage_off<NR>(my & (kStageRows - 1), 32 * ks + 8 * g));
         if ((my >> 3) == grp) bfr[part][ks] = __builtin_bit_cast(bf16x8, v);
       }
     }
@@ -300,9 +386,10 @@ __device__ __forceinline__ unsigned char* out_buffer(const Run& r, int n) {
   return r.obuf + ((n - r.t0) & 1) * (kConsumers * kOutWave);
 }
 
-// Consumer waves: the staging slots and the coefficients of the first image
-// are read before the prologue's barrier,
-// and the wave's rows of A_b are rebuilt at the first tile and at every image
+// Consumer waves: the support indices and the coefficients of the first
+// image arrive before the prologue's barrier (one round trip); the staging
+// slots are computed after it, while the loaders request the next tiles.  The
+// wave's rows of A_b are built at the first tile and rebuilt at every image
 // change.
 template <int NR, int NS>
 __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __restrict__ s,
@@ -312,11 +399,17 @@ __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __rest
   const int g = lane >> 4, sl = lane & 15;
   int b = r.t0 / p.nt, j = r.t0 - b * p.nt;
   WaveCoefs wc;
-  unsigned char* rows = r.stage + cw * (kStageRows * p.C * 2);
-  wave_slots(p, s, U, wc, cw, lane);
+  unsigned char* rows = r.stage + cw * (kStageRows * 64 * NR);
+  int cs[kPre], cu[kUPer];
   fetch_coefs(p, alpha, b, wc, cw, lane);
+  load_indices(p, s, U, cs, cu, cw, lane);
+#pragma unroll
+  for (int q = 0; q < kPre; ++q) asm volatile("" : "+v"(cs[q]));
+#pragma unroll
+  for (int q = 0; q < kUPer; ++q) asm volatile("" : "+v"(cu[q]));
   __builtin_amdgcn_s_waitcnt(vm_wait(0));
   lds_barrier();
+  wave_slots<NR>(p, cs, cu, wc, cw, lane);
 
   // transposing reads: 16-lane group g reads channels 8 g + 4 h + (l >> 2)
   // (+ 32 ks) at positions 16 pb + 4 (l & 3) .. +3, l = lane & 15
@@ -329,26 +422,29 @@ __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __rest
   const int cres = cw * kOutWave + sl * kRow + 8 * (g & 1);
 
   bf16x8 bfr[NS][NR];
+  // the first build stages in the last ring buffer (4 x 16 rows of 2 C bytes)
+  // and sends empty slots to this wave's own staging rows, unused until an
+  // image changes
+  build_first<NS, NR>(p, b, s, alpha, wc, r.ring + (kRing - 1) * r.tileb + cw * (kExpertsPerWave * 64 * NR), rows,
+                      bfr, cw, lane);
+  lds_barrier();  // tile t0 in LDS
   for (int n = r.t0; n < r.t1; ++n, ++j) {
     if (j == p.nt) {
       ++b;
       j = 0;
     }
-    if (n == r.t0 || j == 0) {
-      // first tile or next image: rebuild this wave's rows of A_b.  The old
-      // operands are dead from here (each lane's are rewritten by one of the
-      // build's passes); a constant frees their registers meanwhile.
+    if (n != r.t0 && j == 0) {
+      // next image: rebuild this wave's rows of A_b.  The old operands are
+      // dead from here (each lane's are rewritten by one of the build's
+      // passes); a constant frees their registers meanwhile.
 #pragma unroll
       for (int part = 0; part < NS; ++part)
 #pragma unroll
         for (int ks = 0; ks < NR; ++ks) bfr[part][ks] = bf16x8{};
-      if (n != r.t0) {
-        fetch_coefs(p, alpha, b, wc, cw, lane);
-        __builtin_amdgcn_s_waitcnt(vm_wait(0));
-      }
+      fetch_coefs(p, alpha, b, wc, cw, lane);
+      __builtin_amdgcn_s_waitcnt(vm_wait(0));
       build_coefs<NS, NR>(p, b, s, alpha, wc, rows, bfr, cw, lane);
     }
-    if (n == r.t0) lds_barrier();  // tile t0 in LDS
 
     const unsigned char* tb = r.ring + ((n - r.t0) & (kRing - 1)) * r.tileb;
     // software pipeline: the operands of channel step ks + 1 are read while
