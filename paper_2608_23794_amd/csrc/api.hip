@@ -213,6 +213,10 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
   if (moce::mfmamix_eligible(sh)) {
     hipError_t e = moce::launch_pool(sh, x, d, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    // k = 32 with the softplus-linear gate: the mix kernel evaluates the
+    // gate itself, in the gate kernel's layout and operations
+    if (moce::mfmamix_gate_fusable(sh, gate->kind))
+      return device_status(moce::launch_mfmamix_gated(sh, x, s, w, d, gate->a, gate->c, U, nU, y, stream));
     e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, nullptr, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
     return device_status(moce::launch_mfmamix(sh, x, s, alpha, U, nU, y, stream));

@@ -201,14 +201,19 @@ __device__ __forceinline__ void wave_slots(const MixArgs& p, const int (&cs)[kPr
     // below 16 with a relative error of a few ulp, far inside its distance
     // of at least 1 / (2 k) from an integer
     const int eo = (int)(((float)i + 0.5f) * rk);
-    const uint32_t v = (i < kExpertsPerWave * p.k && e < nent) ? (uint32_t)stage_off<NR>(eo, cs[r]) : 0xffffu;
+    // computed for every lane and then selected: branch-free, so that this
+    // arithmetic can interleave with other work
+    int off = stage_off<NR>(eo & (kExpertsPerWave - 1), cs[r]);
+    asm volatile("" : "+v"(off));
+    const uint32_t v = (i < kExpertsPerWave * p.k && e < nent) ? (uint32_t)off : 0xffffu;
     wc.slot[r >> 1] = (r & 1) ? (wc.slot[r >> 1] | v << 16) : v;
   }
   const int ro = p.R - kExpertsPerWave * cw;  // the residual row within this wave's experts
 #pragma unroll
   for (int u = 0; u < kUPer; ++u) {
-    const uint32_t v = (ro >= 0 && ro < kExpertsPerWave && lane + 64 * u < p.nU) ? (uint32_t)stage_off<NR>(ro, cu[u])
-                                                                                : 0xffffu;
+    int off = stage_off<NR>(ro & (kExpertsPerWave - 1), cu[u]);
+    asm volatile("" : "+v"(off));
+    const uint32_t v = (ro >= 0 && ro < kExpertsPerWave && lane + 64 * u < p.nU) ? (uint32_t)off : 0xffffu;
     wc.uslot[u >> 1] = (u & 1) ? (wc.uslot[u >> 1] | v << 16) : v;
   }
 }
@@ -220,6 +225,148 @@ __device__ __forceinline__ void fetch_coefs(const MixArgs& p, const float* __res
   const float* ab = alpha + (int64_t)b * nent;
 #pragma unroll
   for (int r = 0; r < kPre; ++r) wc.a[r] = ab[min(first + lane + 64 * r, nent - 1)];
+}
+
+// The softplus-linear gate's inputs, for a forward that evaluates the gate
+// inside the mix (Sec. 3.3: temperature from the support's pooled
+// descriptors, then the tempered softmax of the logits): pooled descriptors
+// d [B][C], prepared logits w [R][k], slopes a [R][k], offsets c [R].
+struct GateArgs {
+  const float* d;
+  const float* w;
+  const float* a;
+  const float* c;
+};
+
+// A lane's share of the gate's parameters (k = 32: round r of lane l is
+// coefficient l & 31 of expert 16 w + 2 r + l / 32).
+struct WaveGate {
+  float av[kPre], wv[kPre], co[kPre];
+};
+
+__device__ __forceinline__ void load_gate(const MixArgs& p, const GateArgs& ga, WaveGate& wg, int cw, int lane) {
+  const int nent = p.R * p.k;
+  const int first = kExpertsPerWave * cw * p.k;
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) {
+    const int e = min(first + lane + 64 * r, nent - 1);
+    wg.av[r] = ga.a[e];
+    wg.wv[r] = ga.w[e];
+    wg.co[r] = ga.c[min(kExpertsPerWave * cw + 2 * r + (lane >> 5), p.R - 1)];
+  }
+}
+
+// The pooled descriptors at this wave's support entries for image b.
+__device__ __forceinline__ void gather_desc(const MixArgs& p, const GateArgs& ga, int b, const int (&cs)[kPre],
+                                            float (&dv)[kPre]) {
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) dv[r] = ga.d[(int64_t)b * p.C + cs[r]];
+}
+
+// The value of lane l ^ OFF within 32-lane segments.  Distances 1, 2, 4
+// and 8 stay inside a row of 16 lanes and use DPP moves (quad permutations,
+// row shifts, a half-row rotation); 16 uses a permute.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, true));
+}
+template <int OFF>
+__device__ __forceinline__ float xor_peer(float v, int lane) {
+  if constexpr (OFF == 1) {
+    return dpp_mov<0xb1>(v);  // quad_perm [1, 0, 3, 2]
+  } else if constexpr (OFF == 2) {
+    return dpp_mov<0x4e>(v);  // quad_perm [2, 3, 0, 1]
+  } else if constexpr (OFF == 4) {
+    const float up = dpp_mov<0x104>(v);  // row_shl 4: lane l + 4
+    const float dn = dpp_mov<0x114>(v);  // row_shr 4: lane l - 4
+    return (lane & 4) ? dn : up;
+  } else if constexpr (OFF == 8) {
+    return dpp_mov<0x128>(v);  // row_ror 8: lane l ^ 8 within the row
+  } else {
+    return __shfl_xor(v, OFF, 32);
+  }
+}
+
+// wave_sum<32> and wave_max<32> of kPre values at once: the same butterfly
+// (partners l ^ 16, 8, 4, 2, 1 in that order) for each, with the kPre
+// exchanges of a step issued together.
+template <int OFF>
+__device__ __forceinline__ void seg32_sum_step(float (&v)[kPre], int lane) {
+  float o[kPre];
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) o[r] = xor_peer<OFF>(v[r], lane);
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) v[r] += o[r];
+}
+template <int OFF>
+__device__ __forceinline__ void seg32_max_step(float (&v)[kPre], int lane) {
+  float o[kPre];
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) o[r] = xor_peer<OFF>(v[r], lane);
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) v[r] = fmaxf(v[r], o[r]);
+}
+__device__ __forceinline__ void seg32_sum(float (&v)[kPre], int lane) {
+  seg32_sum_step<16>(v, lane);
+  seg32_sum_step<8>(v, lane);
+  seg32_sum_step<4>(v, lane);
+  seg32_sum_step<2>(v, lane);
+  seg32_sum_step<1>(v, lane);
+}
+__device__ __forceinline__ void seg32_max(float (&v)[kPre], int lane) {
+  seg32_max_step<16>(v, lane);
+  seg32_max_step<8>(v, lane);
+  seg32_max_step<4>(v, lane);
+  seg32_max_step<2>(v, lane);
+  seg32_max_step<1>(v, lane);
+}
+
+// The coefficients of this wave's entries: the gate kernel's operations in
+// the gate kernel's lane layout (one expert per 32 lanes, coefficient i on
+// lane i), so the values are bit-identical to the ones it writes.
+__device__ __forceinline__ void wave_gate(const MixArgs& p, const WaveGate& wg, const float (&dv)[kPre],
+                                          WaveCoefs& wc, int cw, int lane) {
+  const int nent = p.R * p.k;
+  const int first = kExpertsPerWave * cw * p.k;
+  bool in[kPre];
+  float v[kPre], z[kPre];
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) {
+    in[r] = first + lane + 64 * r < nent;
+    v[r] = in[r] ? wg.av[r] * dv[r] : 0.f;
+  }
+  seg32_sum(v, lane);
+  // the temperatures: the 16 experts' sums gathered on lanes 0..15 (lane
+  // 2 r + h holds expert 2 r + h), one softplus for all of them, then each
+  // sent back to its expert's 32 lanes
+  float gp = 0.f;
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) {
+    const float x = __shfl(v[r] + wg.co[r], (lane & 1) * 32);
+    gp = (lane >> 1) == r ? x : gp;
+  }
+  const float tp = softplusf(gp) + 1e-3f;
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) {
+    z[r] = wg.wv[r] / __shfl(tp, 2 * r + (lane >> 5));
+    v[r] = in[r] ? z[r] : -INFINITY;
+  }
+  seg32_max(v, lane);
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) {
+    // evaluated on every lane, then selected (branch-free)
+    float ex = expf(z[r] - v[r]);
+    asm volatile("" : "+v"(ex));
+    z[r] = in[r] ? ex : 0.f;
+    v[r] = z[r];
+  }
+  seg32_sum(v, lane);
+#pragma unroll
+  for (int r = 0; r < kPre; ++r) {
+    float q = z[r] / v[r];
+    asm volatile("" : "+v"(q));
+    wc.a[r] = in[r] ? q : 0.f;
+  }
 }
 
 // The exact split a = hi + mid + lo into bf16 parts (with two parts: hi and
@@ -391,9 +538,10 @@ __device__ __forceinline__ unsigned char* out_buffer(const Run& r, int n) {
 // slots are computed after it, while the loaders request the next tiles.  The
 // wave's rows of A_b are built at the first tile and rebuilt at every image
 // change.
-template <int NR, int NS>
+template <int NR, int NS, bool GATE>
 __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __restrict__ s,
-                                             const int32_t* __restrict__ U, const float* __restrict__ alpha) {
+                                             const int32_t* __restrict__ U, const float* __restrict__ alpha,
+                                             const GateArgs& ga) {
   const MixArgs& p = r.p;
   const int lane = r.lane, cw = r.wv;
   const int g = lane >> 4, sl = lane & 15;
@@ -401,14 +549,27 @@ __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __rest
   WaveCoefs wc;
   unsigned char* rows = r.stage + cw * (kStageRows * 64 * NR);
   int cs[kPre], cu[kUPer];
-  fetch_coefs(p, alpha, b, wc, cw, lane);
+  WaveGate wg;
+  float dv[kPre];
+  if constexpr (GATE)
+    load_gate(p, ga, wg, cw, lane);
+  else
+    fetch_coefs(p, alpha, b, wc, cw, lane);
   load_indices(p, s, U, cs, cu, cw, lane);
 #pragma unroll
   for (int q = 0; q < kPre; ++q) asm volatile("" : "+v"(cs[q]));
 #pragma unroll
   for (int q = 0; q < kUPer; ++q) asm volatile("" : "+v"(cu[q]));
+  if constexpr (GATE) {
+    // the descriptors at the support entries: a second round trip, before
+    // the barrier too
+    gather_desc(p, ga, b, cs, dv);
+#pragma unroll
+    for (int q = 0; q < kPre; ++q) asm volatile("" : "+v"(dv[q]));
+  }
   __builtin_amdgcn_s_waitcnt(vm_wait(0));
   lds_barrier();
+  if constexpr (GATE) wave_gate(p, wg, dv, wc, cw, lane);
   wave_slots<NR>(p, cs, cu, wc, cw, lane);
 
   // transposing reads: 16-lane group g reads channels 8 g + 4 h + (l >> 2)
@@ -441,8 +602,27 @@ __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __rest
       for (int part = 0; part < NS; ++part)
 #pragma unroll
         for (int ks = 0; ks < NR; ++ks) bfr[part][ks] = bf16x8{};
-      fetch_coefs(p, alpha, b, wc, cw, lane);
-      __builtin_amdgcn_s_waitcnt(vm_wait(0));
+      if constexpr (GATE) {
+        // the static reads are repeated here: an opaque lane index keeps
+        // them from being hoisted out of the loop, where they would stay
+        // live through the products
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        WaveGate wg2;
+        int cs2[kPre];
+        float dv2[kPre];
+        load_gate(p, ga, wg2, cw, ln);
+#pragma unroll
+        for (int q = 0; q < kPre; ++q) cs2[q] = s[min(kExpertsPerWave * cw * p.k + ln + 64 * q, p.R * p.k - 1)];
+#pragma unroll
+        for (int q = 0; q < kPre; ++q) asm volatile("" : "+v"(cs2[q]));
+        gather_desc(p, ga, b, cs2, dv2);
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+        wave_gate(p, wg2, dv2, wc, cw, ln);
+      } else {
+        fetch_coefs(p, alpha, b, wc, cw, lane);
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+      }
       build_coefs<NS, NR>(p, b, s, alpha, wc, rows, bfr, cw, lane);
     }
 
@@ -551,12 +731,12 @@ __device__ __forceinline__ void store_run(const Run& r, uint16_t* __restrict__ y
   store_results(out_buffer(r, r.t1 - 1));
 }
 
-template <int NR, int NS>
+template <int NR, int NS, bool GATE>
 __device__ __forceinline__ void run_tiles(const Run& r, const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
                                           const int32_t* __restrict__ s, const int32_t* __restrict__ U,
-                                          const float* __restrict__ alpha) {
+                                          const float* __restrict__ alpha, const GateArgs& ga) {
   if (r.wv < kConsumers)
-    consumer_run<NR, NS>(r, s, U, alpha);
+    consumer_run<NR, NS, GATE>(r, s, U, alpha, ga);
   else if (r.wv < kConsumers + kLoaders)
     loader_run<NR>(r, x);
   else
@@ -564,25 +744,29 @@ __device__ __forceinline__ void run_tiles(const Run& r, const uint16_t* __restri
 }
 
 // NR = C / 32 channel steps of 32, NS coefficient parts.  One contiguous
-// range of tiles per workgroup.
-template <int NR, int NS>
+// range of tiles per workgroup.  GATE: the consumer waves evaluate the
+// softplus-linear gate for their own coefficients (k = 32) from the pooled
+// descriptors instead of reading alpha.
+template <int NR, int NS, bool GATE>
 __global__ void __launch_bounds__(kThreads, 1)
 k_mfmamix(MixArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, const int32_t* __restrict__ s,
-          const float* __restrict__ alpha, const int32_t* __restrict__ U) {
+          const float* __restrict__ alpha, const int32_t* __restrict__ U, GateArgs ga) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int t0 = (int)((int64_t)blockIdx.x * p.ntiles / gridDim.x);
   const int t1 = (int)((int64_t)(blockIdx.x + 1) * p.ntiles / gridDim.x);
   if (t0 >= t1) return;
   const Run r = make_run(p, t0, t1, smem);
-  run_tiles<NR, NS>(r, x, y, s, U, alpha);
+  run_tiles<NR, NS, GATE>(r, x, y, s, U, alpha, ga);
 }
 
-using MfmaKernel = void (*)(MixArgs, const uint16_t*, uint16_t*, const int32_t*, const float*, const int32_t*);
+using MfmaKernel = void (*)(MixArgs, const uint16_t*, uint16_t*, const int32_t*, const float*, const int32_t*,
+                            GateArgs);
 
-template <int NS>
+template <int NS, bool GATE>
 MfmaKernel pick(int nr) {
-  static const MfmaKernel k[8] = {k_mfmamix<1, NS>, k_mfmamix<2, NS>, k_mfmamix<3, NS>, k_mfmamix<4, NS>,
-                                  k_mfmamix<5, NS>, k_mfmamix<6, NS>, k_mfmamix<7, NS>, k_mfmamix<8, NS>};
+  static const MfmaKernel k[8] = {k_mfmamix<1, NS, GATE>, k_mfmamix<2, NS, GATE>, k_mfmamix<3, NS, GATE>,
+                                  k_mfmamix<4, NS, GATE>, k_mfmamix<5, NS, GATE>, k_mfmamix<6, NS, GATE>,
+                                  k_mfmamix<7, NS, GATE>, k_mfmamix<8, NS, GATE>};
   return k[nr - 1];
 }
 
@@ -623,20 +807,39 @@ int cu_count() {
 
 }  // namespace
 
-hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
-                          int nU, void* y, hipStream_t st) {
+namespace {
+
+hipError_t launch_mix_kernel(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
+                             int nU, const GateArgs* ga, void* y, hipStream_t st) {
   const MixArgs p = mix_args(sh, nU);
   if (p.ntiles == 0) return hipSuccess;
   const int grid = std::min(cu_count(), p.ntiles);
   const size_t lds = mfma_lds(p.C);
-  const MfmaKernel k = pick<kParts>(p.C / 32);
+  const MfmaKernel k = ga ? pick<kParts, true>(p.C / 32) : pick<kParts, false>(p.C / 32);
   // the dynamic LDS limit, set on the current device at every launch (the
   // library keeps no state between calls)
   const hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, st, p, static_cast<const uint16_t*>(x),
-                     static_cast<uint16_t*>(y), s, alpha, U);
+                     static_cast<uint16_t*>(y), s, alpha, U, ga ? *ga : GateArgs{});
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
+                          int nU, void* y, hipStream_t st) {
+  return launch_mix_kernel(sh, x, s, alpha, U, nU, nullptr, y, st);
+}
+
+bool mfmamix_gate_fusable(const Shape& sh, int gate_kind) {
+  return mfmamix_eligible(sh) && gate_kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k == 32;
+}
+
+hipError_t launch_mfmamix_gated(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* d,
+                                const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st) {
+  const GateArgs ga{d, w, a, c};
+  return launch_mix_kernel(sh, x, s, nullptr, U, nU, &ga, y, st);
 }
 
 }  // namespace moce

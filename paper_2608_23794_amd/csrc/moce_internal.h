@@ -86,5 +86,11 @@ hipError_t launch_tilemix(const Shape& sh, const void* x, const int32_t* s, cons
 bool mfmamix_eligible(const Shape& sh);
 hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
                           int nU, void* y, hipStream_t st);
+// The same product with the softplus-linear gate evaluated inside the mix
+// kernel from the pooled descriptors d (bit-identical coefficients, no
+// temperatures or coefficients written), for k = 32.
+bool mfmamix_gate_fusable(const Shape& sh, int gate_kind);
+hipError_t launch_mfmamix_gated(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* d,
+                                const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st);
 
 }  // namespace moce

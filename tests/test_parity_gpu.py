@@ -464,6 +464,9 @@ MFMA_STAGES = [
     (9, 32, 8, 3, 8, 8),         # C = 32, one partial expert group, k not a power of two
     (3, 96, 40, 20, 6, 12),      # three expert groups, the last partial; ragged last tile (72 positions)
     (2, 64, 17, 8, 4, 4),        # the residual row alone in the second group
+    # k = 32: the forward evaluates the gate inside the mix kernel
+    (120, 64, 9, 32, 12, 16),    # ranges that straddle images (the gate again mid-range), one partial group
+    (7, 64, 33, 32, 28, 28),     # the residual row alone in the third group; ragged last tile (16 positions)
 ]
 
 
