@@ -10,8 +10,9 @@ stream the kernels are launched on.
 Prints one JSON line.  ``value`` is the effective bandwidth in GB/s with the
 workload's metric bytes (two reads of x, one write of y, the parameters);
 ``roofline`` prices the dominant kernel's algorithmic bytes against the
-8 TB/s HBM peak: the forward runs pool, gate and mix kernels, each also
-reachable through its own entry point, and the slowest of the three, timed
+8 TB/s HBM peak: the forward runs a pooling kernel and either one kernel for
+gate and mix (k = 32 on the MFMA path) or a gate kernel and a mix kernel,
+each also reachable through its own entry point; the slowest of them, timed
 through that entry point (launches captured in a HIP graph, replays timed
 with HIP events), is priced.  ``cpu_baseline``
 times the CPU oracle on a bounded sample of the same workload.
@@ -181,12 +182,21 @@ def main():
     t_mix = launch_time_ms(lambda i, st: mb.moce_mix(desc, xs[i % nsets], layer.s_c, alpha, U, layer.nU,
                                                      ys[i % nsets], st), n_k)
     R, k = wl.E - 1, wl.k
-    kernels = {
+    stages = {
         "pool": (t_pool, traffic["x"] + B * wl.C * 4),
         "gate": (t_gate, B * R * k * 4 + R * k * 12 + B * R * 4 + B * R * k * 4),
         "mix": (t_mix, traffic["x"] + traffic["y"] + B * R * k * 4 + R * k * 4),
     }
     path = mb.moce_forward_path(desc, mb.MOCE_GATE_SOFTPLUS_LINEAR)
+    if path == mb.PATH_MFMA_GATE:
+        # the forward's second kernel: gate and mix in one (x, y, the pooled
+        # descriptors, supports, slopes, logits and offsets)
+        t_gm = launch_time_ms(lambda i, st: mb.moce_gate_mix(desc, xs[i % nsets], d, layer.s_c, layer.w_c,
+                                                             layer.gate, U, layer.nU, ys[i % nsets], st), n_k)
+        kernels = {"pool": stages["pool"],
+                   "gate_mix": (t_gm, traffic["x"] + traffic["y"] + B * wl.C * 4 + R * k * 12 + R * 4)}
+    else:
+        kernels = stages
     dom = max(kernels, key=lambda n: kernels[n][0])
     dom_ms, dom_bytes = kernels[dom]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
@@ -207,7 +217,8 @@ def main():
         "accumulate": "f32",
         "data": "synthetic (seeded, shapes and distributions of the named layer)",
         "config": {**wl.describe(), "layout": layout,
-                   "forward": "pool, gate, tile mix" if path == mb.PATH_TILE else "pool, gate, mix"},
+                   "forward": {mb.PATH_TILE: "pool, gate, tile mix",
+                               mb.PATH_MFMA_GATE: "pool, gate inside the mix"}.get(path, "pool, gate, mix")},
         "latency_us": round(ms * 1e3, 2),
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 1),
         "latency_us_warm_cache": round(ms_warm * 1e3, 2),
@@ -215,10 +226,11 @@ def main():
         "compulsory_GBps": round(traffic["compulsory"] / (ms * 1e-3) / 1e9, 1),
         "rotation_sets": nsets,
         "kernels_us": {n: round(v[0] * 1e3, 2) for n, v in kernels.items()},
+        "stage_entry_points_us": {n: round(v[0] * 1e3, 2) for n, v in stages.items()},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("k_mfmamix<8, 3>")
-                     if dom == "mix" and path == mb.PATH_MFMA and wl.name == "resnet50_stage1" else None,
+                     "traffic": measured_traffic(f"k_mfmamix<{wl.C // 32}, 3, {'true' if dom == 'gate_mix' else 'false'}>")
+                     if dom in ("mix", "gate_mix") and path in (mb.PATH_MFMA, mb.PATH_MFMA_GATE) else None,
                      "algorithmic_bytes": dom_bytes},
     }
 

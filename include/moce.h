@@ -130,6 +130,17 @@ moce_status moce_pool(const moce_desc* desc, const void* x, float* d, hipStream_
 moce_status moce_gate(const moce_desc* desc, const float* d, const int32_t* s, const float* w,
                       const moce_gate_params* gate, float* tau, float* alpha, hipStream_t stream);
 
+/* Temperatures, coefficients and mixing in one kernel (Secs. 3.3-3.4): the
+ * y of moce_gate followed by moce_mix, bit for bit, from the pooled
+ * descriptors d [B][C], without writing tau or alpha.  Each workgroup of the
+ * mix evaluates the softplus-linear gate for the experts of the images it
+ * mixes.  Only where moce_forward_path(desc, gate->kind) is
+ * MOCE_PATH_MFMA_GATE (otherwise MOCE_ERR_UNSUPPORTED); s, w: prepared rows;
+ * U, nU as for moce_mix; y is fully overwritten. */
+moce_status moce_gate_mix(const moce_desc* desc, const void* x, const float* d, const int32_t* s, const float* w,
+                          const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
+                          hipStream_t stream);
+
 /* Routed outputs (Sec. 3.3 Eq. 5) and residual output (Sec. 3.4 Eq. 6):
  * y[b][o][p] = sum_i alpha[b][o][i] x[b][s[o][i]][p] for o < E-1, and
  * y[b][E-1][p] = (1/nU) sum_{c in U} x[b][c][p], or 0 when nU == 0.
@@ -143,11 +154,13 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
 size_t moce_forward_workspace_bytes(const moce_desc* desc);
 
 /* Paths moce_forward can take. */
-enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1, MOCE_PATH_MFMA = 2 };
+enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1, MOCE_PATH_MFMA = 2, MOCE_PATH_MFMA_GATE = 3 };
 
-/* The path moce_forward (and moce_mix) takes for `desc`, after plane-wise
- * pooling and the gate:
- *  MOCE_PATH_MFMA: the routed and residual outputs of an image as one dense
+/* The path moce_forward takes for `desc` after plane-wise pooling (moce_mix
+ * takes the same kernels, MOCE_PATH_MFMA for MOCE_PATH_MFMA_GATE):
+ *  MOCE_PATH_MFMA_GATE: MOCE_PATH_MFMA with the softplus-linear gate
+ *     evaluated inside the mix kernel, as moce_gate_mix (k = 32);
+ *  MOCE_PATH_MFMA: the gate kernel, then the routed and residual outputs of an image as one dense
  *     bf16 matrix product on the matrix cores, the coefficients split into
  *     bf16 parts that sum to them exactly (NCHW bfloat16, E-1 >= 1, C a
  *     multiple of 32 up to 256, E <= 64, H*W a multiple of 8);
@@ -156,9 +169,8 @@ enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1, MOCE_PATH_MFMA = 2 };
  *  MOCE_PATH_GENERIC: the layout- and type-generic kernels.
  * All compute the same values up to float32 rounding order; the MFMA path
  * requires distinct channels within each support row, as
- * moce_support_prepare guarantees.  `gate_kind` must be a valid gate kind;
- * it does not change the path.  A negative moce_status for an invalid
- * descriptor or gate kind. */
+ * moce_support_prepare guarantees.  `gate_kind` must be a valid gate kind.
+ * A negative moce_status for an invalid descriptor or gate kind. */
 int moce_forward_path(const moce_desc* desc, int gate_kind);
 
 /* The whole layer (Secs. 3.3-3.4): pooling, temperatures, mixing

@@ -28,7 +28,7 @@ STATUS = {
 
 # Every function include/moce.h declares, in declaration order.
 ENTRY_POINTS = (
-    "moce_support_prepare", "moce_pool", "moce_gate", "moce_mix",
+    "moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix",
     "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_status_str",
     "moce_abi_version",
 )
@@ -74,6 +74,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_support_prepare.argtypes = [D, P, P, P, P, P, P, P, IP, IP, P]
     lib.moce_pool.argtypes = [D, P, P, P]
     lib.moce_gate.argtypes = [D, P, P, P, G, P, P, P]
+    lib.moce_gate_mix.argtypes = [D, P, P, P, P, G, P, I32, P, P]
     lib.moce_mix.argtypes = [D, P, P, P, P, I32, P, P]
     lib.moce_forward_workspace_bytes.argtypes = [D]
     lib.moce_forward_workspace_bytes.restype = SZ
@@ -82,7 +83,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_status_str.argtypes = [ctypes.c_int]
     lib.moce_status_str.restype = ctypes.c_char_p
     lib.moce_abi_version.restype = ctypes.c_int
-    for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_mix", "moce_forward"):
+    for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -147,6 +148,11 @@ def moce_gate(desc: moce_desc, d, s, w, gate: moce_gate_params, tau, alpha=None,
                                          _ptr(tau), _ptr(alpha), _stream(stream)))
 
 
+def moce_gate_mix(desc: moce_desc, x, d, s, w, gate: moce_gate_params, U, nU: int, y, stream=None) -> None:
+    _check("moce_gate_mix", load().moce_gate_mix(ctypes.byref(desc), _ptr(x), _ptr(d), _ptr(s), _ptr(w),
+                                                 ctypes.byref(gate), _ptr(U), nU, _ptr(y), _stream(stream)))
+
+
 def moce_mix(desc: moce_desc, x, s, alpha, U, nU: int, y, stream=None) -> None:
     _check("moce_mix", load().moce_mix(ctypes.byref(desc), _ptr(x), _ptr(s), _ptr(alpha), _ptr(U), nU,
                                        _ptr(y), _stream(stream)))
@@ -156,11 +162,12 @@ def moce_forward_workspace_bytes(desc: moce_desc) -> int:
     return int(load().moce_forward_workspace_bytes(ctypes.byref(desc)))
 
 
-PATH_GENERIC, PATH_TILE, PATH_MFMA = 0, 1, 2
+PATH_GENERIC, PATH_TILE, PATH_MFMA, PATH_MFMA_GATE = 0, 1, 2, 3
 
 
 def moce_forward_path(desc: moce_desc, gate_kind: int) -> int:
-    """PATH_MFMA, PATH_TILE or PATH_GENERIC: the kernels moce_forward and moce_mix use for desc."""
+    """PATH_MFMA_GATE, PATH_MFMA, PATH_TILE or PATH_GENERIC: the kernels moce_forward uses for desc
+    (moce_mix: the same, PATH_MFMA for PATH_MFMA_GATE)."""
     r = int(load().moce_forward_path(ctypes.byref(desc), gate_kind))
     if r < 0:
         raise MoceError("moce_forward_path", r)

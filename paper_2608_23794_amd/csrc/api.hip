@@ -169,6 +169,22 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
   return device_status(moce::launch_mix(sh, x, s, alpha, nullptr, nullptr, nullptr, U, nU, y, stream));
 }
 
+moce_status moce_gate_mix(const moce_desc* desc, const void* x, const float* d, const int32_t* s, const float* w,
+                          const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
+                          hipStream_t stream) {
+  Shape sh;
+  moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  st = check_gate(sh, gate);
+  if (st != MOCE_OK) return st;
+  if (!moce::mfmamix_gate_fusable(sh, gate->kind)) return MOCE_ERR_UNSUPPORTED;
+  if (!x || !y || !d || !s || !w) return MOCE_ERR_NULL;
+  if (nU < 0 || (int64_t)nU > sh.C) return MOCE_ERR_SHAPE;
+  if (nU > 0 && !U) return MOCE_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(y, 16)) return MOCE_ERR_ALIGN;
+  return device_status(moce::launch_mfmamix_gated(sh, x, s, w, d, gate->a, gate->c, U, nU, y, stream));
+}
+
 size_t moce_forward_workspace_bytes(const moce_desc* desc) {
   Shape sh;
   if (check_desc(desc, &sh) != MOCE_OK) return 0;
@@ -180,6 +196,7 @@ int moce_forward_path(const moce_desc* desc, int gate_kind) {
   const moce_status st = check_desc(desc, &sh);
   if (st != MOCE_OK) return st;
   if (gate_kind != MOCE_GATE_SOFTPLUS_LINEAR && gate_kind != MOCE_GATE_MLP_SIGMOID) return MOCE_ERR_GATE;
+  if (moce::mfmamix_gate_fusable(sh, gate_kind)) return MOCE_PATH_MFMA_GATE;
   if (moce::mfmamix_eligible(sh)) return MOCE_PATH_MFMA;
   return sh.R > 0 && moce::tilemix_eligible(sh) ? MOCE_PATH_TILE : MOCE_PATH_GENERIC;
 }

@@ -99,6 +99,15 @@ class MoceLayer:
         mb.moce_gate(self.desc(B), d, self.s_c, self.w_c, self.gate, tau, alpha, self._stream())
         return tau, alpha
 
+    def gate_mix(self, x: torch.Tensor, d: torch.Tensor, y: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """moce_gate_mix: temperatures, coefficients and mixing in one kernel from the pooled d."""
+        B = x.shape[0]
+        if y is None:
+            y = torch.empty(self.y_shape(B), dtype=x.dtype, device=self.device)
+        mb.moce_gate_mix(self.desc(B), x, d, self.s_c, self.w_c, self.gate, self.U if self.nU else None, self.nU,
+                         y, self._stream())
+        return y
+
     def mix(self, x: torch.Tensor, alpha: torch.Tensor, y: Optional[torch.Tensor] = None) -> torch.Tensor:
         B = x.shape[0]
         if y is None:

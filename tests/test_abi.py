@@ -87,6 +87,11 @@ def _call_forward(desc, gate, x=FAKE, s=FAKE, w=FAKE, U=FAKE, nU=0, y=FAKE, ws=F
     return mb.raw_status("moce_forward", ctypes.byref(desc), x, s, w, g, U, nU, y, ws, ws_bytes, None)
 
 
+def _call_gate_mix(desc, gate, x=FAKE, d=FAKE, s=FAKE, w=FAKE, U=FAKE, nU=0, y=FAKE):
+    g = ctypes.byref(gate) if gate is not None else None
+    return mb.raw_status("moce_gate_mix", ctypes.byref(desc), x, d, s, w, g, U, nU, y, None)
+
+
 def _call_prepare(desc, s=FAKE, w=FAKE, s_out=FAKE + 256, w_out=FAKE + 512, covered=FAKE, U=FAKE, info=FAKE,
                   nU=True, bad=True):
     n = ctypes.c_int32(0)
@@ -154,6 +159,32 @@ def test_alignment_and_residual_count(lib):
     assert _call_mix(desc, nU=-1) == -2
     assert _call_mix(desc, nU=65) == -2
     assert _call_forward(desc, gate, nU=65) == -2
+
+
+def test_gate_mix_errors(lib):
+    """The one-kernel gate and mix: host-side checks, and only where the forward takes that path."""
+    fused = good_desc(k=32)
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+    assert lib.moce_forward_path(ctypes.byref(fused), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_MFMA_GATE
+    for change, code in BAD_DESCS:
+        assert _call_gate_mix(good_desc(**{"k": 32, **change}), gate) == code
+    assert _call_gate_mix(fused, None) == -1
+    assert _call_gate_mix(fused, mb.make_gate(a=None, c=FAKE)) == -1
+    assert _call_gate_mix(fused, mb.make_gate(kind=9, a=FAKE, c=FAKE)) == -6
+    mlp = mb.make_gate(mb.MOCE_GATE_MLP_SIGMOID, W1=FAKE, b1=FAKE, w2=FAKE)
+    assert lib.moce_forward_path(ctypes.byref(fused), mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_MFMA
+    for desc, g in [(good_desc(k=8), gate), (fused, mlp), (good_desc(k=32, dtype=mb.MOCE_F32), gate),
+                    (good_desc(k=32, layout=mb.MOCE_NHWC), gate), (good_desc(C=48, k=32), gate),
+                    (good_desc(k=32, E=1), gate)]:
+        assert _call_gate_mix(desc, g) == -10
+        assert lib.moce_forward_path(ctypes.byref(desc), g.kind) != mb.PATH_MFMA_GATE
+    for name in ("x", "d", "s", "w", "y"):
+        assert _call_gate_mix(fused, gate, **{name: None}) == -1
+    assert _call_gate_mix(fused, gate, U=None, nU=2) == -1
+    assert _call_gate_mix(fused, gate, nU=65) == -2
+    assert _call_gate_mix(fused, gate, nU=-1) == -2
+    assert _call_gate_mix(fused, gate, x=FAKE_UNALIGNED) == -8
+    assert _call_gate_mix(fused, gate, y=FAKE_UNALIGNED) == -8
 
 
 def test_gate_parameter_errors(lib):

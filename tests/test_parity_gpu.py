@@ -358,7 +358,7 @@ def test_mfma_forward_shapes(B, C, E, k, H, W):
     x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=B + C + E + k + H, signed=(C % 64 == 32))
     ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
     layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
-    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_MFMA
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == _mfma_path(k)
     y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
     check_y(y, ref["y"], ref["mag"], "bf16")
     res = y[:, E - 1]
@@ -429,8 +429,9 @@ def test_forward_path_choice():
         d = mb.make_desc(B, C, H, W, E, k, mb.MOCE_BF16 if dtype == "bf16" else mb.MOCE_F32,
                          mb.MOCE_NCHW if layout == "nchw" else mb.MOCE_NHWC)
         return mb.moce_forward_path(d, gate)
-    assert path(64, 256, 64, 32, 56, 56) == mb.PATH_MFMA
+    assert path(64, 256, 64, 32, 56, 56) == mb.PATH_MFMA_GATE     # k = 32: the gate inside the mix
     assert path(64, 256, 64, 32, 56, 56, gate=mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_MFMA
+    assert path(5, 128, 24, 64, 12, 16) == mb.PATH_MFMA
     assert path(4, 240, 64, 32, 16, 16) == mb.PATH_TILE          # C not a multiple of 32
     assert path(4, 256, 65, 32, 16, 16) == mb.PATH_TILE          # E > 64
     assert path(2, 64, 16, 8, 8, 8, dtype="f32") == mb.PATH_GENERIC
@@ -455,6 +456,11 @@ def test_forward_reused_workspace_sees_new_inputs():
         check_y(to_host_f64(y), ref["y"], ref["mag"], wl.dtype)
 
 
+def _mfma_path(k):
+    """The forward's path code on the MFMA mix with the softplus-linear gate."""
+    return mb.PATH_MFMA_GATE if k == 32 else mb.PATH_MFMA
+
+
 MFMA_STAGES = [
     # B, C, E, k, H, W: moce_forward against moce_pool + moce_gate + moce_mix on the MFMA path
     (64, 256, 64, 32, 56, 56),   # the ResNet-50 stage-1 layer
@@ -475,7 +481,7 @@ def test_mfma_forward_equals_stages(B, C, E, k, H, W):
     """The whole-layer entry point gives the same bits as the three stage entry points in a row."""
     x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=11 * B + k, signed=(E % 2 == 1))
     layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
-    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_MFMA
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == _mfma_path(k)
     xd = to_device_x(x, "bf16")
     y = layer.forward(xd)
     d = layer.pool(xd)
@@ -483,5 +489,13 @@ def test_mfma_forward_equals_stages(B, C, E, k, H, W):
     y_st = layer.mix(xd, alpha)
     torch.cuda.synchronize()
     assert torch.equal(y.view(torch.int16), y_st.view(torch.int16))
+    if k == 32:
+        # the one-kernel gate and mix entry point, twice (the second output
+        # buffer starts from other contents)
+        for fill in (0, -1):
+            y_gm = torch.full_like(y, fill)
+            layer.gate_mix(xd, d, y_gm)
+            torch.cuda.synchronize()
+            assert torch.equal(y_gm.view(torch.int16), y_st.view(torch.int16))
     ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
     check_y(to_host_f64(y), ref["y"], ref["mag"], "bf16")
