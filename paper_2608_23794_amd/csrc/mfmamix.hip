@@ -535,7 +535,8 @@ __device__ __forceinline__ unsigned char* out_buffer(const Run& r, int n) {
 
 // Consumer waves: the support indices and the coefficients of the first
 // image arrive before the prologue's barrier (one round trip); the staging
-// slots are computed after it, while the loaders request the next tiles.  The
+// slots are computed after it, while the loaders request the next tiles (with
+// the gate inside, while the descriptor gather is in flight, before it).  The
 // wave's rows of A_b are built at the first tile and rebuilt at every image
 // change.
 template <int NR, int NS, bool GATE>
@@ -562,15 +563,18 @@ __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __rest
   for (int q = 0; q < kUPer; ++q) asm volatile("" : "+v"(cu[q]));
   if constexpr (GATE) {
     // the descriptors at the support entries: a second round trip, before
-    // the barrier too
+    // the barrier too, with the slot arithmetic done while it is in flight
     gather_desc(p, ga, b, cs, dv);
+    wave_slots<NR>(p, cs, cu, wc, cw, lane);
 #pragma unroll
     for (int q = 0; q < kPre; ++q) asm volatile("" : "+v"(dv[q]));
   }
   __builtin_amdgcn_s_waitcnt(vm_wait(0));
   lds_barrier();
-  if constexpr (GATE) wave_gate(p, wg, dv, wc, cw, lane);
-  wave_slots<NR>(p, cs, cu, wc, cw, lane);
+  if constexpr (GATE)
+    wave_gate(p, wg, dv, wc, cw, lane);
+  else
+    wave_slots<NR>(p, cs, cu, wc, cw, lane);
 
   // transposing reads: 16-lane group g reads channels 8 g + 4 h + (l >> 2)
   // (+ 32 ks) at positions 16 pb + 4 (l & 3) .. +3, l = lane & 15
