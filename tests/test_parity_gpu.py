@@ -266,6 +266,7 @@ EDGE = [
     (2, 700, 40, 20, 6, 6, "f32", "nchw", {}),         # tile beyond LDS: global-memory path
     (3, 60, 10, 6, 5, 7, "bf16", "nhwc", {}),          # C*2 not a multiple of 16: scalar pooling
     (2, 6000, 30, 40, 3, 3, "bf16", "nhwc", {}),        # tile beyond LDS: global-memory path
+    (2, 3000, 30, 40, 3, 3, "bf16", "nhwc", {}),        # 16-position tile beyond LDS: 8 positions
     (4, 72, 9, 9, 9, 1, "f32", "nhwc", dict(signed=True)),
     (1, 2048, 512, 128, 1, 1, "bf16", "nhwc", {}),      # single token
 ]
