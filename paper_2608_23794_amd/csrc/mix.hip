@@ -211,13 +211,16 @@ k_mix_nchw_global(const T* __restrict__ x, const int32_t* __restrict__ s, const 
 }
 
 // ------------------------------------------------------------------ NHWC
+// 512 threads; work item (expert o, half h) computes o at positions
+// h TP/2 .. h TP/2 + TP/2 - 1 of the tile, so each item's chain of index,
+// LDS and FMA steps is half as long in products and twice as many chains run.
 template <typename T, int TP, bool ALPHA>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(512)
 k_mix_nhwc(const T* __restrict__ x, const int32_t* __restrict__ s, const float* __restrict__ alpha,
            const float* __restrict__ w, const float* __restrict__ tau, const float* __restrict__ lse,
            const int32_t* __restrict__ U, int nU, T* __restrict__ y, int C, int HW, int E, int R, int k,
            int tiles) {
-  static_assert(TP % 4 == 0, "tile rows are read as float4");
+  static_assert(TP % 8 == 0, "half tile rows are read as float4");
   extern __shared__ __align__(16) unsigned char smem[];
   float* tile = reinterpret_cast<float*>(smem);  // [C][TP]
 
@@ -232,20 +235,22 @@ k_mix_nhwc(const T* __restrict__ x, const int32_t* __restrict__ s, const float* 
   }
   __syncthreads();
 
+  constexpr int TH = TP / 2;  // positions per work item
   T* yb = y + (b * HW + p0) * (int64_t)E;
-  for (int o = threadIdx.x; o < E; o += blockDim.x) {
-    float acc[TP];
+  for (int it = threadIdx.x; it < 2 * E; it += blockDim.x) {
+    const int o = it >> 1, h = it & 1;
+    float acc[TH];
 #pragma unroll
-    for (int j = 0; j < TP; ++j) acc[j] = 0.f;
+    for (int j = 0; j < TH; ++j) acc[j] = 0.f;
     if (o < R) {
       const int32_t* so = s + (int64_t)o * k;
       const Coef<ALPHA> coef(alpha, w, tau, lse, b * R + o, o, k);
 #pragma unroll 2
       for (int i = 0; i < k; ++i) {
         const float a = coef(i);
-        const float4* r = reinterpret_cast<const float4*>(tile + so[i] * TP);
+        const float4* r = reinterpret_cast<const float4*>(tile + so[i] * TP + h * TH);
 #pragma unroll
-        for (int q = 0; q < TP / 4; ++q) {
+        for (int q = 0; q < TH / 4; ++q) {
           const float4 v = r[q];
           acc[4 * q + 0] = fmaf(a, v.x, acc[4 * q + 0]);
           acc[4 * q + 1] = fmaf(a, v.y, acc[4 * q + 1]);
@@ -255,19 +260,19 @@ k_mix_nhwc(const T* __restrict__ x, const int32_t* __restrict__ s, const float* 
       }
     } else if (nU > 0) {
       for (int u = 0; u < nU; ++u) {
-        const float4* r = reinterpret_cast<const float4*>(tile + U[u] * TP);
+        const float4* r = reinterpret_cast<const float4*>(tile + U[u] * TP + h * TH);
 #pragma unroll
-        for (int q = 0; q < TP / 4; ++q) {
+        for (int q = 0; q < TH / 4; ++q) {
           const float4 v = r[q];
           acc[4 * q + 0] += v.x; acc[4 * q + 1] += v.y; acc[4 * q + 2] += v.z; acc[4 * q + 3] += v.w;
         }
       }
 #pragma unroll
-      for (int j = 0; j < TP; ++j) acc[j] = acc[j] / (float)nU;
+      for (int j = 0; j < TH; ++j) acc[j] = acc[j] / (float)nU;
     }
 #pragma unroll
-    for (int j = 0; j < TP; ++j)
-      if (j < valid) Elem<T>::store(yb + (int64_t)j * E + o, acc[j]);
+    for (int j = 0; j < TH; ++j)
+      if (h * TH + j < valid) Elem<T>::store(yb + (int64_t)(h * TH + j) * E + o, acc[j]);
   }
 }
 
@@ -356,7 +361,7 @@ hipError_t nhwc_launch(const Shape& sh, const T* x, T* y, const MixArgs& a, hipS
   const int tiles = (int)((sh.HW + TP - 1) / TP);
   auto kern = k_mix_nhwc<T, TP, ALPHA>;
   allow_lds(kern, lds);
-  hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * tiles)), dim3(256), lds, st, x, a.s, a.alpha, a.w, a.tau,
+  hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * tiles)), dim3(512), lds, st, x, a.s, a.alpha, a.w, a.tau,
                      a.lse, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k, tiles);
   return hipGetLastError();
 }
