@@ -211,16 +211,16 @@ k_mix_nchw_global(const T* __restrict__ x, const int32_t* __restrict__ s, const 
 }
 
 // ------------------------------------------------------------------ NHWC
-// 512 threads; work item (expert o, half h) computes o at positions
-// h TP/2 .. h TP/2 + TP/2 - 1 of the tile, so each item's chain of index,
-// LDS and FMA steps is half as long in products and twice as many chains run.
-template <typename T, int TP, bool ALPHA>
-__global__ void __launch_bounds__(512)
+// 64 NS threads; work item (expert o, part h < NS) computes o at positions
+// h TP/NS .. h TP/NS + TP/NS - 1 of the tile, so each item's chain of index,
+// LDS and FMA steps covers fewer products and NS times as many chains run.
+template <typename T, int TP, int NS, bool ALPHA>
+__global__ void __launch_bounds__(64 * NS * 4)
 k_mix_nhwc(const T* __restrict__ x, const int32_t* __restrict__ s, const float* __restrict__ alpha,
            const float* __restrict__ w, const float* __restrict__ tau, const float* __restrict__ lse,
            const int32_t* __restrict__ U, int nU, T* __restrict__ y, int C, int HW, int E, int R, int k,
            int tiles) {
-  static_assert(TP % 8 == 0, "half tile rows are read as float4");
+  static_assert(TP % (4 * NS) == 0, "a work item's positions are read as float4");
   extern __shared__ __align__(16) unsigned char smem[];
   float* tile = reinterpret_cast<float*>(smem);  // [C][TP]
 
@@ -235,10 +235,10 @@ k_mix_nhwc(const T* __restrict__ x, const int32_t* __restrict__ s, const float* 
   }
   __syncthreads();
 
-  constexpr int TH = TP / 2;  // positions per work item
+  constexpr int TH = TP / NS;  // positions per work item
   T* yb = y + (b * HW + p0) * (int64_t)E;
-  for (int it = threadIdx.x; it < 2 * E; it += blockDim.x) {
-    const int o = it >> 1, h = it & 1;
+  for (int it = threadIdx.x; it < NS * E; it += blockDim.x) {
+    const int o = it / NS, h = it % NS;
     float acc[TH];
 #pragma unroll
     for (int j = 0; j < TH; ++j) acc[j] = 0.f;
@@ -357,11 +357,12 @@ hipError_t mix_nchw(const Shape& sh, const T* x, T* y, const MixArgs& a, hipStre
 
 template <typename T, int TP, bool ALPHA>
 hipError_t nhwc_launch(const Shape& sh, const T* x, T* y, const MixArgs& a, hipStream_t st) {
+  constexpr int NS = TP / 4;  // work items of 4 positions
   const size_t lds = (size_t)sh.C * TP * sizeof(float);
   const int tiles = (int)((sh.HW + TP - 1) / TP);
-  auto kern = k_mix_nhwc<T, TP, ALPHA>;
+  auto kern = k_mix_nhwc<T, TP, NS, ALPHA>;
   allow_lds(kern, lds);
-  hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * tiles)), dim3(512), lds, st, x, a.s, a.alpha, a.w, a.tau,
+  hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * tiles)), dim3(256 * NS), lds, st, x, a.s, a.alpha, a.w, a.tau,
                      a.lse, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k, tiles);
   return hipGetLastError();
 }
