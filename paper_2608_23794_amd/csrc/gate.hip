@@ -48,6 +48,64 @@ k_gate_softplus(const float* __restrict__ d, const int32_t* __restrict__ s, cons
                    lse ? lse + item : nullptr);
 }
 
+// The same for 64 < k <= 64 PER: every input of a lane's PER positions is
+// read up front (indices, slopes and logits, then the descriptor gathers),
+// so the wave makes two dependent round trips instead of one per pass, and
+// the quotients are kept for the three reductions.  The operations and their
+// order per lane are those of k_gate_softplus.
+template <int PER>
+__global__ void __launch_bounds__(kGateWaves * kWave)
+k_gate_softplus_wide(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
+                     const float* __restrict__ a, const float* __restrict__ c, float* __restrict__ tau,
+                     float* __restrict__ alpha, float* __restrict__ lse, int64_t B, int64_t C, int R, int k) {
+  const int lane = threadIdx.x & 63;
+  const int64_t item = (int64_t)blockIdx.x * kGateWaves + (threadIdx.x >> 6);
+  if (item >= B * R) return;
+  const int64_t b = item / R;
+  const int o = (int)(item % R);
+  const int32_t* so = s + (int64_t)o * k;
+  const float* ao = a + (int64_t)o * k;
+  const float* wo = w + (int64_t)o * k;
+  const float* db = d + b * C;
+  int ch[PER];
+  float av[PER], wv[PER], dv[PER];
+#pragma unroll
+  for (int r = 0; r < PER; ++r) {
+    const int i = min(lane + kWave * r, k - 1);
+    ch[r] = so[i];
+    av[r] = ao[i];
+    wv[r] = wo[i];
+  }
+#pragma unroll
+  for (int r = 0; r < PER; ++r) dv[r] = db[ch[r]];
+  float g = 0.f;
+#pragma unroll
+  for (int r = 0; r < PER; ++r)
+    if (lane + kWave * r < k) g += av[r] * dv[r];
+  g = wave_sum(g) + c[o];
+  const float t = softplusf(g) + 1e-3f;
+  if (lane == 0) tau[item] = t;
+  float z[PER];
+  float m = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < PER; ++r) {
+    z[r] = wv[r] / t;
+    if (lane + kWave * r < k) m = fmaxf(m, z[r]);
+  }
+  m = wave_max(m);
+  float zs = 0.f;
+#pragma unroll
+  for (int r = 0; r < PER; ++r)
+    if (lane + kWave * r < k) zs += expf(z[r] - m);
+  zs = wave_sum(zs);
+  if (alpha) {
+#pragma unroll
+    for (int r = 0; r < PER; ++r)
+      if (lane + kWave * r < k) alpha[item * k + lane + kWave * r] = expf(z[r] - m) / zs;
+  }
+  if (lse && lane == 0) lse[item] = m + logf(zs);
+}
+
 // The same for k <= W (W = 32 or 64): segments of W lanes, one per (image,
 // expert), 64 / W per wave, lane i of a segment holding support position i.
 // Every input of a position is read up front (the selected logit too), so the
@@ -131,6 +189,12 @@ hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const 
                        tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
   } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 64) {
     hipLaunchKernelGGL(k_gate_softplus_seg<64>, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
+                       tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
+  } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 128) {
+    hipLaunchKernelGGL(k_gate_softplus_wide<2>, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
+                       tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
+  } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 256) {
+    hipLaunchKernelGGL(k_gate_softplus_wide<4>, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
                        tau, alpha, lse, sh.B, sh.C, sh.R, sh.k);
   } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR) {
     hipLaunchKernelGGL(k_gate_softplus, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,

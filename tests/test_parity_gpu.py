@@ -267,6 +267,8 @@ EDGE = [
     (3, 60, 10, 6, 5, 7, "bf16", "nhwc", {}),          # C*2 not a multiple of 16: scalar pooling
     (2, 6000, 30, 40, 3, 3, "bf16", "nhwc", {}),        # tile beyond LDS: global-memory path
     (2, 3000, 30, 40, 3, 3, "bf16", "nhwc", {}),        # 16-position tile beyond LDS: 8 positions
+    (2, 512, 8, 200, 4, 4, "bf16", "nhwc", {}),         # gate with 128 < k <= 256: four positions per lane
+    (1, 600, 4, 300, 2, 2, "f32", "nchw", {}),          # gate with k > 256: the looping kernel
     (4, 72, 9, 9, 9, 1, "f32", "nhwc", dict(signed=True)),
     (1, 2048, 512, 128, 1, 1, "bf16", "nhwc", {}),      # single token
 ]
