@@ -372,3 +372,69 @@ def test_forward_coverage_every_channel_reaches_an_output():
         x2[:, c] += 1.0
         y2 = oracle.mix(x2, r["s"], r["alpha"], r["U"], wl.E, oracle.NCHW)[0]
         assert np.abs(y2 - base).max() > 1e-6
+
+
+# --------------------------------------------------------------------------
+# The tolerance magnitude M that the oracle returns beside y: M = sum_i
+# alpha_i |x_i| for a routed output (Eq. 5 applied to |x|) and the mean of |x|
+# over U for the residual (Eq. 6 applied to |x|).  Every GPU parity check of y
+# is scaled by it, so it is pinned here on its own.
+
+@pytest.mark.parametrize("layout", [oracle.NCHW, oracle.NHWC])
+def test_mag_equals_y_for_nonnegative_inputs(layout):
+    # For x >= 0 the magnitude and the output are the same sum: bit-identical.
+    rng = np.random.default_rng(31)
+    B, C, E, k, H, W = 3, 40, 9, 6, 5, 4
+    x = np.maximum(rng.standard_normal((B, C, H, W)).astype(np.float32), 0)
+    s, w = rand_support(rng, C, E - 1, k)
+    s_c, w_c, _, U, nU = oracle.prepare(C, E, s, w)
+    assert nU > 0
+    al = oracle.softmax(w_c, rng.uniform(0.2, 3.0, (B, E - 1)))
+    if layout == oracle.NHWC:
+        x = np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+    y, mag = oracle.mix(x, s_c, al, U, E, layout)
+    assert np.array_equal(mag, y)
+
+
+@pytest.mark.parametrize("layout", [oracle.NCHW, oracle.NHWC])
+def test_mag_is_the_dense_equivalent_of_abs_x(layout):
+    # Signed inputs: M equals the dense-equivalent product with |x| (a textbook
+    # einsum), so a dropped coefficient (a k-fold larger M) or a missing 1/|U|
+    # fails here.
+    rng = np.random.default_rng(32)
+    B, C, E, k, H, W = 2, 30, 7, 5, 3, 4
+    x = rng.standard_normal((B, C, H, W)).astype(np.float32)
+    s, w = rand_support(rng, C, E - 1, k)
+    s_c, w_c, _, U, nU = oracle.prepare(C, E, s, w)
+    assert nU > 0
+    al = oracle.softmax(w_c, rng.uniform(0.2, 3.0, (B, E - 1)))
+    Weff = dense_equivalent(s_c, al, U, C, E)
+    ref = np.einsum("boc,bchw->bohw", Weff, np.abs(x).astype(np.float64))
+    xin = x if layout == oracle.NCHW else np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+    _, mag = oracle.mix(xin, s_c, al, U, E, layout)
+    if layout == oracle.NHWC:
+        mag = mag.transpose(0, 3, 1, 2)
+    np.testing.assert_allclose(mag, ref, rtol=1e-12, atol=0)
+    # the residual's magnitude is the mean of |x| over U, and it is at most
+    # the largest |x| over U (a mean, not a sum)
+    xa = np.abs(x).astype(np.float64)
+    np.testing.assert_allclose(mag[:, E - 1], xa[:, U].mean(axis=1), rtol=1e-13, atol=0)
+    assert np.all(mag[:, E - 1] <= xa[:, U].max(axis=1) + 1e-15)
+    # a routed magnitude is a convex combination of the support's |x|
+    for o in range(E - 1):
+        sup = xa[:, s_c[o]]
+        assert np.all(mag[:, o] <= sup.max(axis=1) + 1e-14)
+        assert np.all(mag[:, o] >= sup.min(axis=1) - 1e-14)
+
+
+def test_mag_of_empty_residual_is_zero():
+    rng = np.random.default_rng(33)
+    B, C, E, k = 2, 16, 5, 4
+    s = np.array([[(e * k + j) % C for j in range(k)] for e in range(E - 1)], np.int32)
+    w = rng.standard_normal((E - 1, k)).astype(np.float32)
+    s_c, w_c, _, U, nU = oracle.prepare(C, E, s, w)
+    assert nU == 0
+    x = rng.standard_normal((B, C, 3, 3)).astype(np.float32)
+    al = oracle.softmax(w_c, np.ones((B, E - 1)))
+    y, mag = oracle.mix(x, s_c, al, U, E, oracle.NCHW)
+    assert np.all(mag[:, E - 1] == 0.0) and np.all(y[:, E - 1] == 0.0)
