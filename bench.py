@@ -7,15 +7,18 @@ least 1 GiB together) that no step finds its input left in the 256 MB
 Infinity Cache by an earlier step.  Timing uses HIP events recorded on the
 stream the kernels are launched on.
 
-Prints one JSON line.  ``value`` is the effective bandwidth in GB/s with the
-workload's metric bytes (two reads of x, one write of y, the parameters);
-``roofline`` prices the dominant kernel's algorithmic bytes against the
-8 TB/s HBM peak: the forward runs a pooling kernel and either one kernel for
-gate and mix (k = 32 on the MFMA path) or a gate kernel and a mix kernel,
-each also reachable through its own entry point; the slowest of them, timed
-through that entry point (launches captured in a HIP graph, replays timed
-with HIP events), is priced.  ``cpu_baseline``
-times the CPU oracle on a bounded sample of the same workload.
+Prints one JSON line for the headline workload (ResNet-50 stage-1 by
+default).  ``value`` is the effective bandwidth in GB/s with the workload's
+metric bytes (two reads of x, one write of y, the parameters) over the mean
+step time of the K timed steps; ``latency_us_median`` / ``latency_us_iqr``
+come from a second run of K steps with an event recorded between every two.  ``roofline`` prices the
+dominant kernel's algorithmic bytes against the 8 TB/s HBM peak: each kernel
+the forward runs is timed through its own entry point (launches captured in a
+HIP graph, replays timed with HIP events).  ``other_configs`` repeats the
+measurement for the other workloads (stage 3 in both layouts, stage 4, the ViT
+token layer), with forwards captured in HIP graphs so that host time never
+enters.  ``cpu_baseline`` times the CPU oracle on a bounded sample of the
+headline workload, with all host threads and with one.
 """
 from __future__ import annotations
 
@@ -32,6 +35,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "MoCE fwd latency (us) + effective HBM GB/s (% of peak) at ResNet-50 shapes"
+OTHER = (("resnet50_stage3", "nchw"), ("resnet50_stage3", "nhwc"), ("resnet50_stage4", "nhwc"),
+         ("vit_tokens", "nhwc"))
 
 
 def parse():
@@ -45,6 +50,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--no-context", action="store_true")
+    p.add_argument("--no-other", action="store_true", help="skip the other workloads")
+    p.add_argument("--gate", default="softplus", choices=("softplus", "mlp"),
+                   help="gate kind of the headline workload (the benchmark configurations use softplus)")
     # after the measurements, copy this many MiB device to device five times:
     # a plain copy kernel of known size against which hardware byte counters
     # (rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE) are calibrated
@@ -78,11 +86,9 @@ def measured_traffic(kernel: str):
     return int(rec["traffic_bytes"])
 
 
-def launch_time_ms(fn, n, reps=3):
-    """Average duration of one launch of fn(i): the launches of fn(0) ..
-    fn(n-1) are captured in one HIP graph (so no host time falls between
-    them) and the graph's replays are timed with HIP events on the stream
-    that replays it; best of `reps` replays."""
+def _capture(fn, n):
+    """A HIP graph of the launches fn(0, st) .. fn(n-1, st), after a few eager
+    warm-up calls on a side stream."""
     import torch
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -99,7 +105,17 @@ def launch_time_ms(fn, n, reps=3):
     torch.cuda.synchronize()
     graph.replay()
     torch.cuda.synchronize()
-    best = None
+    return graph
+
+
+def graph_times_ms(fn, n, reps):
+    """Per-launch duration of fn, once per replay: the launches of fn(0) ..
+    fn(n-1) are captured in one HIP graph (so no host time falls between
+    them) and each of `reps` replays is timed with HIP events on the stream
+    that replays it."""
+    import torch
+    graph = _capture(fn, n)
+    out = []
     for _ in range(reps):
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
@@ -108,12 +124,34 @@ def launch_time_ms(fn, n, reps=3):
         graph.replay()
         t1.record(st)
         torch.cuda.synchronize()
-        ms = t0.elapsed_time(t1) / n
-        best = ms if best is None else min(best, ms)
-    return best
+        out.append(t0.elapsed_time(t1) / n)
+    return out
 
 
-def event_time_ms(fn, n, stream):
+def launch_time_ms(fn, n, reps=3):
+    """Best per-launch duration over `reps` graph replays (see graph_times_ms)."""
+    return min(graph_times_ms(fn, n, reps))
+
+
+def timed_steps(fn, n, stream):
+    """Runs fn(0) .. fn(n-1) eagerly between two synchronisations, with an
+    event recorded on `stream` before each step and after the last.  Returns
+    (mean ms per step over the bracketed region, per-step ms list)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    torch.cuda.synchronize()
+    for i in range(n):
+        ev[i].record(stream)
+        fn(i)
+    ev[n].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+    return ev[0].elapsed_time(ev[n]) / n, per
+
+
+def mean_steps(fn, n, stream):
+    """Mean ms per step of fn(0) .. fn(n-1), run eagerly between two
+    synchronisations with one event before the first and one after the last."""
     import torch
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
@@ -126,6 +164,177 @@ def event_time_ms(fn, n, stream):
     return t0.elapsed_time(t1) / n
 
 
+def quartiles(v):
+    import numpy as np
+    q1, q2, q3 = np.percentile(np.asarray(v, dtype=np.float64), [25, 50, 75])
+    return float(q1), float(q2), float(q3)
+
+
+class Bench:
+    """Device inputs and timers for one workload and layout."""
+
+    def __init__(self, name, layout, rotate_gib, gate="softplus"):
+        import torch
+
+        from paper_2608_23794_amd import binding as mb
+        from paper_2608_23794_amd import cost, inputs
+        from paper_2608_23794_amd.layer import MoceLayer, to_device_x
+
+        self.mb = mb
+        self.wl = wl = inputs.WORKLOADS[name]
+        self.layout = layout or wl.layouts[0]
+        self.g = g = inputs.generate(wl, self.layout)
+        self.layer = layer = MoceLayer.from_workload(wl, g, self.layout, gate=gate)
+        self.gate_kind = mb.MOCE_GATE_SOFTPLUS_LINEAR if gate == "softplus" else mb.MOCE_GATE_MLP_SIGMOID
+        self.B = B = wl.B
+        self.traffic = cost.layer_traffic(B, wl.C, wl.E, wl.k, wl.HW, wl.elem_bytes)
+        per_set = self.traffic["x"] + self.traffic["y"]
+        self.per_set = per_set
+        self.nsets = nsets = max(1, math.ceil(rotate_gib * 2 ** 30 / per_set))
+        x0 = to_device_x(g["x"], wl.dtype)
+        self.xs = [x0] + [x0.clone() for _ in range(nsets - 1)]
+        self.ys = [torch.empty(layer.y_shape(B), dtype=x0.dtype, device="cuda") for _ in range(nsets)]
+        self.ws = layer.new_workspace(B)
+        self.desc = layer.desc(B)
+        self.U = layer.U if layer.nU else None
+        self.path = mb.moce_forward_path(self.desc, self.gate_kind)
+        del g["x"]
+
+    def forward(self, i, st=None):
+        n = i % self.nsets
+        self.layer.forward(self.xs[n], self.ys[n], self.ws)
+
+    def stage_times(self, n_k):
+        """Each kernel of the forward timed through its own entry point (HIP
+        graph replays), with its algorithmic bytes."""
+        import torch
+        mb, wl, B, L = self.mb, self.wl, self.B, self.layer
+        R, k, C = wl.E - 1, wl.k, wl.C
+        d = torch.empty((B, C), dtype=torch.float32, device="cuda")
+        tau = torch.empty((B, R), dtype=torch.float32, device="cuda")
+        alpha = torch.empty((B, R, k), dtype=torch.float32, device="cuda")
+        desc, nsets, xs, ys, U = self.desc, self.nsets, self.xs, self.ys, self.U
+        t_pool = launch_time_ms(lambda i, st: mb.moce_pool(desc, xs[i % nsets], d, st), n_k)
+        t_gate = launch_time_ms(lambda i, st: mb.moce_gate(desc, d, L.s_c, L.w_c, L.gate, tau, alpha, st), n_k)
+        t_mix = launch_time_ms(lambda i, st: mb.moce_mix(desc, xs[i % nsets], L.s_c, alpha, U, L.nU,
+                                                         ys[i % nsets], st), n_k)
+        tr = self.traffic
+        stages = {
+            "pool": (t_pool, tr["x"] + B * C * 4),
+            "gate": (t_gate, B * R * k * 4 + R * k * 12 + B * R * 4 + B * R * k * 4),
+            "mix": (t_mix, tr["x"] + tr["y"] + B * R * k * 4 + R * k * 4),
+        }
+        if self.path == mb.PATH_MFMA_GATE:
+            t_gm = launch_time_ms(lambda i, st: mb.moce_gate_mix(desc, xs[i % nsets], d, L.s_c, L.w_c, L.gate, U,
+                                                                 L.nU, ys[i % nsets], st), n_k)
+            kernels = {"pool": stages["pool"],
+                       "gate_mix": (t_gm, tr["x"] + tr["y"] + B * C * 4 + R * k * 12 + R * 4)}
+        else:
+            kernels = stages
+        return stages, kernels
+
+    def dense_context(self, n, stream):
+        import torch
+        wl, nsets, xs = self.wl, self.nsets, self.xs
+        C, E = wl.C, wl.E
+        Wd = torch.randn((E, C), device="cuda", dtype=torch.float32).to(xs[0].dtype)
+        if self.layout == "nchw":
+            W4 = Wd.view(E, C, 1, 1)
+            dense = lambda i: torch.nn.functional.conv2d(xs[i % nsets], W4)
+        else:
+            dense = lambda i: xs[i % nsets].view(-1, C) @ Wd.t()
+        for i in range(5):
+            dense(i)
+        t = mean_steps(dense, n, stream)
+        return {"dense_1x1_us": round(t * 1e3, 2),
+                "dense_1x1_GBps_x_plus_y": round(self.per_set / (t * 1e-3) / 1e9, 1)}
+
+    def release(self):
+        import torch
+        self.xs = self.ys = None
+        torch.cuda.empty_cache()
+
+
+def roofline_entry(kernels, path, mb, C):
+    dom = max(kernels, key=lambda n: kernels[n][0])
+    dom_ms, dom_bytes = kernels[dom]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    traffic = None
+    if dom in ("mix", "gate_mix") and path in (mb.PATH_MFMA, mb.PATH_MFMA_GATE):
+        traffic = measured_traffic(f"k_mfmamix<{C // 32}, 3, {'true' if dom == 'gate_mix' else 'false'}>")
+    return {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "algorithmic_bytes": dom_bytes}
+
+
+FORWARD_NAMES = {0: "pool, gate, mix", 1: "pool, gate, tile mix", 2: "pool, gate, matrix-core mix",
+                 3: "pool, gate inside the matrix-core mix"}
+
+
+def other_config(name, layout, args, stream):
+    bn = Bench(name, layout, args.rotate_gib)
+    mb, wl = bn.mb, bn.wl
+    n_g = 20
+    reps = 15
+    fwd = graph_times_ms(bn.forward, n_g, reps)
+    q1, med, q3 = quartiles(fwd)
+    stages, kernels = bn.stage_times(n_g)
+    rf = roofline_entry(kernels, bn.path, mb, wl.C)
+    out = {
+        "workload": name, "layout": layout, "B": wl.B, "C_in": wl.C, "C_out": wl.E, "k": wl.k,
+        "H": wl.H, "W": wl.W, "dtype": wl.dtype, "forward": FORWARD_NAMES.get(bn.path, str(bn.path)),
+        "latency_us": round(med * 1e3, 2), "latency_us_iqr": [round(q1 * 1e3, 2), round(q3 * 1e3, 2)],
+        "timing": f"HIP graph of {n_g} forwards over {bn.nsets} rotating input sets, median of {reps} replays",
+        "GBps": round(bn.traffic["metric"] / (med * 1e-3) / 1e9, 1),
+        "pct_of_hbm_peak": round(100 * bn.traffic["metric"] / (med * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+        "stage_entry_points_us": {n: round(v[0] * 1e3, 2) for n, v in stages.items()},
+        "dominant_kernel": rf["kernel"], "dominant_kernel_us": round(kernels[rf["kernel"]][0] * 1e3, 2),
+        "roofline_frac": rf["frac"],
+    }
+    if not args.no_context:
+        out["context"] = bn.dense_context(max(args.steps // 4, 10), stream)
+        out["context"]["moce_over_dense_time"] = round(med * 1e3 / out["context"]["dense_1x1_us"], 3)
+    bn.release()
+    return out
+
+
+def cpu_baseline(bench, seconds):
+    import oracle
+    oracle.build(force=False)
+    wl, g, layout = bench.wl, bench.g, bench.layout
+    from paper_2608_23794_amd import inputs
+    x = inputs.generate(wl, layout)["x"]
+    ol = oracle.NCHW if layout == "nchw" else oracle.NHWC
+    s_c, w_c, _, U_h, _ = oracle.prepare(wl.C, wl.E, g["s"], g["w"])
+
+    def one_pass():
+        dd = oracle.pool(x, ol)
+        tt = oracle.gate_softplus(dd, s_c, g["a"], g["c"])
+        al = oracle.softmax(w_c, tt)
+        oracle.mix(x, s_c, al, U_h, wl.E, ol)
+
+    def run(limit):
+        passes, t_start = 0, time.perf_counter()
+        while True:
+            one_pass()
+            passes += 1
+            if time.perf_counter() - t_start >= limit:
+                break
+        return passes, (time.perf_counter() - t_start) / passes
+
+    all_threads = oracle.threads()
+    passes, per_pass = run(seconds)
+    oracle.set_threads(1)
+    p1, per_pass_1 = run(max(seconds / 3, 1.0))
+    oracle.set_threads(all_threads)
+    metric = bench.traffic["metric"]
+    return {"value": round(metric / per_pass / 1e9, 3), "unit": "GB/s", "cores": all_threads, "kind": "oracle",
+            "sample": f"{passes} full-batch forward passes of {wl.name} (B={wl.B}), {per_pass * 1e3:.1f} ms each "
+                      f"on {all_threads} threads",
+            "single_thread": {"value": round(metric / per_pass_1 / 1e9, 4), "unit": "GB/s",
+                              "ms_per_pass": round(per_pass_1 * 1e3, 1), "passes": p1},
+            "os_cpu_count": os.cpu_count(), "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -134,74 +343,30 @@ def main():
               "with the per-GPU share).", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
-    from paper_2608_23794_amd import binding as mb
-    from paper_2608_23794_amd import cost, inputs
-    from paper_2608_23794_amd.layer import MoceLayer, to_device_x
-
-    wl = inputs.WORKLOADS[args.workload]
-    layout = args.layout or wl.layouts[0]
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    g = inputs.generate(wl, layout)
-    layer = MoceLayer.from_workload(wl, g, layout)
-    if layer.status != 0:
-        raise RuntimeError(f"support preparation failed: status {layer.status}")
-    B = wl.B
-    traffic = cost.layer_traffic(B, wl.C, wl.E, wl.k, wl.HW, wl.elem_bytes)
-    per_set = traffic["x"] + traffic["y"]
-    nsets = max(1, math.ceil(args.rotate_gib * 2 ** 30 / per_set))
-    x0 = to_device_x(g["x"], wl.dtype)
-    xs = [x0] + [x0.clone() for _ in range(nsets - 1)]
-    ys = [torch.empty(layer.y_shape(B), dtype=x0.dtype, device="cuda") for _ in range(nsets)]
-    ws = layer.new_workspace(B)
-
-    def step(i):
-        layer.forward(xs[i % nsets], ys[i % nsets], ws)
+    bn = Bench(args.workload, args.layout, args.rotate_gib, gate=args.gate)
+    mb, wl = bn.mb, bn.wl
+    if bn.layer.status != 0:
+        raise RuntimeError(f"support preparation failed: status {bn.layer.status}")
 
     for i in range(args.warmup):
-        step(i)
+        bn.forward(i)
     torch.cuda.synchronize()
-    ms = event_time_ms(step, args.steps, stream)
-    ms_warm = event_time_ms(lambda i: layer.forward(xs[0], ys[0], ws), max(args.steps // 2, 1), stream)
+    # the K timed steps with events only around them (the headline), then the
+    # same number of steps with an event between every two (the per-step
+    # distribution; an event between kernels can add a gap of its own)
+    ms = mean_steps(bn.forward, args.steps, stream)
+    _, per = timed_steps(bn.forward, args.steps, stream)
+    q1, med, q3 = quartiles(per)
+    ms_warm = mean_steps(lambda i: bn.layer.forward(bn.xs[0], bn.ys[0], bn.ws), max(args.steps // 2, 1), stream)
+    fwd_graph = quartiles(graph_times_ms(bn.forward, 20, 15))[1]
 
-    # per-kernel times of the same work through the stage entry points (the
-    # inputs rotate as in the forward's timing, so the mix reads x that is not
-    # in the infinity cache, unlike the forward's mix)
-    d = torch.empty((B, wl.C), dtype=torch.float32, device="cuda")
-    tau = torch.empty((B, wl.E - 1), dtype=torch.float32, device="cuda")
-    alpha = torch.empty((B, wl.E - 1, wl.k), dtype=torch.float32, device="cuda")
-    desc = layer.desc(B)
-    n_k = max(args.steps // 2, 10)
-    U = layer.U if layer.nU else None
-    t_pool = launch_time_ms(lambda i, st: mb.moce_pool(desc, xs[i % nsets], d, st), n_k)
-    t_gate = launch_time_ms(lambda i, st: mb.moce_gate(desc, d, layer.s_c, layer.w_c, layer.gate, tau, alpha, st),
-                            n_k)
-    t_mix = launch_time_ms(lambda i, st: mb.moce_mix(desc, xs[i % nsets], layer.s_c, alpha, U, layer.nU,
-                                                     ys[i % nsets], st), n_k)
-    R, k = wl.E - 1, wl.k
-    stages = {
-        "pool": (t_pool, traffic["x"] + B * wl.C * 4),
-        "gate": (t_gate, B * R * k * 4 + R * k * 12 + B * R * 4 + B * R * k * 4),
-        "mix": (t_mix, traffic["x"] + traffic["y"] + B * R * k * 4 + R * k * 4),
-    }
-    path = mb.moce_forward_path(desc, mb.MOCE_GATE_SOFTPLUS_LINEAR)
-    if path == mb.PATH_MFMA_GATE:
-        # the forward's second kernel: gate and mix in one (x, y, the pooled
-        # descriptors, supports, slopes, logits and offsets)
-        t_gm = launch_time_ms(lambda i, st: mb.moce_gate_mix(desc, xs[i % nsets], d, layer.s_c, layer.w_c,
-                                                             layer.gate, U, layer.nU, ys[i % nsets], st), n_k)
-        kernels = {"pool": stages["pool"],
-                   "gate_mix": (t_gm, traffic["x"] + traffic["y"] + B * wl.C * 4 + R * k * 12 + R * 4)}
-    else:
-        kernels = stages
-    dom = max(kernels, key=lambda n: kernels[n][0])
-    dom_ms, dom_bytes = kernels[dom]
-    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-
-    value = traffic["metric"] / (ms * 1e-3) / 1e9
+    stages, kernels = bn.stage_times(max(args.steps // 2, 10))
+    roof = roofline_entry(kernels, bn.path, mb, wl.C)
+    value = bn.traffic["metric"] / (ms * 1e-3) / 1e9
     line = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -216,58 +381,37 @@ def main():
         "dtype": "bf16" if wl.dtype == "bf16" else "f32",
         "accumulate": "f32",
         "data": "synthetic (seeded, shapes and distributions of the named layer)",
-        "config": {**wl.describe(), "layout": layout,
-                   "forward": {mb.PATH_TILE: "pool, gate, tile mix",
-                               mb.PATH_MFMA_GATE: "pool, gate inside the mix"}.get(path, "pool, gate, mix")},
+        "config": {**wl.describe(), "layout": bn.layout, "gate": args.gate,
+                   "forward": FORWARD_NAMES.get(bn.path, str(bn.path))},
         "latency_us": round(ms * 1e3, 2),
+        "latency_us_median": round(med * 1e3, 2),
+        "latency_us_iqr": [round(q1 * 1e3, 2), round(q3 * 1e3, 2)],
+        "latency_us_graph": round(fwd_graph * 1e3, 2),
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 1),
         "latency_us_warm_cache": round(ms_warm * 1e3, 2),
-        "bytes": {"metric": traffic["metric"], "compulsory": traffic["compulsory"]},
-        "compulsory_GBps": round(traffic["compulsory"] / (ms * 1e-3) / 1e9, 1),
-        "rotation_sets": nsets,
+        "bytes": {"metric": bn.traffic["metric"], "compulsory": bn.traffic["compulsory"]},
+        "compulsory_GBps": round(bn.traffic["compulsory"] / (ms * 1e-3) / 1e9, 1),
+        "rotation_sets": bn.nsets,
         "kernels_us": {n: round(v[0] * 1e3, 2) for n, v in kernels.items()},
         "stage_entry_points_us": {n: round(v[0] * 1e3, 2) for n, v in stages.items()},
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(f"k_mfmamix<{wl.C // 32}, 3, {'true' if dom == 'gate_mix' else 'false'}>")
-                     if dom in ("mix", "gate_mix") and path in (mb.PATH_MFMA, mb.PATH_MFMA_GATE) else None,
-                     "algorithmic_bytes": dom_bytes},
+        "roofline": roof,
     }
-
     if not args.no_context:
-        C, E = wl.C, wl.E
-        Wd = torch.randn((E, C), device="cuda", dtype=torch.float32).to(x0.dtype)
-        if layout == "nchw":
-            W4 = Wd.view(E, C, 1, 1)
-            dense = lambda i: torch.nn.functional.conv2d(xs[i % nsets], W4)
-        else:
-            dense = lambda i: xs[i % nsets].view(-1, C) @ Wd.t()
-        for i in range(5):
-            dense(i)
-        t_dense = event_time_ms(dense, max(args.steps // 2, 10), stream)
-        line["context"] = {"dense_1x1_us": round(t_dense * 1e3, 2),
-                           "dense_1x1_GBps_x_plus_y": round(per_set / (t_dense * 1e-3) / 1e9, 1),
-                           "moce_over_dense_time": round(ms / t_dense, 3)}
-
+        line["context"] = bn.dense_context(max(args.steps // 2, 10), stream)
+        line["context"]["moce_over_dense_time"] = round(ms * 1e3 / line["context"]["dense_1x1_us"], 3)
     if not args.no_cpu_baseline:
-        import oracle
-        oracle.build(force=False)
-        ol = oracle.NCHW if layout == "nchw" else oracle.NHWC
-        s_c, w_c, _, U_h, _ = oracle.prepare(wl.C, wl.E, g["s"], g["w"])
-        passes, t_start = 0, time.perf_counter()
-        while True:
-            dd = oracle.pool(g["x"], ol)
-            tt = oracle.gate_softplus(dd, s_c, g["a"], g["c"])
-            al = oracle.softmax(w_c, tt)
-            oracle.mix(g["x"], s_c, al, U_h, wl.E, ol)
-            passes += 1
-            if time.perf_counter() - t_start >= args.cpu_seconds:
-                break
-        per_pass = (time.perf_counter() - t_start) / passes
-        line["cpu_baseline"] = {"value": round(traffic["metric"] / per_pass / 1e9, 3), "unit": "GB/s",
-                                "cores": oracle.threads(), "kind": "oracle",
-                                "sample": f"{passes} full-batch forward passes of {wl.name} (B={B}), "
-                                          f"{per_pass * 1e3:.1f} ms each, os.cpu_count()={os.cpu_count()}"}
+        line["cpu_baseline"] = cpu_baseline(bn, args.cpu_seconds)
+    bn.release()
+
+    if not args.no_other:
+        others = {}
+        for name, layout in OTHER:
+            if (name, layout) == (args.workload, bn.layout):
+                continue
+            print(f"# bench: {name}/{layout}", file=sys.stderr, flush=True)
+            others[f"{name}/{layout}"] = other_config(name, layout, args, stream)
+        line["other_configs"] = others
+
     if args.copy_probe_mib > 0:
         n = args.copy_probe_mib * 2 ** 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)

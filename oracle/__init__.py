@@ -58,6 +58,7 @@ def _load():
         lib.moce_oracle_softmax.argtypes = [I, I, I, P, P, P]
         lib.moce_oracle_mix.argtypes = [I, I, I, I, I, I, I, P, P, P, P, I, P, P]
         lib.moce_oracle_threads.restype = I
+        lib.moce_oracle_set_threads.argtypes = [I]
         _lib = lib
     return _lib
 
@@ -72,6 +73,11 @@ def _c(a, dtype) -> np.ndarray:
 
 def threads() -> int:
     return _load().moce_oracle_threads()
+
+
+def set_threads(n: int) -> None:
+    """Sets the OpenMP thread count of the oracle's loops (results do not depend on it)."""
+    _load().moce_oracle_set_threads(int(n))
 
 
 def prepare(C: int, E: int, s: np.ndarray, w: np.ndarray):

@@ -36,6 +36,14 @@ int moce_oracle_threads(void) {
 #endif
 }
 
+void moce_oracle_set_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Exact widening of one input element to double. */
 static double load_x(const void* x, int elem, size_t idx) {
     if (elem == 0) return (double)((const float*)x)[idx];

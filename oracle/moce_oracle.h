@@ -63,8 +63,9 @@ void moce_oracle_mix(int B, int C, int E, int k, int HW, int layout, int elem,
                      const void* x, const int32_t* s, const double* alpha,
                      const int32_t* U, int nU, double* y, double* mag);
 
-/* Number of threads the OpenMP loops above use. */
+/* Number of threads the OpenMP loops above use, and a setter (n >= 1). */
 int moce_oracle_threads(void);
+void moce_oracle_set_threads(int n);
 
 #ifdef __cplusplus
 }

@@ -64,10 +64,11 @@ moce_status device_status(hipError_t e) { return e == hipSuccess ? MOCE_OK : MOC
 
 size_t elem_bytes(const Shape& sh) { return sh.elem == MOCE_F32 ? 4 : 2; }
 
-// Forward workspace: d [B][C], tau [B][R], lse [B][R], and for NCHW the
-// coefficients alpha [B][R][k]; every region starts on a 256-byte boundary.
+// Forward workspace: d [B][C], tau [B][R], the softmax statistics
+// [3][B][R] (rt, m, rzs), and for NCHW the coefficients alpha [B][R][k];
+// every region starts on a 256-byte boundary.
 struct WsLayout {
-  size_t d, tau, lse, alpha, total;
+  size_t d, tau, stats, alpha, total;
 };
 WsLayout ws_layout(const Shape& sh) {
   WsLayout l{};
@@ -76,8 +77,8 @@ WsLayout ws_layout(const Shape& sh) {
   off += round_up((size_t)sh.B * sh.C * sizeof(float));
   l.tau = off;
   off += round_up((size_t)sh.B * sh.R * sizeof(float));
-  l.lse = off;
-  off += round_up((size_t)sh.B * sh.R * sizeof(float));
+  l.stats = off;
+  off += round_up((size_t)3 * sh.B * sh.R * sizeof(float));
   l.alpha = off;
   if (sh.layout == MOCE_NCHW) off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
   l.total = off;
@@ -166,7 +167,7 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
     return device_status(moce::launch_mfmamix(sh, x, s, alpha, U, nU, y, stream));
   if (sh.R > 0 && moce::tilemix_eligible(sh))
     return device_status(moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream));
-  return device_status(moce::launch_mix(sh, x, s, alpha, nullptr, nullptr, nullptr, U, nU, y, stream));
+  return device_status(moce::launch_mix(sh, x, s, alpha, nullptr, nullptr, U, nU, y, stream));
 }
 
 moce_status moce_gate_mix(const moce_desc* desc, const void* x, const float* d, const int32_t* s, const float* w,
@@ -221,7 +222,7 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
   char* base = static_cast<char*>(ws);
   float* d = reinterpret_cast<float*>(base + l.d);
   float* tau = reinterpret_cast<float*>(base + l.tau);
-  float* lse = reinterpret_cast<float*>(base + l.lse);
+  float* stats = reinterpret_cast<float*>(base + l.stats);
   float* alpha = sh.layout == MOCE_NCHW ? reinterpret_cast<float*>(base + l.alpha) : nullptr;
 
   // pooling reads x plane by plane (the order HBM serves best) and leaves it
@@ -248,10 +249,10 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
   hipError_t e = moce::launch_pool(sh, x, d, stream);
   if (e != hipSuccess) return MOCE_ERR_DEVICE;
   if (sh.R > 0) {
-    e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, alpha ? nullptr : lse, stream);
+    e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, alpha ? nullptr : stats, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
   }
-  e = moce::launch_mix(sh, x, s, alpha, w, tau, lse, U, nU, y, stream);
+  e = moce::launch_mix(sh, x, s, alpha, w, stats, U, nU, y, stream);
   return device_status(e);
 }
 

@@ -346,16 +346,17 @@ __device__ __forceinline__ void wave_gate(const MixArgs& p, const WaveGate& wg, 
     gp = (lane >> 1) == r ? x : gp;
   }
   const float tp = softplusf(gp) + 1e-3f;
+  const float rtp = 1.f / tp;
 #pragma unroll
   for (int r = 0; r < kPre; ++r) {
-    z[r] = wg.wv[r] / __shfl(tp, 2 * r + (lane >> 5));
+    z[r] = coef_z(wg.wv[r], __shfl(rtp, 2 * r + (lane >> 5)));
     v[r] = in[r] ? z[r] : -INFINITY;
   }
   seg32_max(v, lane);
 #pragma unroll
   for (int r = 0; r < kPre; ++r) {
     // evaluated on every lane, then selected (branch-free)
-    float ex = expf(z[r] - v[r]);
+    float ex = coef_e(z[r], v[r]);
     asm volatile("" : "+v"(ex));
     z[r] = in[r] ? ex : 0.f;
     v[r] = z[r];
@@ -363,7 +364,7 @@ __device__ __forceinline__ void wave_gate(const MixArgs& p, const WaveGate& wg, 
   seg32_sum(v, lane);
 #pragma unroll
   for (int r = 0; r < kPre; ++r) {
-    float q = z[r] / v[r];
+    float q = coef_alpha(z[r], 1.f / v[r]);
     asm volatile("" : "+v"(q));
     wc.a[r] = in[r] ? q : 0.f;
   }

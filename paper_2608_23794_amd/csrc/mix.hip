@@ -14,8 +14,8 @@
 // a support channel as contiguous 16-byte loads.  Output rows y[b][p][:] are
 // written with consecutive lanes on consecutive channels.
 //
-// Coefficients come from alpha[b][o][i] or are rebuilt from the logits as
-// 2^(w * log2(e)/tau - lse * log2(e)), lse = log sum_j exp(w_j / tau).
+// Coefficients come from alpha[b][o][i] or are rebuilt from the logits and
+// the softmax statistics of (b, o) with the gate kernel's operations.
 #include "moce_internal.h"
 
 namespace moce {
@@ -94,29 +94,29 @@ template <> struct VecOf<8> { using type = uint2; };
 template <> struct VecOf<4> { using type = uint32_t; };
 template <> struct VecOf<2> { using type = uint16_t; };
 
-constexpr float kLog2e = 1.4426950408889634f;
-
-// Coefficient source for expert o of image b.
+// Coefficient source for expert o of image b: alpha as given, or rebuilt
+// from the logits and the softmax statistics with the gate's operations
+// (bit-identical to the coefficients the gate kernel writes).
 template <bool ALPHA> struct Coef;
 template <> struct Coef<true> {
   const float* row;
-  __device__ Coef(const float* alpha, const float*, const float*, const float*, int64_t bo, int o, int k)
+  __device__ Coef(const float* alpha, const float*, const float*, int64_t, int64_t bo, int o, int k)
       : row(alpha + bo * k) {}
   __device__ float operator()(int i) const { return row[i]; }
 };
 template <> struct Coef<false> {
   const float* wo;
-  float scale, shift;
-  __device__ Coef(const float*, const float* w, const float* tau, const float* lse, int64_t bo, int o, int k)
-      : wo(w + (int64_t)o * k), scale(kLog2e / tau[bo]), shift(-lse[bo] * kLog2e) {}
-  __device__ float operator()(int i) const { return __builtin_amdgcn_exp2f(fmaf(wo[i], scale, shift)); }
+  float rt, m, rzs;
+  __device__ Coef(const float*, const float* w, const float* st, int64_t n, int64_t bo, int o, int k)
+      : wo(w + (int64_t)o * k), rt(st[bo]), m(st[n + bo]), rzs(st[2 * n + bo]) {}
+  __device__ float operator()(int i) const { return coef_alpha(coef_e(coef_z(wo[i], rt), m), rzs); }
 };
 
 // ------------------------------------------------------------------ NCHW
 template <typename T, int PPL, int NW, int VB, bool ALPHA>
 __global__ void __launch_bounds__(NW * 64)
 k_mix_nchw(const T* __restrict__ x, const int32_t* __restrict__ s, const float* __restrict__ alpha,
-           const float* __restrict__ w, const float* __restrict__ tau, const float* __restrict__ lse,
+           const float* __restrict__ w, const float* __restrict__ st, int64_t nst,
            const int32_t* __restrict__ U, int nU, T* __restrict__ y, int C, int HW, int E, int R, int k,
            int tiles) {
   constexpr int TT = 64 * PPL;
@@ -152,7 +152,7 @@ k_mix_nchw(const T* __restrict__ x, const int32_t* __restrict__ s, const float* 
     for (int j = 0; j < PPL; ++j) acc[j] = 0.f;
     if (o < R) {
       const int32_t* so = s + (int64_t)o * k;
-      const Coef<ALPHA> coef(alpha, w, tau, lse, b * R + o, o, k);
+      const Coef<ALPHA> coef(alpha, w, st, nst, b * R + o, o, k);
 #pragma unroll 4
       for (int i = 0; i < k; ++i) {
         float v[PPL];
@@ -187,7 +187,7 @@ k_mix_nchw(const T* __restrict__ x, const int32_t* __restrict__ s, const float* 
 template <typename T, bool ALPHA>
 __global__ void __launch_bounds__(256)
 k_mix_nchw_global(const T* __restrict__ x, const int32_t* __restrict__ s, const float* __restrict__ alpha,
-                  const float* __restrict__ w, const float* __restrict__ tau, const float* __restrict__ lse,
+                  const float* __restrict__ w, const float* __restrict__ st, int64_t nst,
                   const int32_t* __restrict__ U, int nU, T* __restrict__ y, int C, int HW, int E, int R, int k,
                   int tiles) {
   const int64_t b = blockIdx.x / tiles;
@@ -198,7 +198,7 @@ k_mix_nchw_global(const T* __restrict__ x, const int32_t* __restrict__ s, const 
     float acc = 0.f;
     if (o < R) {
       const int32_t* so = s + (int64_t)o * k;
-      const Coef<ALPHA> coef(alpha, w, tau, lse, b * R + o, o, k);
+      const Coef<ALPHA> coef(alpha, w, st, nst, b * R + o, o, k);
       if (p < HW)
         for (int i = 0; i < k; ++i) acc = fmaf(coef(i), Elem<T>::load(xb + (int64_t)so[i] * HW), acc);
     } else if (nU > 0) {
@@ -217,7 +217,7 @@ k_mix_nchw_global(const T* __restrict__ x, const int32_t* __restrict__ s, const 
 template <typename T, int TP, int NS, bool ALPHA>
 __global__ void __launch_bounds__(64 * NS * 4)
 k_mix_nhwc(const T* __restrict__ x, const int32_t* __restrict__ s, const float* __restrict__ alpha,
-           const float* __restrict__ w, const float* __restrict__ tau, const float* __restrict__ lse,
+           const float* __restrict__ w, const float* __restrict__ st, int64_t nst,
            const int32_t* __restrict__ U, int nU, T* __restrict__ y, int C, int HW, int E, int R, int k,
            int tiles) {
   static_assert(TP % (4 * NS) == 0, "a work item's positions are read as float4");
@@ -244,7 +244,7 @@ k_mix_nhwc(const T* __restrict__ x, const int32_t* __restrict__ s, const float* 
     for (int j = 0; j < TH; ++j) acc[j] = 0.f;
     if (o < R) {
       const int32_t* so = s + (int64_t)o * k;
-      const Coef<ALPHA> coef(alpha, w, tau, lse, b * R + o, o, k);
+      const Coef<ALPHA> coef(alpha, w, st, nst, b * R + o, o, k);
 #pragma unroll 2
       for (int i = 0; i < k; ++i) {
         const float a = coef(i);
@@ -279,7 +279,7 @@ k_mix_nhwc(const T* __restrict__ x, const int32_t* __restrict__ s, const float* 
 template <typename T, bool ALPHA>
 __global__ void __launch_bounds__(256)
 k_mix_nhwc_global(const T* __restrict__ x, const int32_t* __restrict__ s, const float* __restrict__ alpha,
-                  const float* __restrict__ w, const float* __restrict__ tau, const float* __restrict__ lse,
+                  const float* __restrict__ w, const float* __restrict__ st, int64_t nst,
                   const int32_t* __restrict__ U, int nU, T* __restrict__ y, int C, int HW, int E, int R, int k) {
   const int64_t b = blockIdx.x / HW;
   const int p = (int)(blockIdx.x % HW);
@@ -288,7 +288,7 @@ k_mix_nhwc_global(const T* __restrict__ x, const int32_t* __restrict__ s, const 
     float acc = 0.f;
     if (o < R) {
       const int32_t* so = s + (int64_t)o * k;
-      const Coef<ALPHA> coef(alpha, w, tau, lse, b * R + o, o, k);
+      const Coef<ALPHA> coef(alpha, w, st, nst, b * R + o, o, k);
       for (int i = 0; i < k; ++i) acc = fmaf(coef(i), Elem<T>::load(row + so[i]), acc);
     } else if (nU > 0) {
       for (int u = 0; u < nU; ++u) acc += Elem<T>::load(row + U[u]);
@@ -309,7 +309,7 @@ void allow_lds(K kernel, size_t bytes) {
 }
 
 struct MixArgs {
-  const int32_t* s; const float* alpha; const float* w; const float* tau; const float* lse;
+  const int32_t* s; const float* alpha; const float* w; const float* st;
   const int32_t* U; int nU;
 };
 
@@ -325,7 +325,7 @@ hipError_t nchw_launch(const Shape& sh, const T* x, T* y, const MixArgs& a, hipS
   auto kern = k_mix_nchw<T, PPL, NW, VB, ALPHA>;
   allow_lds(kern, lds);
   hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * tiles)), dim3(NW * 64), lds, st, x, a.s, a.alpha, a.w,
-                     a.tau, a.lse, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k, tiles);
+                     a.st, sh.B * sh.R, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k, tiles);
   return hipGetLastError();
 }
 
@@ -351,7 +351,7 @@ hipError_t mix_nchw(const Shape& sh, const T* x, T* y, const MixArgs& a, hipStre
   if (row1 <= kLdsMax) return nchw_pick_vec<T, 1, ALPHA>(sh, x, y, a, st);
   const int tiles = (int)((sh.HW + 63) / 64);
   hipLaunchKernelGGL((k_mix_nchw_global<T, ALPHA>), dim3((unsigned)(sh.B * tiles)), dim3(256), 0, st, x, a.s,
-                     a.alpha, a.w, a.tau, a.lse, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k, tiles);
+                     a.alpha, a.w, a.st, sh.B * sh.R, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k, tiles);
   return hipGetLastError();
 }
 
@@ -362,8 +362,8 @@ hipError_t nhwc_launch(const Shape& sh, const T* x, T* y, const MixArgs& a, hipS
   const int tiles = (int)((sh.HW + TP - 1) / TP);
   auto kern = k_mix_nhwc<T, TP, NS, ALPHA>;
   allow_lds(kern, lds);
-  hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * tiles)), dim3(256 * NS), lds, st, x, a.s, a.alpha, a.w, a.tau,
-                     a.lse, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k, tiles);
+  hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * tiles)), dim3(256 * NS), lds, st, x, a.s, a.alpha, a.w, a.st,
+                     sh.B * sh.R, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k, tiles);
   return hipGetLastError();
 }
 
@@ -376,7 +376,7 @@ hipError_t mix_nhwc(const Shape& sh, const T* x, T* y, const MixArgs& a, hipStre
   if ((size_t)sh.C * 16 * sizeof(float) <= kLdsMax) return nhwc_launch<T, 16, ALPHA>(sh, x, y, a, st);
   if ((size_t)sh.C * 8 * sizeof(float) <= kLdsMax) return nhwc_launch<T, 8, ALPHA>(sh, x, y, a, st);
   hipLaunchKernelGGL((k_mix_nhwc_global<T, ALPHA>), dim3((unsigned)(sh.B * sh.HW)), dim3(256), 0, st, x, a.s,
-                     a.alpha, a.w, a.tau, a.lse, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k);
+                     a.alpha, a.w, a.st, sh.B * sh.R, a.U, a.nU, y, (int)sh.C, (int)sh.HW, sh.E, sh.R, sh.k);
   return hipGetLastError();
 }
 
@@ -390,9 +390,9 @@ hipError_t mix_typed(const Shape& sh, const T* x, T* y, const MixArgs& a, hipStr
 }  // namespace
 
 hipError_t launch_mix(const Shape& sh, const void* x, const int32_t* s, const float* alpha,
-                      const float* w, const float* tau, const float* lse, const int32_t* U, int nU,
+                      const float* w, const float* stats, const int32_t* U, int nU,
                       void* y, hipStream_t st) {
-  const MixArgs a{s, alpha, w, tau, lse, U, nU};
+  const MixArgs a{s, alpha, w, stats, U, nU};
   if (sh.elem == MOCE_F32)
     return mix_typed(sh, static_cast<const float*>(x), static_cast<float*>(y), a, st);
   return mix_typed(sh, static_cast<const uint16_t*>(x), static_cast<uint16_t*>(y), a, st);

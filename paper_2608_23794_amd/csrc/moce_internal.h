@@ -51,6 +51,43 @@ __device__ __forceinline__ float softplusf(float t) {
   return fmaxf(t, 0.f) + log1pf(expf(-fabsf(t)));
 }
 
+// ---- mixing coefficients (Sec. 3.3 Eq. 4) ----------------------------------
+// Every kernel forms coefficient i of routed expert o for image b with the
+// same operations, so a coefficient that a mix kernel rebuilds from the
+// softmax statistics of (b, o) equals the one a gate kernel writes, bit for
+// bit:
+//   rt = 1 / tau (IEEE division, once per (b, o)),   z_i = w_i * rt,
+//   m = max_i z_i,   e_i = 2^((z_i - m) * log2(e)),  rzs = 1 / sum_i e_i,
+//   alpha_i = e_i * rzs.
+// The largest entry has z_i - m = 0 and e_i = 1 exactly, so k = 1 and the
+// one-hot limit (tau -> 0 with a clear top logit) give coefficients of
+// exactly 1.  The products and the difference are kept apart (no fused
+// multiply-add), so the same bits come out wherever the helpers are inlined.
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ float coef_z(float w, float rt) {
+#pragma clang fp contract(off)
+  return w * rt;
+}
+__device__ __forceinline__ float coef_e(float z, float m) {
+#pragma clang fp contract(off)
+  const float t = (z - m) * kLog2e;
+  return __builtin_amdgcn_exp2f(t);
+}
+__device__ __forceinline__ float coef_alpha(float e, float rzs) {
+#pragma clang fp contract(off)
+  return e * rzs;
+}
+
+// Softmax statistics of the B*R (image, expert) pairs, three planes of n =
+// B*R floats: rt[n], m[n], rzs[n].
+struct Stats {
+  float* rt;
+  float* m;
+  float* rzs;
+};
+__host__ __device__ inline Stats stats_planes(float* base, int64_t n) { return Stats{base, base + n, base + 2 * n}; }
+
 // ---- launch parameters derived from a validated descriptor ---------------
 struct Shape {
   int64_t B, C, HW;
@@ -64,13 +101,15 @@ hipError_t launch_prepare(const Shape& sh, const int32_t* s, const float* w, int
                           float* w_out, uint8_t* covered, int32_t* U, int32_t* info,
                           hipStream_t st);
 hipError_t launch_pool(const Shape& sh, const void* x, float* d, hipStream_t st);
-// alpha and lse are optional outputs (nullptr: not written).
+// alpha and the softmax statistics (a block of 3 B R floats, planes as in
+// stats_planes) are optional outputs (nullptr: not written).
 hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const float* w,
-                       const moce_gate_params& g, float* tau, float* alpha, float* lse, hipStream_t st);
+                       const moce_gate_params& g, float* tau, float* alpha, float* stats, hipStream_t st);
 // alpha != nullptr: coefficients are read from alpha[B][R][k]; otherwise
-// they are rebuilt as exp(w[o][i] / tau[b][o] - lse[b][o]).
+// they are rebuilt from the logits w and the softmax statistics (a block of
+// 3 B R floats), with the gate's operations.
 hipError_t launch_mix(const Shape& sh, const void* x, const int32_t* s, const float* alpha,
-                      const float* w, const float* tau, const float* lse, const int32_t* U, int nU,
+                      const float* w, const float* stats, const int32_t* U, int nU,
                       void* y, hipStream_t st);
 
 // Tile gather-mix for NCHW bfloat16 with C <= 256 (tilemix.hip), from the

@@ -1,4 +1,4 @@
-// Device pieces shared by the tile kernels (tilemix.hip, pipe.hip): the LDS
+// Device pieces of the tile kernels (tilemix.hip): the LDS
 // tile of 64 positions by all C channels held as float32, its loads and
 // stores, and the quarter-wave expert mix that reads it.
 //

@@ -287,10 +287,8 @@ TileKernel pick_kernel(const Shape& sh) {
                                           {k_tilemix_regs<4, 1>, k_tilemix_regs<4, 2>}};
     return regs[nr - 1][np - 1];
   }
-  const int kq = rounded_k(sh);
-  if (kq == 32 && np == 1) return k_tilemix<32, 1>;
-  if (kq == 32 && np == 2) return k_tilemix<32, 2>;
-  if (kq == 64 && np == 2) return k_tilemix<64, 2>;
+  // k <= 64 with at most two expert passes always takes the register
+  // kernel above, so only the general form is instantiated here
   return k_tilemix<0, 0>;
 }
 

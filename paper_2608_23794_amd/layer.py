@@ -29,7 +29,7 @@ class MoceLayer:
     def __init__(self, C: int, E: int, k: int, H: int, W: int, dtype: str, layout: str,
                  s: np.ndarray, w: np.ndarray, gate: str = "softplus", a=None, c=None,
                  W1=None, b1=None, w2=None, b2: float = 0.0, tau_min: float = 0.2, tau_max: float = 6.0,
-                 device: str = "cuda"):
+                 device: str = "cuda", allow_invalid: bool = False):
         self.C, self.E, self.k, self.H, self.W = C, E, k, H, W
         self.R = E - 1
         self.dtype, self.layout, self.device = dtype, layout, device
@@ -56,6 +56,12 @@ class MoceLayer:
         else:
             raise ValueError(gate)
         self.status, self.nU, self.bad_expert = self.prepare(check=False)
+        # A failed preparation leaves s_c and U unspecified (channels may lie
+        # outside [0, C)), and the kernels do not validate indices.  Such a
+        # layer is only kept for inspecting the status (allow_invalid=True),
+        # and every entry method below refuses to run on it.
+        if self.status != 0 and not allow_invalid:
+            raise mb.MoceError("moce_support_prepare", self.status, f"(first bad expert {self.bad_expert})")
 
     # -- construction helpers ------------------------------------------------
     @classmethod
@@ -80,12 +86,17 @@ class MoceLayer:
     def _stream(self):
         return torch.cuda.current_stream(self.device)
 
+    def _ready(self):
+        if self.status != 0:
+            raise mb.MoceError("MoceLayer", self.status, "(support preparation failed; the layer cannot run)")
+
     # -- the C ABI -------------------------------------------------------------
     def prepare(self, check: bool = True):
         return mb.moce_support_prepare(self.desc(1), self.s, self.w, self.s_c, self.w_c, self.covered, self.U,
                                        self.info, self._stream(), check=check)
 
     def pool(self, x: torch.Tensor, d: Optional[torch.Tensor] = None) -> torch.Tensor:
+        self._ready()
         B = x.shape[0]
         if d is None:
             d = torch.empty((B, self.C), dtype=torch.float32, device=self.device)
@@ -93,6 +104,7 @@ class MoceLayer:
         return d
 
     def gate_tau(self, d: torch.Tensor, with_alpha: bool = True):
+        self._ready()
         B = d.shape[0]
         tau = torch.empty((B, self.R), dtype=torch.float32, device=self.device)
         alpha = torch.empty((B, self.R, self.k), dtype=torch.float32, device=self.device) if with_alpha else None
@@ -101,6 +113,7 @@ class MoceLayer:
 
     def gate_mix(self, x: torch.Tensor, d: torch.Tensor, y: Optional[torch.Tensor] = None) -> torch.Tensor:
         """moce_gate_mix: temperatures, coefficients and mixing in one kernel from the pooled d."""
+        self._ready()
         B = x.shape[0]
         if y is None:
             y = torch.empty(self.y_shape(B), dtype=x.dtype, device=self.device)
@@ -109,6 +122,7 @@ class MoceLayer:
         return y
 
     def mix(self, x: torch.Tensor, alpha: torch.Tensor, y: Optional[torch.Tensor] = None) -> torch.Tensor:
+        self._ready()
         B = x.shape[0]
         if y is None:
             y = torch.empty(self.y_shape(B), dtype=x.dtype, device=self.device)
@@ -123,6 +137,7 @@ class MoceLayer:
 
     def forward(self, x: torch.Tensor, y: Optional[torch.Tensor] = None,
                 ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+        self._ready()
         B = x.shape[0]
         if y is None:
             y = torch.empty(self.y_shape(B), dtype=x.dtype, device=self.device)

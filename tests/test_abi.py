@@ -202,13 +202,13 @@ def test_gate_parameter_errors(lib):
 def test_workspace_size_and_errors(lib):
     desc = good_desc()
     need = lib.moce_forward_workspace_bytes(ctypes.byref(desc))
-    # d [2][64] + tau [2][15] + lse [2][15] + alpha [2][15][8], each rounded up to 256 bytes
-    assert need == 512 + 256 + 256 + 1024
+    # d [2][64] + tau [2][15] + softmax statistics [3][2][15] + alpha [2][15][8], each rounded up to 256 bytes
+    assert need == 512 + 256 + 512 + 1024
     gate = mb.make_gate(a=FAKE, c=FAKE)
     assert _call_forward(desc, gate, ws=None) == -7
     assert _call_forward(desc, gate, ws_bytes=need - 1) == -7
     nhwc = good_desc(layout=mb.MOCE_NHWC)
-    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 256
+    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 512
 
 
 def test_prepare_limits(lib):

@@ -145,9 +145,13 @@ def test_prepare_rejects_invalid_rows_like_the_oracle(bad):
         s[o, 4] = C + 5
     with pytest.raises(oracle.SupportError) as ei:
         oracle.prepare(C, E, s, w)
-    layer = MoceLayer(C, E, k, 2, 2, "f32", "nchw", s, w, a=np.zeros((R, k)), c=np.zeros(R))
+    with pytest.raises(mb.MoceError):
+        MoceLayer(C, E, k, 2, 2, "f32", "nchw", s, w, a=np.zeros((R, k)), c=np.zeros(R))
+    layer = MoceLayer(C, E, k, 2, 2, "f32", "nchw", s, w, a=np.zeros((R, k)), c=np.zeros(R), allow_invalid=True)
     assert layer.status == -5
     assert layer.bad_expert == ei.value.expert == o
+    with pytest.raises(mb.MoceError):  # an invalid layer refuses to run
+        layer.forward(torch.zeros((1, C, 2, 2), dtype=torch.float32, device="cuda"))
 
 
 # --------------------------------------------------------------------------- pool / gate / mix
@@ -174,7 +178,7 @@ def test_gate_softplus_isolated(name):
     check_tau_alpha(tau.cpu().numpy(), tau_ref, alpha.cpu().numpy(), alpha_ref)
 
 
-@pytest.mark.parametrize("name", ["tiny", "resnet50_stage1", "resnet50_stage3"])
+@pytest.mark.parametrize("name", ["tiny", "resnet50_stage1", "resnet50_stage3", "resnet50_stage4", "vit_tokens"])
 def test_gate_mlp_isolated(name):
     wl = inputs.WORKLOADS[name]
     g = inputs.generate(wl, with_x=False)
@@ -209,7 +213,8 @@ def test_forward(name, layout):
     print(f"{name}/{layout}: max |y - y_ref| / M = {e:.3e}")
 
 
-@pytest.mark.parametrize("name,layout", [("tiny", "nchw"), ("resnet50_stage3", "nchw"), ("vit_tokens", "nhwc")])
+@pytest.mark.parametrize("name,layout", [("tiny", "nchw"), ("resnet50_stage3", "nchw"), ("resnet50_stage3", "nhwc"),
+                                         ("resnet50_stage4", "nhwc"), ("vit_tokens", "nhwc")])
 def test_forward_mlp_gate(name, layout):
     wl = inputs.WORKLOADS[name]
     g = inputs.generate(wl, layout)
@@ -291,16 +296,69 @@ def test_forward_edge_cases(B, C, E, k, H, W, dtype, layout, extra):
         assert np.array_equal(routed, rr)
 
 
-def test_one_hot_limit_is_an_exact_copy():
+@pytest.mark.parametrize("dtype,layout", [("bf16", "nchw"), ("f32", "nchw"), ("bf16", "nhwc"), ("f32", "nhwc")])
+def test_one_hot_limit_is_an_exact_copy(dtype, layout):
+    """tau at its floor (c = -1e4) with a clear top logit: every routed output is an exact copy of its
+    top channel, in every layout and element type (the coefficients are exactly 1 and 0)."""
     B, C, E, k, H, W = 2, 80, 12, 6, 8, 8
-    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=77)
+    x, s, w, a, c = _custom(B, C, E, k, H, W, dtype, layout, seed=77, signed=True)
     w[:, 0] = w.max(axis=1) + 1.0       # a clear top logit
     a[:] = 0.0
     c[:] = -1e4                          # tau = 1e-3
-    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
-    layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
-    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
-    assert np.array_equal(y[:, :E - 1], ref["y"][:, :E - 1])
+    ref = oracle.forward(x, s, w, E, OL[layout], a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, dtype, layout, s, w, a=a, c=c)
+    y = to_host_f64(layer.forward(to_device_x(x, dtype)))
+    routed = (lambda t: t[:, :E - 1]) if layout == "nchw" else (lambda t: t[..., :E - 1])
+    assert np.array_equal(routed(y), routed(ref["y"]))
+
+
+@pytest.mark.parametrize("dtype,layout", [("f32", "nhwc"), ("bf16", "nhwc"), ("f32", "nchw")])
+def test_forward_low_temperature_mlp_gate(dtype, layout):
+    """The paper's gate with a low temperature floor (tau_min = 0.01, g pushed negative): the
+    coefficients are near one-hot, where rebuilding them from the softmax statistics must not lose
+    precision against the oracle."""
+    B, C, E, k, H, W = 3, 96, 20, 12, 6, 6
+    x, s, w, a, c = _custom(B, C, E, k, H, W, dtype, layout, seed=5, signed=True)
+    rng = np.random.default_rng(6)
+    W1 = (rng.standard_normal((k, k)) * k ** -0.5).astype(np.float32)
+    b1 = (rng.standard_normal(k) * 0.1).astype(np.float32)
+    w2 = (rng.standard_normal(k) * k ** -0.5).astype(np.float32)
+    b2 = np.float32(-12.0)
+    ref = oracle.forward(x, s, w, E, OL[layout], gate="mlp", W1=W1, b1=b1, w2=w2, b2=b2, tau_min=0.01,
+                         tau_max=6.0)
+    assert ref["tau"].max() < 0.02
+    layer = MoceLayer(C, E, k, H, W, dtype, layout, s, w, gate="mlp", W1=W1, b1=b1, w2=w2, b2=b2,
+                      tau_min=0.01, tau_max=6.0)
+    xd = to_device_x(x, dtype)
+    tau, alpha = layer.gate_tau(layer.pool(xd))
+    check_tau_alpha(tau.cpu().numpy(), ref["tau"], alpha.cpu().numpy(), ref["alpha"])
+    check_y(to_host_f64(layer.forward(xd)), ref["y"], ref["mag"], dtype)
+
+
+GENERIC_STAGES = [
+    # B, C, E, k, H, W, dtype, layout: the generic kernels, where the forward rebuilds the
+    # coefficients from the softmax statistics instead of reading them
+    (4, 96, 20, 12, 6, 6, "bf16", "nhwc"),
+    (2, 64, 16, 8, 8, 8, "f32", "nchw"),
+    (3, 64, 16, 8, 8, 8, "f32", "nhwc"),
+    (2, 300, 40, 70, 5, 5, "bf16", "nhwc"),
+]
+
+
+@pytest.mark.parametrize("B,C,E,k,H,W,dtype,layout", GENERIC_STAGES)
+def test_generic_forward_equals_stages(B, C, E, k, H, W, dtype, layout):
+    """The forward's rebuilt coefficients equal those moce_gate writes, bit for bit, so the forward
+    and pool + gate + mix agree bit for bit."""
+    x, s, w, a, c = _custom(B, C, E, k, H, W, dtype, layout, seed=B * 7 + k, signed=True)
+    layer = MoceLayer(C, E, k, H, W, dtype, layout, s, w, a=a, c=c)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_GENERIC
+    xd = to_device_x(x, dtype)
+    y = layer.forward(xd)
+    _, alpha = layer.gate_tau(layer.pool(xd))
+    y_st = layer.mix(xd, alpha)
+    torch.cuda.synchronize()
+    iv = torch.int16 if dtype == "bf16" else torch.int32
+    assert torch.equal(y.view(iv), y_st.view(iv))
 
 
 @pytest.mark.parametrize("layout", ["nchw", "nhwc"])
@@ -413,6 +471,10 @@ TILED = [
     (4, 88, 24, 12, 28, 30),     # ragged last tile
     (2, 256, 96, 16, 16, 16),    # E above the MFMA path's 64
     (2, 48, 2, 5, 8, 8),         # one routed expert, k not a multiple of 4
+    (3, 200, 20, 40, 8, 16),     # 33 <= k <= 48: three register rows per expert, one expert pass
+    (2, 200, 40, 45, 8, 8),      # three register rows, two expert passes
+    (2, 168, 30, 56, 12, 12),    # 49 <= k <= 64: four register rows, one pass
+    (2, 200, 50, 60, 8, 8),      # four register rows, two passes
 ]
 
 
