@@ -183,6 +183,26 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
                          const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
                          void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Bytes of the device array that moce_forward_static uses as its workspace. */
+#define MOCE_STATIC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/* The whole layer, as moce_forward, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): no workspace argument and no allocation.  The
+ * workspace is a fixed array of MOCE_STATIC_SCRATCH_BYTES inside the library,
+ * one per GPU, held from the library's load until the process ends; its
+ * device address is looked up on the first call on each device.  Same
+ * arguments, kernels and results as moce_forward.  Errors: those of
+ * moce_forward, and MOCE_ERR_WORKSPACE (before any launch) when
+ * moce_forward_workspace_bytes(desc) exceeds MOCE_STATIC_SCRATCH_BYTES;
+ * MOCE_ERR_DEVICE if the array's address cannot be obtained.  Every call on
+ * one GPU shares that array: calls that overlap on the same device (on
+ * different streams or from different host threads) race, and the caller
+ * must serialise them. */
+moce_status moce_forward_static(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
+                                const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
+                                hipStream_t stream);
+
 /* Static string naming a status code. */
 const char* moce_status_str(int status);
 

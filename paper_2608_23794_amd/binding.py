@@ -29,9 +29,11 @@ STATUS = {
 # Every function include/moce.h declares, in declaration order.
 ENTRY_POINTS = (
     "moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix",
-    "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_status_str",
-    "moce_abi_version",
+    "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_forward_static",
+    "moce_status_str", "moce_abi_version",
 )
+
+MOCE_STATIC_SCRATCH_BYTES = 16 << 20
 
 
 class MoceError(RuntimeError):
@@ -80,10 +82,12 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_forward_workspace_bytes.restype = SZ
     lib.moce_forward_path.argtypes = [D, ctypes.c_int]
     lib.moce_forward.argtypes = [D, P, P, P, G, P, I32, P, P, SZ, P]
+    lib.moce_forward_static.argtypes = [D, P, P, P, G, P, I32, P, P]
     lib.moce_status_str.argtypes = [ctypes.c_int]
     lib.moce_status_str.restype = ctypes.c_char_p
     lib.moce_abi_version.restype = ctypes.c_int
-    for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward"):
+    for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward",
+                 "moce_forward_static"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -179,6 +183,12 @@ def moce_forward(desc: moce_desc, x, s, w, gate: moce_gate_params, U, nU: int, y
     _check("moce_forward", load().moce_forward(ctypes.byref(desc), _ptr(x), _ptr(s), _ptr(w),
                                                ctypes.byref(gate), _ptr(U), nU, _ptr(y), _ptr(ws),
                                                ws_bytes, _stream(stream)))
+
+
+def moce_forward_static(desc: moce_desc, x, s, w, gate: moce_gate_params, U, nU: int, y, stream=None) -> None:
+    _check("moce_forward_static", load().moce_forward_static(ctypes.byref(desc), _ptr(x), _ptr(s), _ptr(w),
+                                                             ctypes.byref(gate), _ptr(U), nU, _ptr(y),
+                                                             _stream(stream)))
 
 
 def raw_status(fn: str, *args) -> int:

@@ -5,6 +5,7 @@
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "moce_internal.h"
 
@@ -202,23 +203,31 @@ int moce_forward_path(const moce_desc* desc, int gate_kind) {
   return sh.R > 0 && moce::tilemix_eligible(sh) ? MOCE_PATH_TILE : MOCE_PATH_GENERIC;
 }
 
-moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
-                         const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y, void* ws,
-                         size_t ws_bytes, hipStream_t stream) {
-  Shape sh;
-  moce_status st = check_desc(desc, &sh);
+}  // extern "C"
+
+namespace {
+
+// The host-side checks of the forward's arguments other than the workspace.
+moce_status check_forward(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
+                          const moce_gate_params* gate, const int32_t* U, int32_t nU, const void* y, Shape* sh) {
+  moce_status st = check_desc(desc, sh);
   if (st != MOCE_OK) return st;
-  st = check_gate(sh, gate);
+  st = check_gate(*sh, gate);
   if (st != MOCE_OK) return st;
   if (!x || !y) return MOCE_ERR_NULL;
-  if (sh.R > 0 && (!s || !w)) return MOCE_ERR_NULL;
-  if (nU < 0 || (int64_t)nU > sh.C) return MOCE_ERR_SHAPE;
+  if (sh->R > 0 && (!s || !w)) return MOCE_ERR_NULL;
+  if (nU < 0 || (int64_t)nU > sh->C) return MOCE_ERR_SHAPE;
   if (nU > 0 && !U) return MOCE_ERR_NULL;
   if (!aligned(x, 16) || !aligned(y, 16)) return MOCE_ERR_ALIGN;
-  const WsLayout l = ws_layout(sh);
-  if (!ws || ws_bytes < l.total) return MOCE_ERR_WORKSPACE;
-  if (!aligned(ws, kAlign)) return MOCE_ERR_ALIGN;
+  return MOCE_OK;
+}
 
+// The forward's launches on a validated call, with the workspace at `ws`
+// (device memory of at least ws_layout(sh).total bytes, 256-byte aligned).
+moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, const float* w,
+                           const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y, void* ws,
+                           hipStream_t stream) {
+  const WsLayout l = ws_layout(sh);
   char* base = static_cast<char*>(ws);
   float* d = reinterpret_cast<float*>(base + l.d);
   float* tau = reinterpret_cast<float*>(base + l.tau);
@@ -254,6 +263,64 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
   }
   e = moce::launch_mix(sh, x, s, alpha, w, stats, U, nU, y, stream);
   return device_status(e);
+}
+
+// ---- the forward without a workspace argument ------------------------------
+//
+// Its workspace is this file-scope device array.  In host code the array's
+// name is only a stand-in for the symbol, not a device address: the address
+// comes from hipGetSymbolAddress, taken once per device with that device
+// current, and only that address is ever handed to a kernel.
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+static_assert(kStaticScratchBytes == MOCE_STATIC_SCRATCH_BYTES, "header and library agree on the size");
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device (taken on the first
+// call there), or nullptr if the runtime cannot provide it.
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
+                         const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  Shape sh;
+  const moce_status st = check_forward(desc, x, s, w, gate, U, nU, y, &sh);
+  if (st != MOCE_OK) return st;
+  if (!ws || ws_bytes < ws_layout(sh).total) return MOCE_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return MOCE_ERR_ALIGN;
+  return forward_launch(sh, x, s, w, gate, U, nU, y, ws, stream);
+}
+
+moce_status moce_forward_static(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
+                                const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
+                                hipStream_t stream) {
+  Shape sh;
+  const moce_status st = check_forward(desc, x, s, w, gate, U, nU, y, &sh);
+  if (st != MOCE_OK) return st;
+  if (ws_layout(sh).total > kStaticScratchBytes) return MOCE_ERR_WORKSPACE;
+  void* ws = scratch_on_current_device();
+  if (!ws) return MOCE_ERR_DEVICE;
+  // every region of the workspace is written before it is read (d by the
+  // pooling, tau and the statistics or coefficients by the gate), so nothing
+  // left by an earlier call is ever used
+  return forward_launch(sh, x, s, w, gate, U, nU, y, ws, stream);
 }
 
 }  // extern "C"

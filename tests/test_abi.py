@@ -213,3 +213,27 @@ def test_workspace_size_and_errors(lib):
 
 def test_prepare_limits(lib):
     assert _call_prepare(good_desc(C=1 << 25, H=1, W=1, E=2, k=4097)) == -10
+
+
+def _call_static(desc, gate, x=FAKE, s=FAKE, w=FAKE, U=FAKE, nU=0, y=FAKE):
+    g = ctypes.byref(gate) if gate is not None else None
+    return mb.raw_status("moce_forward_static", ctypes.byref(desc), x, s, w, g, U, nU, y, None)
+
+
+def test_forward_static_host_errors(lib):
+    """The forward without a workspace argument: every host-side check runs before the library looks up
+    its device array, including the size limit of that array."""
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+    for change, code in BAD_DESCS:
+        assert _call_static(good_desc(**change), gate) == code
+    desc = good_desc()
+    assert _call_static(desc, None) == -1
+    assert _call_static(desc, gate, x=None) == -1
+    assert _call_static(desc, gate, w=None) == -1
+    assert _call_static(desc, gate, U=None, nU=2) == -1
+    assert _call_static(desc, gate, nU=65) == -2
+    assert _call_static(desc, gate, y=FAKE_UNALIGNED) == -8
+    # a workspace beyond the array: B * R * k coefficients of 4 bytes alone exceed 16 MiB
+    big = good_desc(B=64, C=4096, E=4096, k=64, H=2, W=2)
+    assert lib.moce_forward_workspace_bytes(ctypes.byref(big)) > mb.MOCE_STATIC_SCRATCH_BYTES
+    assert _call_static(big, gate) == -7
