@@ -150,14 +150,25 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
                      const int32_t* U, int32_t nU, void* y, hipStream_t stream);
 
 /* Bytes of device workspace moce_forward needs for `desc` (0 on an invalid
- * descriptor).  The workspace holds the descriptor d and the temperatures. */
+ * descriptor).  The workspace holds the descriptor d, the temperatures, the
+ * softmax statistics and, depending on the path, the coefficients or the
+ * support schedule. */
 size_t moce_forward_workspace_bytes(const moce_desc* desc);
 
 /* Paths moce_forward can take. */
-enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1, MOCE_PATH_MFMA = 2, MOCE_PATH_MFMA_GATE = 3 };
+enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1, MOCE_PATH_MFMA = 2, MOCE_PATH_MFMA_GATE = 3,
+       MOCE_PATH_SCHEDULED = 4 };
 
-/* The path moce_forward takes for `desc` after plane-wise pooling (moce_mix
- * takes the same kernels, MOCE_PATH_MFMA for MOCE_PATH_MFMA_GATE):
+/* The path moce_forward takes for `desc` (moce_mix takes the same kernels,
+ * MOCE_PATH_MFMA for MOCE_PATH_MFMA_GATE, MOCE_PATH_GENERIC for
+ * MOCE_PATH_SCHEDULED):
+ *  MOCE_PATH_SCHEDULED: channels-last bfloat16 (C a multiple of 64 up to
+ *     8192, E a multiple of 8): pooling, the gate's softmax statistics, then
+ *     a schedule of the supports by 32-channel step (Sec. 3.2: static
+ *     supports) and the routed and residual outputs as a dense bf16 product
+ *     on the matrix cores whose coefficient operand is written step by step
+ *     from the schedule (coefficients split into two bf16 parts: 16
+ *     significant bits);
  *  MOCE_PATH_MFMA_GATE: MOCE_PATH_MFMA with the softplus-linear gate
  *     evaluated inside the mix kernel, as moce_gate_mix (k = 32);
  *  MOCE_PATH_MFMA: the gate kernel, then the routed and residual outputs of an image as one dense

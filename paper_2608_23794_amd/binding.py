@@ -166,7 +166,7 @@ def moce_forward_workspace_bytes(desc: moce_desc) -> int:
     return int(load().moce_forward_workspace_bytes(ctypes.byref(desc)))
 
 
-PATH_GENERIC, PATH_TILE, PATH_MFMA, PATH_MFMA_GATE = 0, 1, 2, 3
+PATH_GENERIC, PATH_TILE, PATH_MFMA, PATH_MFMA_GATE, PATH_SCHEDULED = 0, 1, 2, 3, 4
 
 
 def moce_forward_path(desc: moce_desc, gate_kind: int) -> int:

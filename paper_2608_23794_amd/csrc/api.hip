@@ -69,7 +69,7 @@ size_t elem_bytes(const Shape& sh) { return sh.elem == MOCE_F32 ? 4 : 2; }
 // [3][B][R] (rt, m, rzs), and for NCHW the coefficients alpha [B][R][k];
 // every region starts on a 256-byte boundary.
 struct WsLayout {
-  size_t d, tau, stats, alpha, total;
+  size_t d, tau, stats, alpha, sched, total;
 };
 WsLayout ws_layout(const Shape& sh) {
   WsLayout l{};
@@ -82,6 +82,8 @@ WsLayout ws_layout(const Shape& sh) {
   off += round_up((size_t)3 * sh.B * sh.R * sizeof(float));
   l.alpha = off;
   if (sh.layout == MOCE_NCHW) off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
+  l.sched = off;
+  if (moce::gmix_eligible(sh)) off += round_up(moce::gmix_sched_bytes(sh));
   l.total = off;
   return l;
 }
@@ -198,6 +200,7 @@ int moce_forward_path(const moce_desc* desc, int gate_kind) {
   const moce_status st = check_desc(desc, &sh);
   if (st != MOCE_OK) return st;
   if (gate_kind != MOCE_GATE_SOFTPLUS_LINEAR && gate_kind != MOCE_GATE_MLP_SIGMOID) return MOCE_ERR_GATE;
+  if (moce::gmix_eligible(sh)) return MOCE_PATH_SCHEDULED;
   if (moce::mfmamix_gate_fusable(sh, gate_kind)) return MOCE_PATH_MFMA_GATE;
   if (moce::mfmamix_eligible(sh)) return MOCE_PATH_MFMA;
   return sh.R > 0 && moce::tilemix_eligible(sh) ? MOCE_PATH_TILE : MOCE_PATH_GENERIC;
@@ -254,6 +257,15 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
     e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, nullptr, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
     return device_status(moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream));
+  }
+  if (moce::gmix_eligible(sh)) {
+    // channels-last on the matrix cores: pooling, the gate's softmax
+    // statistics, then the schedule and the mix
+    hipError_t e = moce::launch_pool(sh, x, d, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    e = moce::launch_gate(sh, d, s, w, *gate, tau, nullptr, stats, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    return device_status(moce::launch_gmix(sh, x, s, w, stats, U, nU, base + l.sched, y, stream));
   }
   hipError_t e = moce::launch_pool(sh, x, d, stream);
   if (e != hipSuccess) return MOCE_ERR_DEVICE;

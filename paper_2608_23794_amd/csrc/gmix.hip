@@ -1,0 +1,640 @@
+// Channels-last mixing as a dense product on the matrix cores, driven by a
+// channel schedule of the static supports (Sec. 3.2: the supports are fixed at
+// inference, so where every coefficient lands can be worked out ahead of the
+// products).
+//
+// For one image b the routed outputs (Sec. 3.3 Eq. 5) and the residual output
+// (Sec. 3.4 Eq. 6) are y_b = A_b x_b, with row o < E-1 of A_b holding
+// alpha[b][o][i] at column s[o][i] and row E-1 holding 1/|U| at the uncovered
+// channels.  With x channels-last, a tile of positions x 32 channels is
+// already the layout of the MFMA's A operand, so this kernel evaluates
+// y^T = x^T A_b^T with 16x16x32 bf16 MFMAs over 32-channel steps, positions
+// as M and experts as N.  A_b is 1/16 dense at the ResNet-50 stage-3/4 and
+// ViT shapes; the matrix cores still run the dense product faster than the
+// vector ALUs run the gather form.
+//
+// The schedule.  Dense A_b is never built: per 32-channel step only the
+// support entries whose channel falls in the step are written into zeroed LDS
+// rows of A_b^T (the B operand), and they are cleared again two steps later,
+// before the next entries go into the same buffer.  A small kernel (k_sched)
+// buckets the entries by step once per forward, one bucket per builder wave
+// of a mix workgroup, each entry carrying the LDS byte offset of its slot.
+//
+// Exactness.  x is bf16; each float32 coefficient is split into NS bf16 parts
+// (hi, the rounded remainder, and with NS = 3 the remainder of that), one
+// MFMA per part, accumulated in float32.  Three parts sum to the coefficient
+// exactly; two carry it to 16 significant bits (relative error at most 2^-17,
+// 2^8 below the rounding of the bf16 output).
+//
+// Work split.  A workgroup takes MT = 16 MB positions of one image and
+// NE = 64 NB consecutive experts (4 NB groups of 16) and walks the C/32
+// channel steps with three kinds of waves meeting at one barrier per step:
+//  - four consumer waves: wave w owns N blocks NB w .. NB w + NB - 1 and all
+//    MT positions, and only issues LDS reads and MFMAs;
+//  - eight builder waves: builder j owns the expert groups j and j + 8 of the
+//    range and writes their B rows: at step ks it clears its entries of step
+//    ks - 1 and writes those of step ks + 1 (in the buffer the consumers left
+//    at the barrier).  Each builder owns whole rows, so no two waves ever
+//    touch one slot.  The schedule is prefetched several steps ahead into
+//    registers, and the bucket's offsets sit in registers, so a step never
+//    waits on memory; eight waves (two per SIMD) keep the dependent chains of
+//    the coefficient arithmetic overlapped;
+//  - two loader waves: copy 64-channel chunks of the x tile straight into a
+//    ring of LDS buffers with global-to-LDS loads, several chunks in flight.
+// At the end the consumers stage their results in LDS and every wave writes
+// whole rows of y.
+#include <algorithm>
+#include <utility>
+
+#include "moce_internal.h"
+
+namespace moce {
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+#define GMIX_LDS __attribute__((address_space(3)))
+
+constexpr int kStep = 32;                 // channels per step (the MFMA's K)
+constexpr int kChunk = 64;                // channels per x copy (two steps)
+constexpr int kXRow = kChunk * 2;         // bytes of one position row of an x chunk
+constexpr int kBRow = kStep * 2;          // bytes of one expert row of a B buffer part
+constexpr int kMaxXRing = 8;              // x chunk buffers at most (the ring fills the LDS left over)
+constexpr int kConsumers = 4;
+constexpr int kBuilders = 8;
+constexpr int kLoaders = 2;
+constexpr int kWaves = kConsumers + kBuilders + kLoaders;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kGroup = 16;                // experts per group (one MFMA N block)
+constexpr int kGroupsPerBuilder = 2;      // 4 NB <= 16 groups per workgroup over 8 builders
+constexpr int kMaxSteps = 64;             // C <= 2048: offsets 0 .. 63 in one register, the total beside
+constexpr int kRounds = 3;                // 64-entry rounds of a builder's step held in registers
+constexpr int kAhead = 6;                 // steps of schedule a builder holds in registers (even)
+constexpr int kCachePolicyNT = 2;         // non-temporal bit of the global-to-LDS load
+constexpr int kLdsBytes = 160 * 1024;
+
+// Schedule entry: x = byte offset of the coefficient's slot in one part of a
+// B buffer (14 bits) | the expert's slot within the workgroup's expert range
+// << 14 (8 bits) | residual flag << 22; y = the selected logit's bits.
+constexpr uint32_t kOffMask = 0x3fff;
+constexpr int kSlotShift = 14;
+constexpr uint32_t kResidualFlag = 1u << 22;
+
+// byte offset of B[o][c] (o: expert within the workgroup, c: channel within
+// the step) in one part of a B buffer: 16-byte chunk c/8 of row o, rotated by
+// (o / 4) mod 4 so that 16 consecutive rows read at one chunk hit 16
+// different bank groups
+__host__ __device__ inline int b_off(int o, int c) {
+  return o * kBRow + ((((c >> 3) ^ (o >> 2)) & 3) << 4) + ((c & 7) << 1);
+}
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// s_waitcnt operand: at most n vector memory operations of this wave
+// outstanding (the LDS/scalar and export counters left at their maxima)
+constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+struct GmArgs {
+  const uint16_t* x;
+  uint16_t* y;
+  const int32_t* off;   // [buckets][nsteps + 1]
+  const uint2* ent;     // [buckets][cap]
+  const float* st;      // softmax statistics, three planes of B R floats
+  int64_t nst;          // B R
+  int C, HW, E, R, nU;
+  int nsteps, ngroups, cap;
+  int nt, nq;           // position tiles per image, expert ranges per image
+  int units, per;       // work units, units per XCD slot
+  float inv_nU;
+};
+
+// ---------------------------------------------------------------- schedule
+// Bucket (q, j) holds the entries of expert groups j and j + 8 of expert
+// range q (the ng groups of one mix workgroup), the residual row E-1 included
+// where it falls there, counted and placed by step.  Order within a step is
+// free: every entry writes its own slot of A_b.
+__global__ void __launch_bounds__(256)
+k_sched(const int32_t* __restrict__ s, const float* __restrict__ w, const int32_t* __restrict__ U, int nU, int R,
+        int k, int nsteps, int cap, int ng, int ngroups, int32_t* __restrict__ off, uint2* __restrict__ ent) {
+  __shared__ int cnt[kMaxSteps];
+  __shared__ int cur[kMaxSteps];
+  const int q = blockIdx.x / kBuilders, j = blockIdx.x % kBuilders, tid = threadIdx.x;
+  // the bucket's groups and their entry counts
+  int gid[kGroupsPerBuilder], nr[kGroupsPerBuilder], first[kGroupsPerBuilder + 1];
+  first[0] = 0;
+#pragma unroll
+  for (int h = 0; h < kGroupsPerBuilder; ++h) {
+    const int gl = j + kBuilders * h;
+    gid[h] = q * ng + gl;
+    const bool live = gl < ng && gid[h] < ngroups;
+    const int o_first = gid[h] * kGroup;
+    nr[h] = live ? max(0, min(kGroup, R - o_first)) * k : 0;
+    const int nres = live && R >= o_first && R < o_first + kGroup ? nU : 0;
+    first[h + 1] = first[h] + nr[h] + nres;
+  }
+  const int total = first[kGroupsPerBuilder];
+  // entry e of the bucket: (expert, channel, logit, residual?)
+  auto entry = [&](int e, int& o, int& c, float& wv, bool& res) __attribute__((always_inline)) {
+    int h = 0;
+#pragma unroll
+    for (int t = 1; t < kGroupsPerBuilder; ++t) h += e >= first[t] ? 1 : 0;
+    const int r = e - first[h];
+    const int o_first = gid[h] * kGroup;
+    res = r >= nr[h];
+    if (!res) {
+      o = o_first + r / k;
+      c = s[(int64_t)o_first * k + r];
+      wv = w[(int64_t)o_first * k + r];
+    } else {
+      o = R;
+      c = U[r - nr[h]];
+      wv = 0.f;
+    }
+  };
+  for (int t = tid; t < nsteps; t += 256) cnt[t] = 0;
+  __syncthreads();
+  for (int e = tid; e < total; e += 256) {
+    int o, c;
+    float wv;
+    bool res;
+    entry(e, o, c, wv, res);
+    atomicAdd(&cnt[c >> 5], 1);
+  }
+  __syncthreads();
+  // exclusive scan of the counts (nsteps <= 64: one wave)
+  int32_t* ob = off + (int64_t)blockIdx.x * (nsteps + 1);
+  if (tid < 64) {
+    const int v = tid < nsteps ? cnt[tid] : 0;
+    int incl = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int t = __shfl_up(incl, d, 64);
+      if (tid >= d) incl += t;
+    }
+    if (tid < nsteps) {
+      cur[tid] = incl - v;
+      ob[tid] = incl - v;
+    }
+    if (tid == 63) ob[nsteps] = incl;
+  }
+  __syncthreads();
+  const int ne = ng * kGroup;
+  uint2* eb = ent + (int64_t)blockIdx.x * cap;
+  for (int e = tid; e < total; e += 256) {
+    int o, c;
+    float wv;
+    bool res;
+    entry(e, o, c, wv, res);
+    const int pos = atomicAdd(&cur[c >> 5], 1);
+    const int ow = o - q * ne;  // the expert's slot within the range
+    const uint32_t packed = (uint32_t)b_off(ow, c & 31) | ((uint32_t)ow << kSlotShift) | (res ? kResidualFlag : 0u);
+    eb[pos] = make_uint2(packed, __float_as_uint(wv));
+  }
+}
+
+// ---------------------------------------------------------------- the mix
+template <int MB, int NB, int NS>
+struct Layout {
+  static constexpr int MT = 16 * MB;                 // positions per tile
+  static constexpr int NE = 64 * NB;                 // experts per workgroup
+  static constexpr int XBUF = MT * kXRow;            // one x chunk
+  static constexpr int PART = NE * kBRow;            // one part of one B buffer
+  static constexpr int BBUF = NS * PART;             // one B buffer
+  // as many x chunks in flight as the LDS left by the B buffers and the
+  // statistics allows: at most kMaxXRing, and so that one loader wave's
+  // outstanding copies stay within its 6-bit counter
+  static constexpr int XR_FIT = (kLdsBytes - 1024 - 2 * BBUF - 16 * NE) / XBUF;
+  static constexpr int ROUNDS = MB;                  // 16-byte copies per loader lane per chunk (MT / 16)
+  static constexpr int XR_CNT = 63 / ROUNDS + 1;
+  static constexpr int XR = XR_FIT < kMaxXRing ? (XR_FIT < XR_CNT ? XR_FIT : XR_CNT)
+                                               : (kMaxXRing < XR_CNT ? kMaxXRing : XR_CNT);
+  static_assert(XR >= 2, "at least two x chunk buffers");
+  static constexpr int OFF_X = 0;
+  static constexpr int OFF_B = OFF_X + XR * XBUF;
+  static constexpr int OFF_ST = OFF_B + 2 * BBUF;    // statistics, one float4 (rt, m, rzs, -) per expert
+  static constexpr int OROW = NE * 2 + 16;           // staging row of the results
+  static size_t bytes() {
+    const size_t main = (size_t)OFF_ST + (size_t)16 * NE;
+    const size_t stage = (size_t)MT * OROW;
+    return std::max(main, stage);
+  }
+};
+
+// the exact split of a float into bf16 parts (hi, the rounded remainder, ...)
+template <int NS>
+__device__ __forceinline__ void split_parts(float a, uint16_t (&pt)[NS]) {
+  pt[0] = f32_to_bf16(a);
+  if constexpr (NS > 1) {
+    const float r1 = a - bf16_to_f32(pt[0]);
+    pt[1] = f32_to_bf16(r1);
+    if constexpr (NS > 2) pt[2] = f32_to_bf16(r1 - bf16_to_f32(pt[1]));
+  }
+}
+
+// work unit of this workgroup: units of one image are consecutive, and
+// consecutive units go to one XCD (workgroup u runs on XCD u mod 8), so the
+// workgroups that share an image share that XCD's L2
+__device__ __forceinline__ int unit_of(const GmArgs& p) {
+  const int u = blockIdx.x;
+  return (u & 7) * p.per + (u >> 3);
+}
+
+template <int MB, int NB, int NS>
+__device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, int wv) {
+  using L = Layout<MB, NB, NS>;
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, n = lane & 15;
+  f32x4 acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // A fragment: row 16 mb + n, logical chunk 4 (ks & 1) + g, stored at chunk
+  // logical ^ ((row >> 1) & 7) = logical ^ (n >> 1)
+  const int arow = n * kXRow;
+  const int aswz = n >> 1;
+  // B fragment: expert row 16 (NB wv + nb) + n, chunk g ^ (n >> 2)
+  const int brow = (16 * NB * wv + n) * kBRow + (((g ^ (n >> 2)) & 3) << 4);
+  lds_barrier();  // prologue: chunk 0 and the step-0 coefficients are in LDS
+  for (int ks = 0; ks < p.nsteps; ++ks) {
+    const unsigned char* xb = smem + L::OFF_X + ((ks >> 1) % L::XR) * L::XBUF + arow +
+                              ((((ks & 1) * 4 + g) ^ aswz) << 4);
+    const unsigned char* bb = smem + L::OFF_B + (ks & 1) * L::BBUF + brow;
+    bf16x8 bf[NB][NS];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int pt = 0; pt < NS; ++pt)
+        bf[nb][pt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(bb + pt * L::PART + nb * 16 * kBRow));
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(xb + mb * 16 * kXRow));
+#pragma unroll
+      for (int pt = 0; pt < NS; ++pt)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bf[nb][pt], acc[mb][nb], 0, 0, 0);
+    }
+    lds_barrier();  // step ks done: its x chunk half and B buffer may be reused
+  }
+  // results: D[m][n] of block (mb, nb) sits on lane n + 16 (m / 4), element m % 4
+  unsigned char* stg = smem;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * mb + 4 * g + r;
+        const int col = 16 * (NB * wv + nb) + n;
+        *reinterpret_cast<uint16_t*>(stg + row * L::OROW + col * 2) = f32_to_bf16(acc[mb][nb][r]);
+      }
+}
+
+template <int MB, int NB, int NS>
+__device__ __forceinline__ void builder(const GmArgs& p, unsigned char* smem, int j, int b, int q) {
+  using L = Layout<MB, NB, NS>;
+  constexpr int NG = 4 * NB;  // groups of the range
+  const int lane = threadIdx.x & 63;
+  float4* st = reinterpret_cast<float4*>(smem + L::OFF_ST);
+  const int o0 = q * L::NE;
+  // this builder's groups' statistics into LDS and their B rows (both
+  // buffers, every part) zeroed; the bucket's offsets into registers
+#pragma unroll
+  for (int h = 0; h < kGroupsPerBuilder; ++h) {
+    const int gl = j + kBuilders * h;
+    if (gl >= NG) continue;
+    if (lane < kGroup) {
+      const int ow = kGroup * gl + lane;
+      const int64_t bo = (int64_t)b * p.R + min(o0 + ow, p.R - 1);
+      st[ow] = make_float4(p.st[bo], p.st[p.nst + bo], p.st[2 * p.nst + bo], 0.f);
+    }
+    for (int i = lane; i < 2 * NS * kGroup * (kBRow / 16); i += 64) {
+      const int part = i / (kGroup * (kBRow / 16));  // buffer * NS + part
+      const int r = i - part * (kGroup * (kBRow / 16));
+      *reinterpret_cast<u32x4*>(smem + L::OFF_B + part * L::PART + (kGroup * gl) * kBRow + r * 16) =
+          u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  const int bucket = q * kBuilders + j;
+  const int32_t* ob = p.off + (int64_t)bucket * (p.nsteps + 1);
+  const int ofr = ob[min(lane, p.nsteps)];
+  const int tot = __builtin_amdgcn_readfirstlane(ob[p.nsteps]);
+  const uint2* eb = p.ent + (int64_t)bucket * p.cap;
+  // offset t of the bucket (t uniform, 0 <= t <= nsteps <= 64)
+  auto ofs = [&](int t) __attribute__((always_inline)) {
+    return t < kMaxSteps ? __builtin_amdgcn_readlane(ofr, t) : tot;
+  };
+  // step t's entries, rounds 0 .. kRounds - 1 (t clamped into range; reads
+  // past the step's list are clamped to the bucket: valid, never used)
+  auto fetch = [&](int t, uint2 (&e)[kRounds]) __attribute__((always_inline)) {
+    const int tc = min(t, p.nsteps - 1);
+    const int beg = ofs(tc);
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) e[r] = eb[min(beg + 64 * r + lane, p.cap - 1)];
+    return ofs(tc + 1) - beg;
+  };
+  __builtin_amdgcn_s_waitcnt(vm_wait(0));
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // this wave's LDS writes done (lgkmcnt 0)
+
+  // a step's list into buffer `buf`: all coefficients first (a lane past the
+  // end holds a placeholder, clamped into range and never stored), then the
+  // stores; more than 64 kRounds entries (rare) are read one round at a time
+  auto put = [&](unsigned char* buf, int t, const uint2 (&e)[kRounds], int n, bool clear)
+      __attribute__((always_inline)) {
+    uint16_t pt[kRounds][NS];
+    if (clear) {
+#pragma unroll
+      for (int r = 0; r < kRounds; ++r)
+#pragma unroll
+        for (int v = 0; v < NS; ++v) pt[r][v] = 0;
+    } else {
+      float4 sv[kRounds];
+#pragma unroll
+      for (int r = 0; r < kRounds; ++r) sv[r] = st[min((int)((e[r].x >> kSlotShift) & 0xff), L::NE - 1)];
+#pragma unroll
+      for (int r = 0; r < kRounds; ++r) {
+        const float a = (e[r].x & kResidualFlag)
+                            ? p.inv_nU
+                            : coef_alpha(coef_e(coef_z(__uint_as_float(e[r].y), sv[r].x), sv[r].y), sv[r].z);
+        split_parts<NS>(a, pt[r]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r)
+      if (64 * r + lane < n)
+#pragma unroll
+        for (int v = 0; v < NS; ++v)
+          *reinterpret_cast<uint16_t*>(buf + v * L::PART + (e[r].x & kOffMask)) = pt[r][v];
+    for (int q0 = 64 * kRounds; q0 < n; q0 += 64) {
+      const uint2 x = eb[min(ofs(t) + q0 + lane, p.cap - 1)];
+      uint16_t px[NS];
+      if (clear) {
+#pragma unroll
+        for (int v = 0; v < NS; ++v) px[v] = 0;
+      } else {
+        const float4 s1 = st[min((int)((x.x >> kSlotShift) & 0xff), L::NE - 1)];
+        const float a = (x.x & kResidualFlag) ? p.inv_nU
+                                              : coef_alpha(coef_e(coef_z(__uint_as_float(x.y), s1.x), s1.y), s1.z);
+        split_parts<NS>(a, px);
+      }
+      if (q0 + lane < n)
+#pragma unroll
+        for (int v = 0; v < NS; ++v) *reinterpret_cast<uint16_t*>(buf + v * L::PART + (x.x & kOffMask)) = px[v];
+    }
+  };
+
+  // schedule ring: ring[t % kAhead] holds step t's list, cnt its length;
+  // prev[t & 1] keeps step t - 2's for the clearing
+  uint2 ring[kAhead][kRounds];
+  int cnt[kAhead];
+#pragma unroll
+  for (int a = 0; a < kAhead; ++a) cnt[a] = fetch(a, ring[a]);
+  uint2 prev[2][kRounds];
+  int pcnt[2] = {0, 0};
+  __builtin_amdgcn_s_waitcnt(vm_wait((kAhead - 1) * kRounds));
+  put(smem + L::OFF_B, 0, ring[0], cnt[0], false);
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) prev[0][r] = ring[0][r];
+  pcnt[0] = cnt[0];
+  cnt[0] = fetch(kAhead, ring[0]);
+  lds_barrier();  // prologue
+  // step ks: consumers multiply step ks; this builder writes step ks + 1
+  for (int ks0 = 0; ks0 < p.nsteps; ks0 += kAhead) {
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) {
+      const int ks = ks0 + u;
+      const int t = ks + 1;
+      // ks0 is a multiple of kAhead (even), so the ring slot and the parity
+      // of t are constants of the unrolled body.  The ring is refilled on
+      // every step, past the end too (clamped, valid reads): a refill under a
+      // condition would merge the in-flight load with the old register at
+      // the join, and the copy that merge needs would wait for the load
+      const int slot = (u + 1) % kAhead;
+      const int par = (u + 1) & 1;
+      __builtin_amdgcn_s_waitcnt(vm_wait((kAhead - 1) * kRounds));
+      if (t < p.nsteps) {
+        unsigned char* buf = smem + L::OFF_B + (t & 1) * L::BBUF;
+        if (t >= 2) put(buf, t - 2, prev[par], pcnt[par], true);
+        put(buf, t, ring[slot], cnt[slot], false);
+      }
+#pragma unroll
+      for (int r = 0; r < kRounds; ++r) prev[par][r] = ring[slot][r];
+      pcnt[par] = cnt[slot];
+      cnt[slot] = fetch(t + kAhead, ring[slot]);
+      if (ks < p.nsteps) lds_barrier();
+    }
+  }
+}
+
+// waits until at most n chunk copies of this loader wave are outstanding
+// (n < XR; one s_waitcnt with a constant operand per possible n)
+template <int ROUNDS, int... Cs>
+__device__ __forceinline__ void wait_chunks_of(int n, std::integer_sequence<int, Cs...>) {
+  ((n == Cs ? (__builtin_amdgcn_s_waitcnt(vm_wait(Cs * ROUNDS)), 0) : 0), ...);
+}
+template <int ROUNDS, int XR>
+__device__ __forceinline__ void wait_chunks(int n) {
+  static_assert((XR - 1) * ROUNDS <= 63, "outstanding copies fit the counter");
+  wait_chunks_of<ROUNDS>(n, std::make_integer_sequence<int, XR>{});
+}
+
+template <int MB, int NB, int NS>
+__device__ __forceinline__ void loader(const GmArgs& p, unsigned char* smem, int lw, int b, int p0) {
+  using L = Layout<MB, NB, NS>;
+  constexpr int XR = L::XR;
+  const int lane = threadIdx.x & 63;
+  const int nchunks = p.nsteps / 2;
+  // chunk n into ring slot n % XR.  Global round u = 2 r + lw of the chunk
+  // (rounds r of this loader wave) covers slots 64 u .. 64 u + 63: row
+  // (64 u + l) / 8, stored chunk l % 8 holding logical chunk
+  // (l % 8) ^ ((row >> 1) & 7); rows past the image repeat its last row
+  auto copy = [&](int n) __attribute__((always_inline)) {
+    GMIX_LDS unsigned char* dst = (GMIX_LDS unsigned char*)(smem + L::OFF_X + (n % XR) * L::XBUF);
+#pragma unroll
+    for (int r = 0; r < L::ROUNDS; ++r) {
+      const int u = 2 * r + lw;
+      const int row = 8 * u + (lane >> 3);
+      const int pos = min(p0 + row, p.HW - 1);
+      const int logical = (lane & 7) ^ ((row >> 1) & 7);
+      const uint16_t* src = p.x + ((int64_t)b * p.HW + pos) * p.C + n * kChunk + logical * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src, (GMIX_LDS void*)(dst + u * 1024), 16, 0, kCachePolicyNT);
+    }
+  };
+  // prologue: chunks 0 .. XR - 2 in flight, chunk 0 complete
+  const int first = min(XR - 1, nchunks);
+  for (int n = 0; n < first; ++n) copy(n);
+  wait_chunks<L::ROUNDS, XR>(first - 1);
+  lds_barrier();  // prologue
+  for (int ks = 0; ks < p.nsteps; ++ks) {
+    const int c = ks >> 1;
+    if ((ks & 1) == 0) {
+      // chunk c + XR - 1 into the slot chunk c - 1 left (free since the
+      // barrier that ended step ks - 1)
+      if (c + XR - 1 < nchunks) copy(c + XR - 1);
+    } else if (ks + 1 < p.nsteps) {
+      // chunk c + 1 complete before the barrier; the later ones may fly on
+      const int issued = min(c + XR - 1, nchunks - 1);
+      wait_chunks<L::ROUNDS, XR>(issued - (c + 1));
+    }
+    lds_barrier();
+  }
+}
+
+template <int MB, int NB, int NS>
+__global__ void __launch_bounds__(kThreads, 1)
+k_gmix(GmArgs p) {
+  using L = Layout<MB, NB, NS>;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int v = unit_of(p);
+  if (v >= p.units) return;  // uniform per workgroup: no barrier is skipped by part of it
+  const int per_img = p.nt * p.nq;
+  const int b = v / per_img;
+  const int r = v - b * per_img;
+  const int jt = r / p.nq, q = r - (r / p.nq) * p.nq;
+  const int p0 = jt * L::MT, o0 = q * L::NE;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (wv < kConsumers)
+    consumer<MB, NB, NS>(p, smem, wv);
+  else if (wv < kConsumers + kBuilders)
+    builder<MB, NB, NS>(p, smem, wv - kConsumers, b, q);
+  else
+    loader<MB, NB, NS>(p, smem, wv - kConsumers - kBuilders, b, p0);
+  lds_barrier();  // results staged
+  // whole 16-byte pieces of the staged rows to y[b][p0 + row][o0 ..]
+  constexpr int kPieces = L::NE / 8;
+  for (int i = threadIdx.x; i < L::MT * kPieces; i += kThreads) {
+    const int row = i / kPieces, c8 = i - row * kPieces;
+    const int pos = p0 + row, o = o0 + 8 * c8;
+    if (pos < p.HW && o < p.E) {
+      const u32x4 val = *reinterpret_cast<const u32x4*>(smem + row * L::OROW + c8 * 16);
+      __builtin_nontemporal_store(val, reinterpret_cast<u32x4*>(p.y + ((int64_t)b * p.HW + pos) * p.E + o));
+    }
+  }
+}
+
+using GmKernel = void (*)(GmArgs);
+
+template <int MB, int NB, int NS>
+size_t lds_of() { return Layout<MB, NB, NS>::bytes(); }
+
+struct Variant {
+  int MB, NB, NS;
+  GmKernel k;
+  size_t (*lds)();
+};
+
+constexpr int kParts = 2;
+
+const Variant kVariants[] = {
+    {4, 4, 2, k_gmix<4, 4, 2>, lds_of<4, 4, 2>},
+    {4, 2, 2, k_gmix<4, 2, 2>, lds_of<4, 2, 2>},
+    {4, 3, 2, k_gmix<4, 3, 2>, lds_of<4, 3, 2>},
+    {7, 2, 2, k_gmix<7, 2, 2>, lds_of<7, 2, 2>},
+    {7, 3, 2, k_gmix<7, 3, 2>, lds_of<7, 3, 2>},
+};
+
+int cu_count() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  return cus;
+}
+
+// The variant with the least modelled time: rounds of workgroups over the
+// CUs times the products one workgroup issues per step.
+const Variant* pick(const Shape& sh) {
+  const int64_t nblk = (sh.E + 15) / 16;
+  const int cus = cu_count();
+  const Variant* best = nullptr;
+  int64_t best_cost = 0;
+  for (const Variant& v : kVariants) {
+    if (v.NS != kParts) continue;
+    if (v.lds() > (size_t)kLdsBytes) continue;
+    const int64_t nt = (sh.HW + 16 * v.MB - 1) / (16 * v.MB);
+    const int64_t nq = (nblk + 4 * v.NB - 1) / (4 * v.NB);
+    const int64_t units = sh.B * nt * nq;
+    const int64_t rounds = (units + cus - 1) / cus;
+    const int64_t cost = rounds * v.MB * v.NB;
+    if (!best || cost < best_cost || (cost == best_cost && v.NB > best->NB)) {
+      best = &v;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+struct SchedShape {
+  int nq, nbuckets, nsteps, cap;
+  size_t off_bytes, total;
+};
+
+SchedShape sched_shape(const Shape& sh, const Variant& v) {
+  SchedShape s{};
+  const int nblk = (int)((sh.E + 15) / 16);
+  s.nq = (nblk + 4 * v.NB - 1) / (4 * v.NB);
+  s.nbuckets = s.nq * kBuilders;
+  s.nsteps = (int)(sh.C / kStep);
+  s.cap = kGroupsPerBuilder * kGroup * sh.k + (int)sh.C;
+  s.off_bytes = ((size_t)s.nbuckets * (s.nsteps + 1) * 4 + 255) / 256 * 256;
+  s.total = s.off_bytes + (size_t)s.nbuckets * s.cap * 8;
+  return s;
+}
+
+}  // namespace
+
+bool gmix_eligible(const Shape& sh) {
+  if (sh.layout != MOCE_NHWC || sh.elem != MOCE_BF16 || sh.R < 1) return false;
+  if (sh.C % kChunk != 0 || sh.C > kStep * kMaxSteps || sh.E % 8 != 0) return false;
+  if ((int64_t)sh.B * sh.HW > INT32_MAX / 2) return false;
+  return pick(sh) != nullptr;
+}
+
+size_t gmix_sched_bytes(const Shape& sh) {
+  const Variant* v = pick(sh);
+  return v ? sched_shape(sh, *v).total : 0;
+}
+
+hipError_t launch_gmix(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* stats,
+                       const int32_t* U, int nU, void* sched, void* y, hipStream_t st) {
+  const Variant* v = pick(sh);
+  if (!v) return hipErrorInvalidValue;
+  const SchedShape ss = sched_shape(sh, *v);
+  const int ngroups = (int)((sh.E + kGroup - 1) / kGroup);
+  int32_t* off = static_cast<int32_t*>(sched);
+  uint2* ent = reinterpret_cast<uint2*>(static_cast<char*>(sched) + ss.off_bytes);
+  hipLaunchKernelGGL(k_sched, dim3(ss.nbuckets), dim3(256), 0, st, s, w, nU > 0 ? U : s, nU, sh.R, sh.k, ss.nsteps,
+                     ss.cap, 4 * v->NB, ngroups, off, ent);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  GmArgs p{};
+  p.x = static_cast<const uint16_t*>(x);
+  p.y = static_cast<uint16_t*>(y);
+  p.off = off;
+  p.ent = ent;
+  p.st = stats;
+  p.nst = sh.B * sh.R;
+  p.C = (int)sh.C;
+  p.HW = (int)sh.HW;
+  p.E = sh.E;
+  p.R = sh.R;
+  p.nU = nU;
+  p.nsteps = ss.nsteps;
+  p.ngroups = ngroups;
+  p.cap = ss.cap;
+  p.nt = (int)((sh.HW + 16 * v->MB - 1) / (16 * v->MB));
+  p.nq = ss.nq;
+  p.units = (int)(sh.B * p.nt * p.nq);
+  p.per = (p.units + 7) / 8;
+  p.inv_nU = nU > 0 ? 1.f / (float)nU : 0.f;
+  const size_t lds = v->lds();
+  e = hipFuncSetAttribute((const void*)v->k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(v->k, dim3(8 * p.per), dim3(kThreads), lds, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace moce

@@ -132,4 +132,14 @@ bool mfmamix_gate_fusable(const Shape& sh, int gate_kind);
 hipError_t launch_mfmamix_gated(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* d,
                                 const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st);
 
+// Channels-last bfloat16 mixing on the matrix cores from a per-forward
+// channel schedule of the supports (gmix.hip): C a multiple of 64 up to 8192,
+// E a multiple of 8.  The schedule needs gmix_sched_bytes(sh) of device
+// workspace; the coefficients are rebuilt from the softmax statistics (a
+// block of 3 B R floats written by launch_gate).
+bool gmix_eligible(const Shape& sh);
+size_t gmix_sched_bytes(const Shape& sh);
+hipError_t launch_gmix(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* stats,
+                       const int32_t* U, int nU, void* sched, void* y, hipStream_t st);
+
 }  // namespace moce

@@ -500,7 +500,11 @@ def test_forward_path_choice():
     assert path(4, 240, 64, 32, 16, 16) == mb.PATH_TILE          # C not a multiple of 32
     assert path(4, 256, 65, 32, 16, 16) == mb.PATH_TILE          # E > 64
     assert path(2, 64, 16, 8, 8, 8, dtype="f32") == mb.PATH_GENERIC
-    assert path(64, 1024, 256, 64, 14, 14, layout="nhwc") == mb.PATH_GENERIC
+    assert path(64, 1024, 256, 64, 14, 14, layout="nhwc") == mb.PATH_SCHEDULED
+    assert path(128, 2048, 512, 128, 7, 7, layout="nhwc") == mb.PATH_SCHEDULED
+    assert path(4, 96, 24, 8, 7, 7, layout="nhwc") == mb.PATH_GENERIC      # C not a multiple of 64
+    assert path(4, 128, 20, 8, 7, 7, layout="nhwc") == mb.PATH_GENERIC     # E not a multiple of 8
+    assert path(4, 128, 24, 8, 7, 7, dtype="f32", layout="nhwc") == mb.PATH_GENERIC
     assert path(4, 512, 64, 32, 16, 16) == mb.PATH_GENERIC       # C > 256
     assert path(4, 96, 24, 12, 30, 30) == mb.PATH_GENERIC        # H*W not a multiple of 8
     assert path(4, 64, 1, 8, 8, 8) == mb.PATH_GENERIC            # no routed expert
@@ -564,3 +568,55 @@ def test_mfma_forward_equals_stages(B, C, E, k, H, W):
             assert torch.equal(y_gm.view(torch.int16), y_st.view(torch.int16))
     ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
     check_y(to_host_f64(y), ref["y"], ref["mag"], "bf16")
+
+
+# --------------------------------------------------------------------------- scheduled matrix-core mix (NHWC bf16)
+SCHEDULED = [
+    # B, C, E, k, H, W, extra: shapes served by the channels-last matrix-core mix
+    (3, 1024, 256, 64, 14, 14, {}),            # stage-3 layer, a few images
+    (2, 2048, 512, 128, 7, 7, {}),             # stage-4 layer
+    (3, 768, 192, 48, 197, 1, dict(signed=True)),  # ViT token layer
+    (2, 64, 8, 4, 5, 5, {}),                   # one 64-channel chunk; experts past E in the range
+    (2, 128, 40, 7, 3, 11, dict(signed=True)),  # residual row in a partial group; 33 positions
+    (1, 256, 24, 256, 2, 9, {}),               # k = C: 256 entries per group and step (overflow path)
+    (2, 192, 96, 17, 10, 10, {}),              # 6 steps: the prefetch ring's tail
+    (2, 256, 16, 8, 4, 4, dict(cyclic=True)),  # cyclic supports: U = channels 120..255
+    (2, 256, 64, 4, 4, 4, dict(cyclic=True)),  # cyclic supports covering C exactly: U empty
+    (4, 512, 40, 1, 6, 6, {}),                 # k = 1: exact copies
+    (1, 64, 64, 64, 113, 1, {}),               # E = C = k, positions over two 112-row tiles
+]
+
+
+@pytest.mark.parametrize("B,C,E,k,H,W,extra", SCHEDULED)
+def test_scheduled_forward_shapes(B, C, E, k, H, W, extra):
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nhwc", seed=B * 31 + C + E + k, **extra)
+    ref = oracle.forward(x, s, w, E, oracle.NHWC, a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nhwc", s, w, a=a, c=c)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_SCHEDULED
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    check_y(y, ref["y"], ref["mag"], "bf16")
+    if ref["nU"] == 0:
+        assert np.all(y[..., E - 1] == 0.0)
+    if k == 1:
+        assert np.array_equal(y[..., :E - 1], ref["y"][..., :E - 1])
+
+
+def test_scheduled_forward_mlp_gate_and_one_hot():
+    """The paper's gate on the scheduled path, and the one-hot limit as exact copies there."""
+    B, C, E, k, H, W = 2, 512, 64, 24, 6, 6
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nhwc", seed=17, signed=True)
+    rng = np.random.default_rng(18)
+    W1 = (rng.standard_normal((k, k)) * k ** -0.5).astype(np.float32)
+    b1 = (rng.standard_normal(k) * 0.1).astype(np.float32)
+    w2 = (rng.standard_normal(k) * k ** -0.5).astype(np.float32)
+    ref = oracle.forward(x, s, w, E, oracle.NHWC, gate="mlp", W1=W1, b1=b1, w2=w2, b2=0.0)
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nhwc", s, w, gate="mlp", W1=W1, b1=b1, w2=w2, b2=0.0)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_MLP_SIGMOID) == mb.PATH_SCHEDULED
+    check_y(to_host_f64(layer.forward(to_device_x(x, "bf16"))), ref["y"], ref["mag"], "bf16")
+    w[:, 0] = w.max(axis=1) + 1.0
+    a[:] = 0.0
+    c[:] = -1e4
+    ref = oracle.forward(x, s, w, E, oracle.NHWC, a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nhwc", s, w, a=a, c=c)
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    assert np.array_equal(y[..., :E - 1], ref["y"][..., :E - 1])
