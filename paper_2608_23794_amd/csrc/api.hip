@@ -259,13 +259,13 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
     return device_status(moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream));
   }
   if (moce::gmix_eligible(sh)) {
-    // channels-last on the matrix cores: pooling, the gate's softmax
-    // statistics, then the schedule and the mix
-    hipError_t e = moce::launch_pool(sh, x, d, stream);
+    // channels-last on the matrix cores: pooling with the support schedule
+    // beside it, the gate's softmax statistics, then the mix
+    hipError_t e = moce::launch_pool_sched(sh, x, d, s, w, U, nU, base + l.sched, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
     e = moce::launch_gate(sh, d, s, w, *gate, tau, nullptr, stats, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
-    return device_status(moce::launch_gmix(sh, x, s, w, stats, U, nU, base + l.sched, y, stream));
+    return device_status(moce::launch_gmix(sh, x, stats, nU, base + l.sched, y, stream));
   }
   hipError_t e = moce::launch_pool(sh, x, d, stream);
   if (e != hipSuccess) return MOCE_ERR_DEVICE;

@@ -1,6 +1,6 @@
 // Temperatures (Sec. 3.3) and mixing coefficients (Sec. 3.3 Eq. 4).
 //
-// One wavefront (or a 32- or 64-lane segment) per (image, routed expert).
+// One wavefront, or a 32- or 16-lane segment, per (image, routed expert).
 // Lanes span the k support positions: each gathers the descriptor of its
 // channel, the segment reduces the gate's pre-activation, and the same lanes
 // then form the softmax of the selected logits over the temperature with the
@@ -8,6 +8,8 @@
 // writes the coefficients alpha[b][o][i] and/or the softmax statistics
 // (rt = 1/tau, the largest scaled logit m, rzs = 1 / partition sum), from
 // which a mix kernel rebuilds exactly the same coefficients.
+#include <type_traits>
+
 #include "moce_internal.h"
 
 namespace moce {
@@ -58,69 +60,7 @@ k_gate_softplus(const float* __restrict__ d, const int32_t* __restrict__ s, cons
                    item);
 }
 
-// The same for 64 < k <= 64 PER: every input of a lane's PER positions is
-// read up front (indices, slopes and logits, then the descriptor gathers),
-// so the wave makes two dependent round trips instead of one per pass, and
-// the quotients are kept for the three reductions.  The operations and their
-// order per lane are those of k_gate_softplus.
-template <int PER>
-__global__ void __launch_bounds__(kGateWaves * kWave)
-k_gate_softplus_wide(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
-                     const float* __restrict__ a, const float* __restrict__ c, float* __restrict__ tau,
-                     float* __restrict__ alpha, Stats st, int64_t B, int64_t C, int R, int k) {
-  const int lane = threadIdx.x & 63;
-  const int64_t item = (int64_t)blockIdx.x * kGateWaves + (threadIdx.x >> 6);
-  if (item >= B * R) return;
-  const int64_t b = item / R;
-  const int o = (int)(item % R);
-  const int32_t* so = s + (int64_t)o * k;
-  const float* ao = a + (int64_t)o * k;
-  const float* wo = w + (int64_t)o * k;
-  const float* db = d + b * C;
-  int ch[PER];
-  float av[PER], wv[PER], dv[PER];
-#pragma unroll
-  for (int r = 0; r < PER; ++r) {
-    const int i = min(lane + kWave * r, k - 1);
-    ch[r] = so[i];
-    av[r] = ao[i];
-    wv[r] = wo[i];
-  }
-#pragma unroll
-  for (int r = 0; r < PER; ++r) dv[r] = db[ch[r]];
-  float g = 0.f;
-#pragma unroll
-  for (int r = 0; r < PER; ++r)
-    if (lane + kWave * r < k) g += av[r] * dv[r];
-  g = wave_sum(g) + c[o];
-  const float t = softplusf(g) + 1e-3f;
-  if (lane == 0) tau[item] = t;
-  const float rt = 1.f / t;
-  float z[PER];
-  float m = -INFINITY;
-#pragma unroll
-  for (int r = 0; r < PER; ++r) {
-    z[r] = coef_z(wv[r], rt);
-    if (lane + kWave * r < k) m = fmaxf(m, z[r]);
-  }
-  m = wave_max(m);
-  float zs = 0.f;
-#pragma unroll
-  for (int r = 0; r < PER; ++r) {
-    z[r] = coef_e(z[r], m);
-    if (lane + kWave * r < k) zs += z[r];
-  }
-  zs = wave_sum(zs);
-  const float rzs = 1.f / zs;
-  if (alpha) {
-#pragma unroll
-    for (int r = 0; r < PER; ++r)
-      if (lane + kWave * r < k) alpha[item * k + lane + kWave * r] = coef_alpha(z[r], rzs);
-  }
-  if (st.rt && lane == 0) put_stats(st, item, rt, m, rzs);
-}
-
-// The same for k <= W (W = 32 or 64): segments of W lanes, one per (image,
+// The same for k <= W (W = 32): segments of W lanes, one per (image,
 // expert), 64 / W per wave, lane i of a segment holding support position i.
 // Every input of a position is read up front (the selected logit too), so the
 // only dependent reads are the descriptor gathers; the exponentials are
@@ -157,6 +97,104 @@ k_gate_softplus_seg(const float* __restrict__ d, const int32_t* __restrict__ s, 
   if (i == 0) tau[item] = t;
   if (alpha && in) alpha[item * k + i] = coef_alpha(ex, rzs);
   if (st.rt && i == 0) put_stats(st, item, rt, m, rzs);
+}
+
+// The value of lane l ^ OFF within rows of 16 lanes, by DPP moves (quad
+// permutations, row shifts, a half-row rotation).
+template <int OFF>
+__device__ __forceinline__ float row16_xor(float v, int lane) {
+  auto mov = [](float u, auto ctrl) __attribute__((always_inline)) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(u), decltype(ctrl)::value, 0xf, 0xf, true));
+  };
+  if constexpr (OFF == 1) {
+    return mov(v, std::integral_constant<int, 0xb1>{});  // quad_perm [1, 0, 3, 2]
+  } else if constexpr (OFF == 2) {
+    return mov(v, std::integral_constant<int, 0x4e>{});  // quad_perm [2, 3, 0, 1]
+  } else if constexpr (OFF == 4) {
+    const float up = mov(v, std::integral_constant<int, 0x104>{});  // row_shl 4: lane l + 4
+    const float dn = mov(v, std::integral_constant<int, 0x114>{});  // row_shr 4: lane l - 4
+    return (lane & 4) ? dn : up;
+  } else {
+    return mov(v, std::integral_constant<int, 0x128>{});  // row_ror 8: lane l ^ 8 within the row
+  }
+}
+__device__ __forceinline__ float row16_sum(float v, int lane) {
+  v += row16_xor<8>(v, lane);
+  v += row16_xor<4>(v, lane);
+  v += row16_xor<2>(v, lane);
+  v += row16_xor<1>(v, lane);
+  return v;
+}
+__device__ __forceinline__ float row16_max(float v, int lane) {
+  v = fmaxf(v, row16_xor<8>(v, lane));
+  v = fmaxf(v, row16_xor<4>(v, lane));
+  v = fmaxf(v, row16_xor<2>(v, lane));
+  v = fmaxf(v, row16_xor<1>(v, lane));
+  return v;
+}
+
+// The softplus-linear gate for 32 < k <= 16 PER: a row of 16 lanes per
+// (image, expert), four per wave, lane h holding support positions
+// h, h + 16, ..., so that each read instruction covers 16 consecutive entries
+// of every pair.  Every input of a lane is read up front; the three
+// reductions are DPP moves within the row.
+template <int PER>
+__global__ void __launch_bounds__(kGateWaves * kWave)
+k_gate_softplus_x16(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
+                    const float* __restrict__ a, const float* __restrict__ c, float* __restrict__ tau,
+                    float* __restrict__ alpha, Stats st, int64_t B, int64_t C, int R, int k) {
+  const int lane = threadIdx.x & 63;
+  const int h = lane & 15;
+  const int64_t item = ((int64_t)blockIdx.x * kGateWaves + (threadIdx.x >> 6)) * 4 + (lane >> 4);
+  const bool live = item < B * R;
+  const int64_t it = live ? item : B * R - 1;
+  const int64_t b = it / R;
+  const int o = (int)(it % R);
+  const int64_t e0 = (int64_t)o * k;
+  int ch[PER];
+  float av[PER], wv[PER], dv[PER];
+#pragma unroll
+  for (int t = 0; t < PER; ++t) {
+    const int i = min(h + 16 * t, k - 1);
+    ch[t] = s[e0 + i];
+    av[t] = a[e0 + i];
+    wv[t] = w[e0 + i];
+  }
+  const float co = c[o];
+  const float* db = d + b * C;
+#pragma unroll
+  for (int t = 0; t < PER; ++t) dv[t] = db[ch[t]];
+  float g = 0.f;
+#pragma unroll
+  for (int t = 0; t < PER; ++t)
+    if (h + 16 * t < k) g += av[t] * dv[t];
+  g = row16_sum(g, lane) + co;
+  const float tv = softplusf(g) + 1e-3f;
+  const float rt = 1.f / tv;
+  float z[PER];
+  float m = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < PER; ++t) {
+    z[t] = coef_z(wv[t], rt);
+    if (h + 16 * t < k) m = fmaxf(m, z[t]);
+  }
+  m = row16_max(m, lane);
+  float zs = 0.f;
+#pragma unroll
+  for (int t = 0; t < PER; ++t) {
+    z[t] = coef_e(z[t], m);
+    if (h + 16 * t < k) zs += z[t];
+  }
+  zs = row16_sum(zs, lane);
+  const float rzs = 1.f / zs;
+  if (!live) return;
+  if (h == 0) tau[item] = tv;
+  if (alpha) {
+#pragma unroll
+    for (int t = 0; t < PER; ++t)
+      if (h + 16 * t < k) alpha[item * k + h + 16 * t] = coef_alpha(z[t], rzs);
+  }
+  if (st.rt && h == 0) put_stats(st, item, rt, m, rzs);
 }
 
 // The paper's shared gate: h = ReLU(W1 z + b1), g = w2 . h + b2,
@@ -204,15 +242,13 @@ hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const 
     const unsigned b32 = (unsigned)((items + 2 * kGateWaves - 1) / (2 * kGateWaves));
     hipLaunchKernelGGL(k_gate_softplus_seg<32>, dim3(b32), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
                        tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);
-  } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 64) {
-    hipLaunchKernelGGL(k_gate_softplus_seg<64>, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
-                       tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);
-  } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 128) {
-    hipLaunchKernelGGL(k_gate_softplus_wide<2>, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
-                       tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);
   } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 256) {
-    hipLaunchKernelGGL(k_gate_softplus_wide<4>, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
-                       tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);
+    // rows of 16 lanes, four (image, expert) pairs per wave
+    const unsigned b16 = (unsigned)((items + 4 * kGateWaves - 1) / (4 * kGateWaves));
+    const int per = (sh.k + 15) / 16;
+    auto kern = per <= 4 ? k_gate_softplus_x16<4> : per <= 8 ? k_gate_softplus_x16<8> : k_gate_softplus_x16<16>;
+    hipLaunchKernelGGL(kern, dim3(b16), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c, tau, alpha, sp, sh.B,
+                       sh.C, sh.R, sh.k);
   } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR) {
     hipLaunchKernelGGL(k_gate_softplus, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
                        tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);

@@ -47,6 +47,7 @@
 #include <utility>
 
 #include "moce_internal.h"
+#include "pool_rows.h"
 
 namespace moce {
 namespace {
@@ -114,23 +115,29 @@ struct GmArgs {
 // range q (the ng groups of one mix workgroup), the residual row E-1 included
 // where it falls there, counted and placed by step.  Order within a step is
 // free: every entry writes its own slot of A_b.
-__global__ void __launch_bounds__(256)
-k_sched(const int32_t* __restrict__ s, const float* __restrict__ w, const int32_t* __restrict__ U, int nU, int R,
-        int k, int nsteps, int cap, int ng, int ngroups, int32_t* __restrict__ off, uint2* __restrict__ ent) {
-  __shared__ int cnt[kMaxSteps];
-  __shared__ int cur[kMaxSteps];
-  const int q = blockIdx.x / kBuilders, j = blockIdx.x % kBuilders, tid = threadIdx.x;
+struct SchedArgs {
+  const int32_t* s;
+  const float* w;
+  const int32_t* U;
+  int nU, R, k, nsteps, cap, ng, ngroups, nbuckets;
+  int32_t* off;
+  uint2* ent;
+};
+
+// bucket `bk` by the whole workgroup (cnt, cur: LDS of kMaxSteps ints each)
+__device__ __forceinline__ void sched_bucket(const SchedArgs& a, int bk, int* cnt, int* cur) {
+  const int q = bk / kBuilders, j = bk % kBuilders, tid = threadIdx.x, nth = blockDim.x;
   // the bucket's groups and their entry counts
   int gid[kGroupsPerBuilder], nr[kGroupsPerBuilder], first[kGroupsPerBuilder + 1];
   first[0] = 0;
 #pragma unroll
   for (int h = 0; h < kGroupsPerBuilder; ++h) {
     const int gl = j + kBuilders * h;
-    gid[h] = q * ng + gl;
-    const bool live = gl < ng && gid[h] < ngroups;
+    gid[h] = q * a.ng + gl;
+    const bool live = gl < a.ng && gid[h] < a.ngroups;
     const int o_first = gid[h] * kGroup;
-    nr[h] = live ? max(0, min(kGroup, R - o_first)) * k : 0;
-    const int nres = live && R >= o_first && R < o_first + kGroup ? nU : 0;
+    nr[h] = live ? max(0, min(kGroup, a.R - o_first)) * a.k : 0;
+    const int nres = live && a.R >= o_first && a.R < o_first + kGroup ? a.nU : 0;
     first[h + 1] = first[h] + nr[h] + nres;
   }
   const int total = first[kGroupsPerBuilder];
@@ -143,18 +150,18 @@ k_sched(const int32_t* __restrict__ s, const float* __restrict__ w, const int32_
     const int o_first = gid[h] * kGroup;
     res = r >= nr[h];
     if (!res) {
-      o = o_first + r / k;
-      c = s[(int64_t)o_first * k + r];
-      wv = w[(int64_t)o_first * k + r];
+      o = o_first + r / a.k;
+      c = a.s[(int64_t)o_first * a.k + r];
+      wv = a.w[(int64_t)o_first * a.k + r];
     } else {
-      o = R;
-      c = U[r - nr[h]];
+      o = a.R;
+      c = a.U[r - nr[h]];
       wv = 0.f;
     }
   };
-  for (int t = tid; t < nsteps; t += 256) cnt[t] = 0;
+  for (int t = tid; t < a.nsteps; t += nth) cnt[t] = 0;
   __syncthreads();
-  for (int e = tid; e < total; e += 256) {
+  for (int e = tid; e < total; e += nth) {
     int o, c;
     float wv;
     bool res;
@@ -163,25 +170,25 @@ k_sched(const int32_t* __restrict__ s, const float* __restrict__ w, const int32_
   }
   __syncthreads();
   // exclusive scan of the counts (nsteps <= 64: one wave)
-  int32_t* ob = off + (int64_t)blockIdx.x * (nsteps + 1);
+  int32_t* ob = a.off + (int64_t)bk * (a.nsteps + 1);
   if (tid < 64) {
-    const int v = tid < nsteps ? cnt[tid] : 0;
+    const int v = tid < a.nsteps ? cnt[tid] : 0;
     int incl = v;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       const int t = __shfl_up(incl, d, 64);
       if (tid >= d) incl += t;
     }
-    if (tid < nsteps) {
+    if (tid < a.nsteps) {
       cur[tid] = incl - v;
       ob[tid] = incl - v;
     }
-    if (tid == 63) ob[nsteps] = incl;
+    if (tid == 63) ob[a.nsteps] = incl;
   }
   __syncthreads();
-  const int ne = ng * kGroup;
-  uint2* eb = ent + (int64_t)blockIdx.x * cap;
-  for (int e = tid; e < total; e += 256) {
+  const int ne = a.ng * kGroup;
+  uint2* eb = a.ent + (int64_t)bk * a.cap;
+  for (int e = tid; e < total; e += nth) {
     int o, c;
     float wv;
     bool res;
@@ -191,6 +198,22 @@ k_sched(const int32_t* __restrict__ s, const float* __restrict__ w, const int32_
     const uint32_t packed = (uint32_t)b_off(ow, c & 31) | ((uint32_t)ow << kSlotShift) | (res ? kResidualFlag : 0u);
     eb[pos] = make_uint2(packed, __float_as_uint(wv));
   }
+}
+
+// Pooling and the schedule in one launch: workgroups below nbuckets build a
+// schedule bucket each, the rest pool one (image, channel block) each, so the
+// schedule's latency chains run beside memory-bound work.
+template <typename T>
+__global__ void __launch_bounds__(kPoolThreads)
+k_pool_sched(const T* __restrict__ x, float* __restrict__ d, int C, int HW, int nblk, SchedArgs a) {
+  __shared__ float part[kPoolGroups * 32 * PoolVec<T>::EPV];
+  if ((int)blockIdx.x < a.nbuckets) {
+    int* cnt = reinterpret_cast<int*>(part);
+    sched_bucket(a, blockIdx.x, cnt, cnt + kMaxSteps);
+    return;
+  }
+  const int i = blockIdx.x - a.nbuckets;
+  pool_rows_block<T>(x, d, C, HW, i / nblk, i % nblk, part);
 }
 
 // ---------------------------------------------------------------- the mix
@@ -597,24 +620,42 @@ size_t gmix_sched_bytes(const Shape& sh) {
   return v ? sched_shape(sh, *v).total : 0;
 }
 
-hipError_t launch_gmix(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* stats,
-                       const int32_t* U, int nU, void* sched, void* y, hipStream_t st) {
+hipError_t launch_pool_sched(const Shape& sh, const void* x, float* d, const int32_t* s, const float* w,
+                             const int32_t* U, int nU, void* sched, hipStream_t st) {
   const Variant* v = pick(sh);
   if (!v) return hipErrorInvalidValue;
   const SchedShape ss = sched_shape(sh, *v);
-  const int ngroups = (int)((sh.E + kGroup - 1) / kGroup);
-  int32_t* off = static_cast<int32_t*>(sched);
-  uint2* ent = reinterpret_cast<uint2*>(static_cast<char*>(sched) + ss.off_bytes);
-  hipLaunchKernelGGL(k_sched, dim3(ss.nbuckets), dim3(256), 0, st, s, w, nU > 0 ? U : s, nU, sh.R, sh.k, ss.nsteps,
-                     ss.cap, 4 * v->NB, ngroups, off, ent);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  SchedArgs a{};
+  a.s = s;
+  a.w = w;
+  a.U = nU > 0 ? U : s;
+  a.nU = nU;
+  a.R = sh.R;
+  a.k = sh.k;
+  a.nsteps = ss.nsteps;
+  a.cap = ss.cap;
+  a.ng = 4 * v->NB;
+  a.ngroups = (int)((sh.E + kGroup - 1) / kGroup);
+  a.nbuckets = ss.nbuckets;
+  a.off = static_cast<int32_t*>(sched);
+  a.ent = reinterpret_cast<uint2*>(static_cast<char*>(sched) + ss.off_bytes);
+  const int nblk = (int)((sh.C / PoolVec<uint16_t>::EPV + 31) / 32);
+  const unsigned grid = (unsigned)(ss.nbuckets + sh.B * nblk);
+  hipLaunchKernelGGL((k_pool_sched<uint16_t>), dim3(grid), dim3(kPoolThreads), 0, st,
+                     static_cast<const uint16_t*>(x), d, (int)sh.C, (int)sh.HW, nblk, a);
+  return hipGetLastError();
+}
 
+hipError_t launch_gmix(const Shape& sh, const void* x, const float* stats, int nU, const void* sched, void* y,
+                       hipStream_t st) {
+  const Variant* v = pick(sh);
+  if (!v) return hipErrorInvalidValue;
+  const SchedShape ss = sched_shape(sh, *v);
   GmArgs p{};
   p.x = static_cast<const uint16_t*>(x);
   p.y = static_cast<uint16_t*>(y);
-  p.off = off;
-  p.ent = ent;
+  p.off = static_cast<const int32_t*>(sched);
+  p.ent = reinterpret_cast<const uint2*>(static_cast<const char*>(sched) + ss.off_bytes);
   p.st = stats;
   p.nst = sh.B * sh.R;
   p.C = (int)sh.C;
@@ -623,7 +664,7 @@ hipError_t launch_gmix(const Shape& sh, const void* x, const int32_t* s, const f
   p.R = sh.R;
   p.nU = nU;
   p.nsteps = ss.nsteps;
-  p.ngroups = ngroups;
+  p.ngroups = (int)((sh.E + kGroup - 1) / kGroup);
   p.cap = ss.cap;
   p.nt = (int)((sh.HW + 16 * v->MB - 1) / (16 * v->MB));
   p.nq = ss.nq;
@@ -631,7 +672,7 @@ hipError_t launch_gmix(const Shape& sh, const void* x, const int32_t* s, const f
   p.per = (p.units + 7) / 8;
   p.inv_nU = nU > 0 ? 1.f / (float)nU : 0.f;
   const size_t lds = v->lds();
-  e = hipFuncSetAttribute((const void*)v->k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipError_t e = hipFuncSetAttribute((const void*)v->k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(v->k, dim3(8 * p.per), dim3(kThreads), lds, st, p);
   return hipGetLastError();

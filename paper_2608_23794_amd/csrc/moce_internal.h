@@ -133,13 +133,16 @@ hipError_t launch_mfmamix_gated(const Shape& sh, const void* x, const int32_t* s
                                 const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st);
 
 // Channels-last bfloat16 mixing on the matrix cores from a per-forward
-// channel schedule of the supports (gmix.hip): C a multiple of 64 up to 8192,
-// E a multiple of 8.  The schedule needs gmix_sched_bytes(sh) of device
-// workspace; the coefficients are rebuilt from the softmax statistics (a
-// block of 3 B R floats written by launch_gate).
+// channel schedule of the supports (gmix.hip): C a multiple of 64 up to 2048,
+// E a multiple of 8.  launch_pool_sched pools x into d and builds the
+// schedule (gmix_sched_bytes(sh) of device workspace) in one launch;
+// launch_gmix then mixes, rebuilding the coefficients from the softmax
+// statistics (a block of 3 B R floats written by launch_gate).
 bool gmix_eligible(const Shape& sh);
 size_t gmix_sched_bytes(const Shape& sh);
-hipError_t launch_gmix(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* stats,
-                       const int32_t* U, int nU, void* sched, void* y, hipStream_t st);
+hipError_t launch_pool_sched(const Shape& sh, const void* x, float* d, const int32_t* s, const float* w,
+                             const int32_t* U, int nU, void* sched, hipStream_t st);
+hipError_t launch_gmix(const Shape& sh, const void* x, const float* stats, int nU, const void* sched, void* y,
+                       hipStream_t st);
 
 }  // namespace moce

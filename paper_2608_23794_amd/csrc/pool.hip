@@ -8,6 +8,7 @@
 // lanes read consecutive bytes), the four waves of a block split the rows,
 // and the four partial sums meet in LDS.
 #include "moce_internal.h"
+#include "pool_rows.h"
 
 namespace moce {
 namespace {
@@ -149,10 +150,26 @@ hipError_t pool_nchw(const Shape& sh, const T* x, float* d, hipStream_t st) {
   return hipGetLastError();
 }
 
+// 1024 threads per (image, block of 32 16-byte channel vectors)
+template <typename T>
+__global__ void __launch_bounds__(kPoolThreads)
+k_pool_nhwc_rows(const T* __restrict__ x, float* __restrict__ d, int C, int HW, int nblk) {
+  __shared__ float part[kPoolGroups * 32 * PoolVec<T>::EPV];
+  pool_rows_block<T>(x, d, C, HW, blockIdx.x / nblk, blockIdx.x % nblk, part);
+}
+
 template <typename T>
 hipError_t pool_nhwc(const Shape& sh, const T* x, float* d, hipStream_t st) {
   constexpr int EPV16 = 16 / sizeof(T);
   const int C = (int)sh.C, HW = (int)sh.HW;
+  if ((sh.C * sizeof(T)) % 16 == 0) {
+    // every 16-byte vector of a row block read by its own lane, 32 row groups
+    // with four loads in flight each
+    const int nblk = (C / EPV16 + 31) / 32;
+    hipLaunchKernelGGL((k_pool_nhwc_rows<T>), dim3((unsigned)(sh.B * nblk)), dim3(kPoolThreads), 0, st, x, d, C,
+                       HW, nblk);
+    return hipGetLastError();
+  }
   if ((sh.C * sizeof(T)) % 16 == 0) {
     const int nblk = (C / EPV16 + 63) / 64;
     hipLaunchKernelGGL((k_pool_nhwc<T, EPV16>), dim3((unsigned)(sh.B * nblk)), dim3(256), 0, st, x, d,

@@ -1,0 +1,73 @@
+// Channels-last pooling of one (image, channel block) by a 1024-thread
+// workgroup (Sec. 3.3: the descriptor is the spatial mean of each channel).
+// Lane l of the 32-lane row groups reads the 16-byte channel vector l of the
+// block; row group r takes positions r, r + 32, ..., four of them per round
+// with all four loads in flight.  The 32 partial sums of each channel are then
+// added in a fixed order through LDS, so the result does not depend on
+// timing.
+#pragma once
+
+#include "moce_internal.h"
+
+namespace moce {
+
+constexpr int kPoolThreads = 1024;
+constexpr int kPoolGroups = kPoolThreads / 32;  // row groups
+
+template <typename T> struct PoolVec;
+template <> struct PoolVec<uint16_t> {
+  static constexpr int EPV = 8;
+  __device__ static void add(const uint4& v, float (&a)[8]) {
+    a[0] += bf16_lo(v.x); a[1] += bf16_hi(v.x); a[2] += bf16_lo(v.y); a[3] += bf16_hi(v.y);
+    a[4] += bf16_lo(v.z); a[5] += bf16_hi(v.z); a[6] += bf16_lo(v.w); a[7] += bf16_hi(v.w);
+  }
+};
+template <> struct PoolVec<float> {
+  static constexpr int EPV = 4;
+  __device__ static void add(const uint4& v, float (&a)[4]) {
+    a[0] += __uint_as_float(v.x); a[1] += __uint_as_float(v.y);
+    a[2] += __uint_as_float(v.z); a[3] += __uint_as_float(v.w);
+  }
+};
+
+// Channels of block cb: 32 EPV of them from channel 32 EPV cb (C a multiple of
+// EPV; vectors past C are skipped).  `part` is LDS of
+// kPoolGroups * 32 * EPV floats.
+template <typename T>
+__device__ __forceinline__ void pool_rows_block(const T* __restrict__ x, float* __restrict__ d, int C, int HW,
+                                                int64_t b, int cb, float* part) {
+  constexpr int EPV = PoolVec<T>::EPV;
+  const int l = threadIdx.x & 31, rg = threadIdx.x >> 5;
+  const int c0 = (cb * 32 + l) * EPV;
+  float acc[EPV];
+#pragma unroll
+  for (int j = 0; j < EPV; ++j) acc[j] = 0.f;
+  if (c0 < C) {
+    const T* col = x + b * HW * (int64_t)C + c0;
+    for (int p0 = rg; p0 < HW; p0 += 4 * kPoolGroups) {
+      uint4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int p = min(p0 + u * kPoolGroups, HW - 1);
+        v[u] = *reinterpret_cast<const uint4*>(col + (int64_t)p * C);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (p0 + u * kPoolGroups < HW) PoolVec<T>::add(v[u], acc);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < EPV; ++j) part[(rg * 32 + l) * EPV + j] = acc[j];
+  __syncthreads();
+  // channel i of the block: the 32 row groups' sums in order
+  for (int i = threadIdx.x; i < 32 * EPV; i += kPoolThreads) {
+    const int c = cb * 32 * EPV + i;
+    if (c < C) {
+      float s = 0.f;
+      for (int r = 0; r < kPoolGroups; ++r) s += part[r * 32 * EPV + i];
+      d[b * C + c] = s / (float)HW;
+    }
+  }
+}
+
+}  // namespace moce
