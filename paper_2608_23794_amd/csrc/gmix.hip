@@ -57,9 +57,8 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 #define GMIX_LDS __attribute__((address_space(3)))
 
-constexpr int kStep = 32;                 // channels per step (the MFMA's K)
-constexpr int kChunk = 64;                // channels per x copy (two steps)
-constexpr int kXRow = kChunk * 2;         // bytes of one position row of an x chunk
+constexpr int kStep = 64;                 // channels per step: two K slices of the MFMA, one x chunk
+constexpr int kXRow = kStep * 2;          // bytes of one position row of an x chunk
 constexpr int kBRow = kStep * 2;          // bytes of one expert row of a B buffer part
 constexpr int kMaxXRing = 8;              // x chunk buffers at most (the ring fills the LDS left over)
 constexpr int kConsumers = 4;
@@ -69,25 +68,30 @@ constexpr int kWaves = kConsumers + kBuilders + kLoaders;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kGroup = 16;                // experts per group (one MFMA N block)
 constexpr int kGroupsPerBuilder = 2;      // 4 NB <= 16 groups per workgroup over 8 builders
-constexpr int kMaxSteps = 64;             // C <= 2048: offsets 0 .. 63 in one register, the total beside
-constexpr int kRounds = 3;                // 64-entry rounds of a builder's step held in registers
-constexpr int kAhead = 6;                 // steps of schedule a builder holds in registers (even)
+constexpr int kMaxSteps = 64;             // C <= 4096: offsets 0 .. 63 in one register, the total beside
+// 64-entry rounds of a builder's step held in registers: two for one group
+// of 16 experts (about 16 k 64 / C entries a step), three for two; longer
+// lists take a slow path
+constexpr int rounds_of(int NB) { return NB <= 2 ? 2 : 3; }
+constexpr int kAhead = 4;                 // steps of schedule a builder holds in registers (even)
 constexpr int kCachePolicyNT = 2;         // non-temporal bit of the global-to-LDS load
-constexpr int kLdsBytes = 160 * 1024;
+constexpr int kLdsBytes = 160 * 1024;  // per CU
 
 // Schedule entry: x = byte offset of the coefficient's slot in one part of a
-// B buffer (14 bits) | the expert's slot within the workgroup's expert range
-// << 14 (8 bits) | residual flag << 22; y = the selected logit's bits.
-constexpr uint32_t kOffMask = 0x3fff;
-constexpr int kSlotShift = 14;
-constexpr uint32_t kResidualFlag = 1u << 22;
+// B buffer (15 bits) | the expert's slot within the workgroup's expert range
+// << 15 (8 bits) | residual flag << 23; y = the selected logit's bits.
+constexpr uint32_t kOffMask = 0x7fff;
+constexpr int kSlotShift = 15;
+constexpr uint32_t kResidualFlag = 1u << 23;
 
 // byte offset of B[o][c] (o: expert within the workgroup, c: channel within
-// the step) in one part of a B buffer: 16-byte chunk c/8 of row o, rotated by
-// (o / 4) mod 4 so that 16 consecutive rows read at one chunk hit 16
-// different bank groups
+// the step) in one part of a B buffer: 16-byte chunk c/8 of the 128-byte row
+// o, stored at chunk (c/8) ^ ((o / 2) mod 8), so that 16 consecutive rows
+// read at one chunk hit 16 different bank groups (the x tile's rows are
+// swizzled the same way)
+__host__ __device__ inline int swz(int row) { return (row >> 1) & 7; }
 __host__ __device__ inline int b_off(int o, int c) {
-  return o * kBRow + ((((c >> 3) ^ (o >> 2)) & 3) << 4) + ((c & 7) << 1);
+  return o * kBRow + (((c >> 3) ^ swz(o)) << 4) + ((c & 7) << 1);
 }
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -166,7 +170,7 @@ __device__ __forceinline__ void sched_bucket(const SchedArgs& a, int bk, int* cn
     float wv;
     bool res;
     entry(e, o, c, wv, res);
-    atomicAdd(&cnt[c >> 5], 1);
+    atomicAdd(&cnt[c >> 6], 1);
   }
   __syncthreads();
   // exclusive scan of the counts (nsteps <= 64: one wave)
@@ -193,9 +197,9 @@ __device__ __forceinline__ void sched_bucket(const SchedArgs& a, int bk, int* cn
     float wv;
     bool res;
     entry(e, o, c, wv, res);
-    const int pos = atomicAdd(&cur[c >> 5], 1);
+    const int pos = atomicAdd(&cur[c >> 6], 1);
     const int ow = o - q * ne;  // the expert's slot within the range
-    const uint32_t packed = (uint32_t)b_off(ow, c & 31) | ((uint32_t)ow << kSlotShift) | (res ? kResidualFlag : 0u);
+    const uint32_t packed = (uint32_t)b_off(ow, c & 63) | ((uint32_t)ow << kSlotShift) | (res ? kResidualFlag : 0u);
     eb[pos] = make_uint2(packed, __float_as_uint(wv));
   }
 }
@@ -217,7 +221,7 @@ k_pool_sched(const T* __restrict__ x, float* __restrict__ d, int C, int HW, int 
 }
 
 // ---------------------------------------------------------------- the mix
-template <int MB, int NB, int NS>
+template <int MB, int NB, int NS, int OCC>
 struct Layout {
   static constexpr int MT = 16 * MB;                 // positions per tile
   static constexpr int NE = 64 * NB;                 // experts per workgroup
@@ -225,9 +229,10 @@ struct Layout {
   static constexpr int PART = NE * kBRow;            // one part of one B buffer
   static constexpr int BBUF = NS * PART;             // one B buffer
   // as many x chunks in flight as the LDS left by the B buffers and the
-  // statistics allows: at most kMaxXRing, and so that one loader wave's
-  // outstanding copies stay within its 6-bit counter
-  static constexpr int XR_FIT = (kLdsBytes - 1024 - 2 * BBUF - 16 * NE) / XBUF;
+  // statistics allows (OCC workgroups per CU share its LDS): at most
+  // kMaxXRing, and so that one loader wave's outstanding copies stay within
+  // its 6-bit counter
+  static constexpr int XR_FIT = (kLdsBytes / OCC - 1024 - 2 * BBUF - 16 * NE) / XBUF;
   static constexpr int ROUNDS = MB;                  // 16-byte copies per loader lane per chunk (MT / 16)
   static constexpr int XR_CNT = 63 / ROUNDS + 1;
   static constexpr int XR = XR_FIT < kMaxXRing ? (XR_FIT < XR_CNT ? XR_FIT : XR_CNT)
@@ -263,9 +268,9 @@ __device__ __forceinline__ int unit_of(const GmArgs& p) {
   return (u & 7) * p.per + (u >> 3);
 }
 
-template <int MB, int NB, int NS>
+template <int MB, int NB, int NS, int OCC>
 __device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, int wv) {
-  using L = Layout<MB, NB, NS>;
+  using L = Layout<MB, NB, NS, OCC>;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, n = lane & 15;
   f32x4 acc[MB][NB];
@@ -273,33 +278,37 @@ __device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, i
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // A fragment: row 16 mb + n, logical chunk 4 (ks & 1) + g, stored at chunk
-  // logical ^ ((row >> 1) & 7) = logical ^ (n >> 1)
+  // fragments of K slice h of a step: A row 16 mb + n and B row
+  // 16 (NB wv + nb) + n, logical chunk 4 h + g of the row, stored at
+  // chunk (4 h + g) ^ swz(row) = (4 h + g) ^ (n >> 1)
   const int arow = n * kXRow;
-  const int aswz = n >> 1;
-  // B fragment: expert row 16 (NB wv + nb) + n, chunk g ^ (n >> 2)
-  const int brow = (16 * NB * wv + n) * kBRow + (((g ^ (n >> 2)) & 3) << 4);
+  const int brow = (16 * NB * wv + n) * kBRow;
+  const int ch0 = (g ^ (n >> 1)) << 4, ch1 = ((4 + g) ^ (n >> 1)) << 4;
   lds_barrier();  // prologue: chunk 0 and the step-0 coefficients are in LDS
   for (int ks = 0; ks < p.nsteps; ++ks) {
-    const unsigned char* xb = smem + L::OFF_X + ((ks >> 1) % L::XR) * L::XBUF + arow +
-                              ((((ks & 1) * 4 + g) ^ aswz) << 4);
+    const unsigned char* xb = smem + L::OFF_X + (ks % L::XR) * L::XBUF + arow;
     const unsigned char* bb = smem + L::OFF_B + (ks & 1) * L::BBUF + brow;
-    bf16x8 bf[NB][NS];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int h = 0; h < 2; ++h) {
+      const int ch = h ? ch1 : ch0;
+      bf16x8 bf[NB][NS];
 #pragma unroll
-      for (int pt = 0; pt < NS; ++pt)
-        bf[nb][pt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(bb + pt * L::PART + nb * 16 * kBRow));
+      for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(xb + mb * 16 * kXRow));
+        for (int pt = 0; pt < NS; ++pt)
+          bf[nb][pt] =
+              __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(bb + pt * L::PART + nb * 16 * kBRow + ch));
 #pragma unroll
-      for (int pt = 0; pt < NS; ++pt)
+      for (int mb = 0; mb < MB; ++mb) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(xb + mb * 16 * kXRow + ch));
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bf[nb][pt], acc[mb][nb], 0, 0, 0);
+        for (int pt = 0; pt < NS; ++pt)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bf[nb][pt], acc[mb][nb], 0, 0, 0);
+      }
     }
-    lds_barrier();  // step ks done: its x chunk half and B buffer may be reused
+    lds_barrier();  // step ks done: its x chunk and B buffer may be reused
   }
   // results: D[m][n] of block (mb, nb) sits on lane n + 16 (m / 4), element m % 4
   unsigned char* stg = smem;
@@ -315,10 +324,11 @@ __device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, i
       }
 }
 
-template <int MB, int NB, int NS>
+template <int MB, int NB, int NS, int OCC>
 __device__ __forceinline__ void builder(const GmArgs& p, unsigned char* smem, int j, int b, int q) {
-  using L = Layout<MB, NB, NS>;
+  using L = Layout<MB, NB, NS, OCC>;
   constexpr int NG = 4 * NB;  // groups of the range
+  constexpr int kRounds = rounds_of(NB);
   const int lane = threadIdx.x & 63;
   float4* st = reinterpret_cast<float4*>(smem + L::OFF_ST);
   const int o0 = q * L::NE;
@@ -463,16 +473,16 @@ __device__ __forceinline__ void wait_chunks(int n) {
   wait_chunks_of<ROUNDS>(n, std::make_integer_sequence<int, XR>{});
 }
 
-template <int MB, int NB, int NS>
+template <int MB, int NB, int NS, int OCC>
 __device__ __forceinline__ void loader(const GmArgs& p, unsigned char* smem, int lw, int b, int p0) {
-  using L = Layout<MB, NB, NS>;
+  using L = Layout<MB, NB, NS, OCC>;
   constexpr int XR = L::XR;
   const int lane = threadIdx.x & 63;
-  const int nchunks = p.nsteps / 2;
-  // chunk n into ring slot n % XR.  Global round u = 2 r + lw of the chunk
-  // (rounds r of this loader wave) covers slots 64 u .. 64 u + 63: row
-  // (64 u + l) / 8, stored chunk l % 8 holding logical chunk
-  // (l % 8) ^ ((row >> 1) & 7); rows past the image repeat its last row
+  const int nchunks = p.nsteps;
+  // chunk n (the x tile's channels of step n) into ring slot n % XR.  Global
+  // round u = 2 r + lw of the chunk (rounds r of this loader wave) covers
+  // slots 64 u .. 64 u + 63: row (64 u + l) / 8, stored chunk l % 8 holding
+  // logical chunk (l % 8) ^ swz(row); rows past the image repeat its last row
   auto copy = [&](int n) __attribute__((always_inline)) {
     GMIX_LDS unsigned char* dst = (GMIX_LDS unsigned char*)(smem + L::OFF_X + (n % XR) * L::XBUF);
 #pragma unroll
@@ -480,8 +490,8 @@ __device__ __forceinline__ void loader(const GmArgs& p, unsigned char* smem, int
       const int u = 2 * r + lw;
       const int row = 8 * u + (lane >> 3);
       const int pos = min(p0 + row, p.HW - 1);
-      const int logical = (lane & 7) ^ ((row >> 1) & 7);
-      const uint16_t* src = p.x + ((int64_t)b * p.HW + pos) * p.C + n * kChunk + logical * 8;
+      const int logical = (lane & 7) ^ swz(row);
+      const uint16_t* src = p.x + ((int64_t)b * p.HW + pos) * p.C + n * kStep + logical * 8;
       __builtin_amdgcn_global_load_lds((const void*)src, (GMIX_LDS void*)(dst + u * 1024), 16, 0, kCachePolicyNT);
     }
   };
@@ -491,24 +501,19 @@ __device__ __forceinline__ void loader(const GmArgs& p, unsigned char* smem, int
   wait_chunks<L::ROUNDS, XR>(first - 1);
   lds_barrier();  // prologue
   for (int ks = 0; ks < p.nsteps; ++ks) {
-    const int c = ks >> 1;
-    if ((ks & 1) == 0) {
-      // chunk c + XR - 1 into the slot chunk c - 1 left (free since the
-      // barrier that ended step ks - 1)
-      if (c + XR - 1 < nchunks) copy(c + XR - 1);
-    } else if (ks + 1 < p.nsteps) {
-      // chunk c + 1 complete before the barrier; the later ones may fly on
-      const int issued = min(c + XR - 1, nchunks - 1);
-      wait_chunks<L::ROUNDS, XR>(issued - (c + 1));
-    }
+    // chunk ks + XR - 1 into the slot chunk ks - 1 left (free since the
+    // barrier that ended step ks - 1); chunk ks + 1 complete before this
+    // step's barrier, the later ones may fly on
+    if (ks + XR - 1 < nchunks) copy(ks + XR - 1);
+    if (ks + 1 < nchunks) wait_chunks<L::ROUNDS, XR>(min(ks + XR - 1, nchunks - 1) - (ks + 1));
     lds_barrier();
   }
 }
 
-template <int MB, int NB, int NS>
-__global__ void __launch_bounds__(kThreads, 1)
+template <int MB, int NB, int NS, int OCC>
+__global__ void __launch_bounds__(kThreads, OCC)
 k_gmix(GmArgs p) {
-  using L = Layout<MB, NB, NS>;
+  using L = Layout<MB, NB, NS, OCC>;
   extern __shared__ __align__(16) unsigned char smem[];
   const int v = unit_of(p);
   if (v >= p.units) return;  // uniform per workgroup: no barrier is skipped by part of it
@@ -519,11 +524,11 @@ k_gmix(GmArgs p) {
   const int p0 = jt * L::MT, o0 = q * L::NE;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (wv < kConsumers)
-    consumer<MB, NB, NS>(p, smem, wv);
+    consumer<MB, NB, NS, OCC>(p, smem, wv);
   else if (wv < kConsumers + kBuilders)
-    builder<MB, NB, NS>(p, smem, wv - kConsumers, b, q);
+    builder<MB, NB, NS, OCC>(p, smem, wv - kConsumers, b, q);
   else
-    loader<MB, NB, NS>(p, smem, wv - kConsumers - kBuilders, b, p0);
+    loader<MB, NB, NS, OCC>(p, smem, wv - kConsumers - kBuilders, b, p0);
   lds_barrier();  // results staged
   // whole 16-byte pieces of the staged rows to y[b][p0 + row][o0 ..]
   constexpr int kPieces = L::NE / 8;
@@ -539,11 +544,11 @@ k_gmix(GmArgs p) {
 
 using GmKernel = void (*)(GmArgs);
 
-template <int MB, int NB, int NS>
-size_t lds_of() { return Layout<MB, NB, NS>::bytes(); }
+template <int MB, int NB, int NS, int OCC>
+size_t lds_of() { return Layout<MB, NB, NS, OCC>::bytes(); }
 
 struct Variant {
-  int MB, NB, NS;
+  int MB, NB, NS, OCC;
   GmKernel k;
   size_t (*lds)();
 };
@@ -551,11 +556,10 @@ struct Variant {
 constexpr int kParts = 2;
 
 const Variant kVariants[] = {
-    {4, 4, 2, k_gmix<4, 4, 2>, lds_of<4, 4, 2>},
-    {4, 2, 2, k_gmix<4, 2, 2>, lds_of<4, 2, 2>},
-    {4, 3, 2, k_gmix<4, 3, 2>, lds_of<4, 3, 2>},
-    {7, 2, 2, k_gmix<7, 2, 2>, lds_of<7, 2, 2>},
-    {7, 3, 2, k_gmix<7, 3, 2>, lds_of<7, 3, 2>},
+    {4, 4, 2, 1, k_gmix<4, 4, 2, 1>, lds_of<4, 4, 2, 1>},
+    {4, 3, 2, 1, k_gmix<4, 3, 2, 1>, lds_of<4, 3, 2, 1>},
+    {7, 2, 2, 1, k_gmix<7, 2, 2, 1>, lds_of<7, 2, 2, 1>},
+    {7, 3, 2, 1, k_gmix<7, 3, 2, 1>, lds_of<7, 3, 2, 1>},
 };
 
 int cu_count() {
@@ -575,7 +579,7 @@ const Variant* pick(const Shape& sh) {
   int64_t best_cost = 0;
   for (const Variant& v : kVariants) {
     if (v.NS != kParts) continue;
-    if (v.lds() > (size_t)kLdsBytes) continue;
+    if (v.lds() * v.OCC > (size_t)kLdsBytes) continue;
     const int64_t nt = (sh.HW + 16 * v.MB - 1) / (16 * v.MB);
     const int64_t nq = (nblk + 4 * v.NB - 1) / (4 * v.NB);
     const int64_t units = sh.B * nt * nq;
@@ -610,7 +614,7 @@ SchedShape sched_shape(const Shape& sh, const Variant& v) {
 
 bool gmix_eligible(const Shape& sh) {
   if (sh.layout != MOCE_NHWC || sh.elem != MOCE_BF16 || sh.R < 1) return false;
-  if (sh.C % kChunk != 0 || sh.C > kStep * kMaxSteps || sh.E % 8 != 0) return false;
+  if (sh.C % kStep != 0 || sh.C > kStep * kMaxSteps || sh.E % 8 != 0) return false;
   if ((int64_t)sh.B * sh.HW > INT32_MAX / 2) return false;
   return pick(sh) != nullptr;
 }

@@ -209,8 +209,9 @@ def test_workspace_size_and_errors(lib):
     assert _call_forward(desc, gate, ws_bytes=need - 1) == -7
     nhwc = good_desc(layout=mb.MOCE_NHWC)
     # bf16 channels-last with C a multiple of 64 takes the scheduled mix: no coefficients, but the support
-    # schedule (offsets [1 group][2 steps + 1] in 256 bytes, entries [1][16 k + C] of 8 bytes)
-    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 512 + 256 + (16 * 8 + 64) * 8
+    # schedule of one expert range with eight builder buckets (offsets [8][1 step + 1] in 256 bytes, entries
+    # [8][2 * 16 k + C] of 8 bytes)
+    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 512 + 256 + 8 * (32 * 8 + 64) * 8
     f32 = good_desc(layout=mb.MOCE_NHWC, dtype=mb.MOCE_F32)
     assert lib.moce_forward_workspace_bytes(ctypes.byref(f32)) == 512 + 256 + 512
 
