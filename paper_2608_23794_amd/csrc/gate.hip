@@ -8,6 +8,8 @@
 // writes the coefficients alpha[b][o][i] and/or the softmax statistics
 // (rt = 1/tau, the largest scaled logit m, rzs = 1 / partition sum), from
 // which a mix kernel rebuilds exactly the same coefficients.
+#include <algorithm>
+#include <cstdint>
 #include <type_traits>
 
 #include "moce_internal.h"
@@ -16,15 +18,19 @@ namespace moce {
 namespace {
 
 constexpr int kGateWaves = 4;
+constexpr int64_t kGateTargetWaves = 4096;  // waves of the image-walking gate (16 per CU)
+constexpr int64_t kLdsGateTargetBlocks = 512;  // workgroups of the LDS gate (two per CU)
+constexpr int64_t kLdsGateMaxImages = 32;     // images per workgroup at most
 
-__device__ __forceinline__ void put_stats(const Stats& st, int64_t item, float rt, float m, float rzs) {
-  st.rt[item] = rt;
-  st.m[item] = m;
-  st.rzs[item] = rzs;
+__device__ __forceinline__ void put_stats(const Stats& st, int64_t b, int o, float rt, float m, float rzs) {
+  const int64_t i = b * st.sb + o * st.so;
+  st.rt[i] = rt;
+  st.m[i] = m;
+  st.rzs[i] = rzs;
 }
 
 __device__ __forceinline__ void softmax_epilogue(const float* __restrict__ wo, int k, float t, int lane,
-                                                 float* __restrict__ alpha_row, const Stats* st, int64_t item) {
+                                                 float* __restrict__ alpha_row, const Stats* st, int64_t b, int o) {
   const float rt = 1.f / t;
   float m = -INFINITY;
   for (int i = lane; i < k; i += kWave) m = fmaxf(m, coef_z(wo[i], rt));
@@ -36,7 +42,7 @@ __device__ __forceinline__ void softmax_epilogue(const float* __restrict__ wo, i
   if (alpha_row) {
     for (int i = lane; i < k; i += kWave) alpha_row[i] = coef_alpha(coef_e(coef_z(wo[i], rt), m), rzs);
   }
-  if (st && lane == 0) put_stats(*st, item, rt, m, rzs);
+  if (st && lane == 0) put_stats(*st, b, o, rt, m, rzs);
 }
 
 __global__ void __launch_bounds__(kGateWaves * kWave)
@@ -56,8 +62,8 @@ k_gate_softplus(const float* __restrict__ d, const int32_t* __restrict__ s, cons
   g = wave_sum(g) + c[o];
   const float t = softplusf(g) + 1e-3f;
   if (lane == 0) tau[item] = t;
-  softmax_epilogue(w + (int64_t)o * k, k, t, lane, alpha ? alpha + item * k : nullptr, st.rt ? &st : nullptr,
-                   item);
+  softmax_epilogue(w + (int64_t)o * k, k, t, lane, alpha ? alpha + item * k : nullptr, st.rt ? &st : nullptr, b,
+                   o);
 }
 
 // The same for k <= W (W = 32): segments of W lanes, one per (image,
@@ -96,7 +102,7 @@ k_gate_softplus_seg(const float* __restrict__ d, const int32_t* __restrict__ s, 
   if (!live) return;
   if (i == 0) tau[item] = t;
   if (alpha && in) alpha[item * k + i] = coef_alpha(ex, rzs);
-  if (st.rt && i == 0) put_stats(st, item, rt, m, rzs);
+  if (st.rt && i == 0) put_stats(st, b, o, rt, m, rzs);
 }
 
 // The value of lane l ^ OFF within rows of 16 lanes, by DPP moves (quad
@@ -134,25 +140,30 @@ __device__ __forceinline__ float row16_max(float v, int lane) {
 }
 
 // The softplus-linear gate for 32 < k <= 16 PER: a row of 16 lanes per
-// (image, expert), four per wave, lane h holding support positions
+// routed expert, four experts per wave, lane h holding support positions
 // h, h + 16, ..., so that each read instruction covers 16 consecutive entries
-// of every pair.  Every input of a lane is read up front; the three
-// reductions are DPP moves within the row.
+// of every expert.  A wave keeps its experts' supports, gate weights and
+// logits in registers and walks `nbi` consecutive images, reading the next
+// image's descriptor gathers while it forms the current one's softmax; the
+// three reductions are DPP moves within the row.  Waves of one workgroup
+// share their images, so an image's descriptor is fetched once per CU.
 template <int PER>
 __global__ void __launch_bounds__(kGateWaves * kWave)
 k_gate_softplus_x16(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
                     const float* __restrict__ a, const float* __restrict__ c, float* __restrict__ tau,
-                    float* __restrict__ alpha, Stats st, int64_t B, int64_t C, int R, int k) {
+                    float* __restrict__ alpha, Stats st, int64_t B, int64_t C, int R, int k, int nrow, int nbi) {
   const int lane = threadIdx.x & 63;
   const int h = lane & 15;
-  const int64_t item = ((int64_t)blockIdx.x * kGateWaves + (threadIdx.x >> 6)) * 4 + (lane >> 4);
-  const bool live = item < B * R;
-  const int64_t it = live ? item : B * R - 1;
-  const int64_t b = it / R;
-  const int o = (int)(it % R);
+  const int64_t wave = (int64_t)blockIdx.x * kGateWaves + (threadIdx.x >> 6);
+  const int64_t b0 = (wave / nrow) * nbi;
+  const int orow = (int)(wave % nrow);
+  const int o_raw = 4 * orow + (lane >> 4);
+  const bool live = o_raw < R && b0 < B;
+  const int o = min(o_raw, R - 1);
+  const int64_t b1 = min(b0 + nbi, B);
   const int64_t e0 = (int64_t)o * k;
   int ch[PER];
-  float av[PER], wv[PER], dv[PER];
+  float av[PER], wv[PER];
 #pragma unroll
   for (int t = 0; t < PER; ++t) {
     const int i = min(h + 16 * t, k - 1);
@@ -161,40 +172,238 @@ k_gate_softplus_x16(const float* __restrict__ d, const int32_t* __restrict__ s, 
     wv[t] = w[e0 + i];
   }
   const float co = c[o];
-  const float* db = d + b * C;
+  // descriptor gathers of image bb (clamped into the wave's range: the read
+  // is issued on every pass, its value used only where bb is live)
+  float dv[PER];
+  auto gather = [&](int64_t bb, float (&v)[PER]) __attribute__((always_inline)) {
+    const float* db = d + min(bb, B - 1) * C;
 #pragma unroll
-  for (int t = 0; t < PER; ++t) dv[t] = db[ch[t]];
-  float g = 0.f;
-#pragma unroll
-  for (int t = 0; t < PER; ++t)
-    if (h + 16 * t < k) g += av[t] * dv[t];
-  g = row16_sum(g, lane) + co;
-  const float tv = softplusf(g) + 1e-3f;
-  const float rt = 1.f / tv;
-  float z[PER];
-  float m = -INFINITY;
-#pragma unroll
-  for (int t = 0; t < PER; ++t) {
-    z[t] = coef_z(wv[t], rt);
-    if (h + 16 * t < k) m = fmaxf(m, z[t]);
-  }
-  m = row16_max(m, lane);
-  float zs = 0.f;
-#pragma unroll
-  for (int t = 0; t < PER; ++t) {
-    z[t] = coef_e(z[t], m);
-    if (h + 16 * t < k) zs += z[t];
-  }
-  zs = row16_sum(zs, lane);
-  const float rzs = 1.f / zs;
-  if (!live) return;
-  if (h == 0) tau[item] = tv;
-  if (alpha) {
+    for (int t = 0; t < PER; ++t) v[t] = db[ch[t]];
+  };
+  gather(b0, dv);
+  for (int64_t b = b0; b < b1; ++b) {
+    float dn[PER];
+    gather(b + 1 < b1 ? b + 1 : b, dn);
+    float g = 0.f;
 #pragma unroll
     for (int t = 0; t < PER; ++t)
-      if (h + 16 * t < k) alpha[item * k + h + 16 * t] = coef_alpha(z[t], rzs);
+      if (h + 16 * t < k) g += av[t] * dv[t];
+    g = row16_sum(g, lane) + co;
+    const float tv = softplusf(g) + 1e-3f;
+    const float rt = 1.f / tv;
+    float z[PER];
+    float m = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < PER; ++t) {
+      z[t] = coef_z(wv[t], rt);
+      if (h + 16 * t < k) m = fmaxf(m, z[t]);
+    }
+    m = row16_max(m, lane);
+    float zs = 0.f;
+#pragma unroll
+    for (int t = 0; t < PER; ++t) {
+      z[t] = coef_e(z[t], m);
+      if (h + 16 * t < k) zs += z[t];
+    }
+    zs = row16_sum(zs, lane);
+    const float rzs = 1.f / zs;
+    const int64_t item = b * R + o;
+    if (live) {
+      if (h == 0) tau[item] = tv;
+      if (alpha) {
+#pragma unroll
+        for (int t = 0; t < PER; ++t)
+          if (h + 16 * t < k) alpha[item * k + h + 16 * t] = coef_alpha(z[t], rzs);
+      }
+      if (st.rt && h == 0) put_stats(st, b, o, rt, m, rzs);
+    }
+#pragma unroll
+    for (int t = 0; t < PER; ++t) dv[t] = dn[t];
   }
-  if (st.rt && h == 0) put_stats(st, item, rt, m, rzs);
+}
+
+// The value of lane l ^ OFF within groups of 8 lanes (OFF = 1, 2, 4).
+template <int OFF>
+__device__ __forceinline__ float row8_xor(float v, int lane) {
+  static_assert(OFF == 1 || OFF == 2 || OFF == 4, "within 8 lanes");
+  return row16_xor<OFF>(v, lane);
+}
+__device__ __forceinline__ float row8_sum(float v, int lane) {
+  v += row8_xor<4>(v, lane);
+  v += row8_xor<2>(v, lane);
+  v += row8_xor<1>(v, lane);
+  return v;
+}
+__device__ __forceinline__ float row8_max(float v, int lane) {
+  v = fmaxf(v, row8_xor<4>(v, lane));
+  v = fmaxf(v, row8_xor<2>(v, lane));
+  v = fmaxf(v, row8_xor<1>(v, lane));
+  return v;
+}
+
+// The softplus-linear gate for 32 < k <= 8 PER with the descriptors in LDS.
+// A group of 8 lanes per routed expert: lane h holds the support positions
+// 8 VW t + VW h + q (q < VW), read as VW-wide vectors so that a read
+// instruction covers whole cache lines of 8 experts' rows.  A workgroup of
+// kLdsGateThreads lanes holds 32 experts and walks `nbi` consecutive images;
+// each image's descriptor row is copied into LDS once (direct
+// global-to-LDS copies, issued while the previous image is formed), so the
+// support gathers are LDS reads.  Since 1/tau > 0 and rounding is
+// monotonic, the largest scaled logit is the largest logit scaled:
+// m = coef_z(max_i w_i, rt) has the bits of max_i coef_z(w_i, rt), and the
+// maximum of the logits is taken once per expert instead of once per image.
+constexpr int kLdsGateMaxC = 4096;  // descriptor rows of at most 16 KB
+constexpr int kGateRing = 4;       // descriptor rows in LDS: the current one and two in flight
+constexpr int kLdsGateThreads = 256;
+constexpr int kLdsGateExperts = kLdsGateThreads / 8;
+
+template <int VW>
+struct VecOf;
+template <>
+struct VecOf<1> {
+  using f = float;
+  using i = int;
+};
+template <>
+struct VecOf<2> {
+  using f = float2;
+  using i = int2;
+};
+template <>
+struct VecOf<4> {
+  using f = float4;
+  using i = int4;
+};
+template <int VW, typename V>
+__device__ __forceinline__ auto vget(const V& v, int q) {
+  if constexpr (VW == 1) {
+    return v;
+  } else if constexpr (VW == 2) {
+    return q == 0 ? v.x : v.y;
+  } else {
+    return q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w;
+  }
+}
+
+// waits until at most n (0 <= n <= 63) vector memory operations of this wave
+// are outstanding (one s_waitcnt with a constant operand per possible n)
+template <int... Ns>
+__device__ __forceinline__ void wait_vm_of(int n, std::integer_sequence<int, Ns...>) {
+  ((n == Ns ? (__builtin_amdgcn_s_waitcnt((Ns & 15) | ((Ns >> 4) << 14) | 0x0f70), 0) : 0), ...);
+}
+__device__ __forceinline__ void wait_vm_at_most(int n) { wait_vm_of(n, std::make_integer_sequence<int, 64>{}); }
+
+template <int PER, int VW>
+__global__ void __launch_bounds__(kLdsGateThreads)
+k_gate_softplus_lds(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
+                    const float* __restrict__ a, const float* __restrict__ c, float* __restrict__ tau,
+                    float* __restrict__ alpha, Stats st, int64_t B, int C, int R, int k, int nblk, int nbi) {
+  static_assert(PER % VW == 0, "whole vectors");
+  constexpr int NV = PER / VW;
+  using VF = typename VecOf<VW>::f;
+  using VI = typename VecOf<VW>::i;
+  // LDS: kGateRing descriptor rows of cpad floats (C rounded up to 64), then
+  // the results (tau, rt, m, rzs) of the workgroup's experts for each image
+  extern __shared__ float gsm[];
+  const int cpad = (C + 63) & ~63;
+  float4* res = reinterpret_cast<float4*>(gsm + kGateRing * cpad);
+  const int lane = threadIdx.x & 63;
+  const int h = lane & 7;
+  const int ex = threadIdx.x >> 3;  // expert slot within the workgroup
+  const int64_t b0 = (int64_t)(blockIdx.x / nblk) * nbi;
+  const int o0 = (blockIdx.x % nblk) * kLdsGateExperts;
+  const int o = min(o0 + ex, R - 1);
+  const int nimg = (int)(min(b0 + nbi, B) - b0);
+  // position of element q of vector t of this lane (k need not fill the last
+  // vectors; a vector that starts past k is read from the row's first
+  // entries)
+  auto pos = [&](int t, int q) __attribute__((always_inline)) { return 8 * VW * t + VW * h + q; };
+  int ch[PER];
+  float av[PER], wv[PER];
+  float wmax = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < NV; ++t) {
+    const int64_t base = (int64_t)o * k + (pos(t, 0) < k ? pos(t, 0) : 0);
+    const VI sv = *reinterpret_cast<const VI*>(s + base);
+    const VF avv = *reinterpret_cast<const VF*>(a + base);
+    const VF wvv = *reinterpret_cast<const VF*>(w + base);
+#pragma unroll
+    for (int q = 0; q < VW; ++q) {
+      // a position past k adds nothing: gate weight 0 (at a valid channel)
+      // and logit -inf (coefficient exp2(-inf) = 0), so no lane branches
+      const bool in = pos(t, q) < k;
+      ch[VW * t + q] = in ? vget<VW>(sv, q) : 0;
+      av[VW * t + q] = in ? vget<VW>(avv, q) : 0.f;
+      wv[VW * t + q] = in ? vget<VW>(wvv, q) : -INFINITY;
+      wmax = fmaxf(wmax, wv[VW * t + q]);
+    }
+  }
+  wmax = row8_max(wmax, lane);
+  const float co = c[o];
+  // descriptor row of image i (clamped into the workgroup's images) into
+  // ring slot i % kGateRing by direct global-to-LDS copies.  Every wave
+  // issues exactly fpw copies per row (64-float pieces v, v + nwaves, ...,
+  // the last piece repeated where the row runs out; a piece past C repeats
+  // entry C - 1 into the padding), so a row is complete once at most
+  // fpw times the number of rows issued after it are outstanding.
+  const int wv_id = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  const int npieces = cpad / 64;
+  const int fpw = (npieces + nwaves - 1) / nwaves;
+  auto fetch = [&](int i) __attribute__((always_inline)) {
+    const float* db = d + (b0 + min(i, nimg - 1)) * C;
+    float* buf = gsm + (i % kGateRing) * cpad;
+    for (int u = 0; u < fpw; ++u) {
+      const int q = min(wv_id + nwaves * u, npieces - 1);
+      __builtin_amdgcn_global_load_lds((const void*)(db + min(q * 64 + lane, C - 1)),
+                                       (__attribute__((address_space(3))) void*)(buf + q * 64), 4, 0, 0);
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < kGateRing - 1; ++i) fetch(i);
+  wait_vm_at_most((kGateRing - 2) * fpw);  // row 0 has landed
+  __syncthreads();
+  for (int i = 0; i < nimg; ++i) {
+    // slot (i + kGateRing - 1) % kGateRing was last read for image i - 1,
+    // before the barrier that ended it
+    fetch(i + kGateRing - 1);
+    const float* dr = gsm + (i % kGateRing) * cpad;
+    float g = 0.f;
+#pragma unroll
+    for (int t = 0; t < PER; ++t) g += av[t] * dr[ch[t]];
+    g = row8_sum(g, lane) + co;
+    const float tv = softplusf(g) + 1e-3f;
+    const float rt = 1.f / tv;
+    const float m = coef_z(wmax, rt);
+    float zs = 0.f;
+    float z[PER];
+#pragma unroll
+    for (int t = 0; t < PER; ++t) {
+      z[t] = coef_e(coef_z(wv[t], rt), m);
+      zs += z[t];
+    }
+    zs = row8_sum(zs, lane);
+    const float rzs = 1.f / zs;
+    if (h == 0) res[i * kLdsGateExperts + ex] = make_float4(tv, rt, m, rzs);
+    if (alpha && o0 + ex < R) {
+      const int64_t item = (b0 + i) * R + o;
+#pragma unroll
+      for (int t = 0; t < NV; ++t)
+#pragma unroll
+        for (int q = 0; q < VW; ++q)
+          if (pos(t, q) < k) alpha[item * k + pos(t, q)] = coef_alpha(z[VW * t + q], rzs);
+    }
+    wait_vm_at_most((kGateRing - 2) * fpw);  // row i + 1 has landed
+    __syncthreads();
+  }
+  // the results, image by image, 32 consecutive experts each
+  for (int idx = threadIdx.x; idx < nimg * kLdsGateExperts; idx += blockDim.x) {
+    const int i = idx / kLdsGateExperts, e = idx - i * kLdsGateExperts;
+    if (o0 + e >= R) continue;
+    const int64_t item = (b0 + i) * R + o0 + e;
+    const float4 r4 = res[idx];
+    tau[item] = r4.x;
+    if (st.rt) put_stats(st, b0 + i, o0 + e, r4.y, r4.z, r4.w);
+  }
 }
 
 // The paper's shared gate: h = ReLU(W1 z + b1), g = w2 . h + b2,
@@ -226,8 +435,8 @@ k_gate_mlp(const float* __restrict__ d, const int32_t* __restrict__ s, const flo
   g = wave_sum(g) + b2;
   const float t = tau_min + (tau_max - tau_min) / (1.f + expf(-g));
   if (lane == 0) tau[item] = t;
-  softmax_epilogue(w + (int64_t)o * k, k, t, lane, alpha ? alpha + item * k : nullptr, st.rt ? &st : nullptr,
-                   item);
+  softmax_epilogue(w + (int64_t)o * k, k, t, lane, alpha ? alpha + item * k : nullptr, st.rt ? &st : nullptr, b,
+                   o);
 }
 
 }  // namespace
@@ -236,19 +445,51 @@ hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const 
                        const moce_gate_params& g, float* tau, float* alpha, float* stats, hipStream_t st) {
   if (sh.R == 0) return hipSuccess;
   const int64_t items = sh.B * sh.R;
-  const Stats sp = stats ? stats_planes(stats, items) : Stats{nullptr, nullptr, nullptr};
+  const Stats sp = stats ? stats_planes(stats, items, sh.R, 1) : Stats{nullptr, nullptr, nullptr, 0, 0};
   const unsigned blocks = (unsigned)((items + kGateWaves - 1) / kGateWaves);
   if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 32) {
     const unsigned b32 = (unsigned)((items + 2 * kGateWaves - 1) / (2 * kGateWaves));
     hipLaunchKernelGGL(k_gate_softplus_seg<32>, dim3(b32), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
                        tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);
+  } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 128 && sh.C <= kLdsGateMaxC) {
+    // 32 experts per workgroup, nbi images each, for about kLdsGateTargetBlocks
+    // workgroups
+    const int nblk = (int)((sh.R + kLdsGateExperts - 1) / kLdsGateExperts);
+    const int64_t nbi = std::min<int64_t>(
+        kLdsGateMaxImages, std::max<int64_t>(1, ((int64_t)nblk * sh.B + kLdsGateTargetBlocks - 1) / kLdsGateTargetBlocks));
+    const unsigned grid = (unsigned)(nblk * ((sh.B + nbi - 1) / nbi));
+    const size_t lds = (kGateRing * ((sh.C + 63) / 64 * 64) + nbi * kLdsGateExperts * 4) * sizeof(float);
+    const int per = (sh.k + 7) / 8;
+    // vectors of 4 (or 2) positions where k fills whole rounds of them and
+    // the three arrays are aligned to the vector
+    auto aligned = [&](size_t bytes) {
+      return ((reinterpret_cast<uintptr_t>(s) | reinterpret_cast<uintptr_t>(g.a) | reinterpret_cast<uintptr_t>(w)) &
+              (bytes - 1)) == 0;
+    };
+    const int vw = sh.k % 32 == 0 && aligned(16) ? 4 : sh.k % 16 == 0 && aligned(8) ? 2 : 1;
+    using K = void (*)(const float*, const int32_t*, const float*, const float*, const float*, float*, float*, Stats,
+                       int64_t, int, int, int, int, int);
+    K kern = per <= 4 ? (vw == 4 ? k_gate_softplus_lds<4, 4> : vw == 2 ? k_gate_softplus_lds<4, 2> : k_gate_softplus_lds<4, 1>)
+             : per <= 6 ? (vw == 2 ? k_gate_softplus_lds<6, 2> : k_gate_softplus_lds<6, 1>)
+             : per <= 8 ? (vw == 4 ? k_gate_softplus_lds<8, 4> : vw == 2 ? k_gate_softplus_lds<8, 2> : k_gate_softplus_lds<8, 1>)
+                        : (vw == 4 ? k_gate_softplus_lds<16, 4> : vw == 2 ? k_gate_softplus_lds<16, 2> : k_gate_softplus_lds<16, 1>);
+    if (lds > 64 * 1024) {
+      const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kLdsGateThreads), lds, st, d, s, w, g.a, g.c, tau, alpha, sp, sh.B,
+                       (int)sh.C, sh.R, sh.k, nblk, (int)nbi);
   } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 256) {
-    // rows of 16 lanes, four (image, expert) pairs per wave
-    const unsigned b16 = (unsigned)((items + 4 * kGateWaves - 1) / (4 * kGateWaves));
+    // rows of 16 lanes, four experts per wave; each wave walks nbi images,
+    // nbi chosen for about 16 waves per CU
+    const int nrow = (int)((sh.R + 3) / 4);
+    const int64_t nbi = std::max<int64_t>(1, ((int64_t)nrow * sh.B + kGateTargetWaves - 1) / kGateTargetWaves);
+    const int64_t waves = (int64_t)nrow * ((sh.B + nbi - 1) / nbi);
+    const unsigned b16 = (unsigned)((waves + kGateWaves - 1) / kGateWaves);
     const int per = (sh.k + 15) / 16;
     auto kern = per <= 4 ? k_gate_softplus_x16<4> : per <= 8 ? k_gate_softplus_x16<8> : k_gate_softplus_x16<16>;
     hipLaunchKernelGGL(kern, dim3(b16), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c, tau, alpha, sp, sh.B,
-                       sh.C, sh.R, sh.k);
+                       sh.C, sh.R, sh.k, nrow, (int)nbi);
   } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR) {
     hipLaunchKernelGGL(k_gate_softplus, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
                        tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);

@@ -55,11 +55,12 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 #define GMIX_LDS __attribute__((address_space(3)))
 
 constexpr int kStep = 64;                 // channels per step: two K slices of the MFMA, one x chunk
 constexpr int kXRow = kStep * 2;          // bytes of one position row of an x chunk
-constexpr int kBRow = kStep * 2;          // bytes of one expert row of a B buffer part
+constexpr int kBRow = kStep * 2;          // bytes of one expert row of one part of a B buffer
 constexpr int kMaxXRing = 8;              // x chunk buffers at most (the ring fills the LDS left over)
 constexpr int kConsumers = 4;
 constexpr int kBuilders = 8;
@@ -217,7 +218,7 @@ k_pool_sched(const T* __restrict__ x, float* __restrict__ d, int C, int HW, int 
     return;
   }
   const int i = blockIdx.x - a.nbuckets;
-  pool_rows_block<T>(x, d, C, HW, i / nblk, i % nblk, part);
+  pool_rows_block<T>(x, d, C, HW, i / nblk, i % nblk, part, C, 1);
 }
 
 // ---------------------------------------------------------------- the mix
@@ -226,7 +227,9 @@ struct Layout {
   static constexpr int MT = 16 * MB;                 // positions per tile
   static constexpr int NE = 64 * NB;                 // experts per workgroup
   static constexpr int XBUF = MT * kXRow;            // one x chunk
-  static constexpr int PART = NE * kBRow;            // one part of one B buffer
+  static_assert(NS == 2, "two coefficient parts");
+  static constexpr int PART = (NE + 1) * kBRow;      // one part of one B buffer: NE rows and a trash row
+  static constexpr int TRASH = NE * kBRow;           // the trash row, stored into by lanes with no entry
   static constexpr int BBUF = NS * PART;             // one B buffer
   // as many x chunks in flight as the LDS left by the B buffers and the
   // statistics allows (OCC workgroups per CU share its LDS): at most
@@ -284,28 +287,63 @@ __device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, i
   const int arow = n * kXRow;
   const int brow = (16 * NB * wv + n) * kBRow;
   const int ch0 = (g ^ (n >> 1)) << 4, ch1 = ((4 + g) ^ (n >> 1)) << 4;
+  // A step is two K slices.  A slice runs one pass per part: every
+  // accumulator once, so an accumulator's products are MB NB MFMAs apart.
+  // The next slice's fragments are read into the registers of this slice's
+  // as soon as their last use is issued: its B part-0 fragments after this
+  // slice's part-0 pass, its A fragments block by block in the part-1 pass,
+  // its B part-1 fragments after it; only the step's first slice waits for
+  // its reads (the barrier before it is what makes them valid).
+  auto load_a = [&](const unsigned char* xb, int h, int mb) __attribute__((always_inline)) {
+    return __builtin_bit_cast(bf16x8,
+                              *reinterpret_cast<const u32x4*>(xb + mb * 16 * kXRow + (h ? ch1 : ch0)));
+  };
+  auto load_b = [&](const unsigned char* bb, int h, int nb, int pt) __attribute__((always_inline)) {
+    return __builtin_bit_cast(
+        bf16x8, *reinterpret_cast<const u32x4*>(bb + pt * L::PART + nb * 16 * kBRow + (h ? ch1 : ch0)));
+  };
   lds_barrier();  // prologue: chunk 0 and the step-0 coefficients are in LDS
   for (int ks = 0; ks < p.nsteps; ++ks) {
     const unsigned char* xb = smem + L::OFF_X + (ks % L::XR) * L::XBUF + arow;
     const unsigned char* bb = smem + L::OFF_B + (ks & 1) * L::BBUF + brow;
+    bf16x8 a[MB], b0[NB], b1[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) b0[nb] = load_b(bb, 0, nb, 0);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) a[mb] = load_a(xb, 0, mb);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) b1[nb] = load_b(bb, 0, nb, 1);
+    // the compiler's scheduler would move each read next to its first use;
+    // the fences keep them where they are issued here
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int ch = h ? ch1 : ch0;
-      bf16x8 bf[NB][NS];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int pt = 0; pt < NS; ++pt)
-          bf[nb][pt] =
-              __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(bb + pt * L::PART + nb * 16 * kBRow + ch));
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mb], b0[nb], acc[mb][nb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (h == 0) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) b0[nb] = load_b(bb, 1, nb, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
-        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(xb + mb * 16 * kXRow + ch));
 #pragma unroll
-        for (int pt = 0; pt < NS; ++pt)
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mb], b1[nb], acc[mb][nb], 0, 0, 0);
+        if (h == 0) {
+          __builtin_amdgcn_sched_barrier(0);
+          a[mb] = load_a(xb, 1, mb);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      if (h == 0) {
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bf[nb][pt], acc[mb][nb], 0, 0, 0);
+        for (int nb = 0; nb < NB; ++nb) b1[nb] = load_b(bb, 1, nb, 1);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     lds_barrier();  // step ks done: its x chunk and B buffer may be reused
@@ -376,37 +414,39 @@ __device__ __forceinline__ void builder(const GmArgs& p, unsigned char* smem, in
   // stores; more than 64 kRounds entries (rare) are read one round at a time
   auto put = [&](unsigned char* buf, int t, const uint2 (&e)[kRounds], int n, bool clear)
       __attribute__((always_inline)) {
-    uint16_t pt[kRounds][NS];
+    // a lane past the list's end stores into the trash row instead of
+    // branching around its store; rounds wholly past the end are skipped
+    // (uniform: n is the wave's)
+    int off[kRounds];
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) off[r] = 64 * r + lane < n ? (int)(e[r].x & kOffMask) : L::TRASH;
     if (clear) {
 #pragma unroll
       for (int r = 0; r < kRounds; ++r)
+        if (r == 0 || 64 * r < n)
 #pragma unroll
-        for (int v = 0; v < NS; ++v) pt[r][v] = 0;
+          for (int v = 0; v < NS; ++v) *reinterpret_cast<uint16_t*>(buf + v * L::PART + off[r]) = 0;
     } else {
       float4 sv[kRounds];
 #pragma unroll
-      for (int r = 0; r < kRounds; ++r) sv[r] = st[min((int)((e[r].x >> kSlotShift) & 0xff), L::NE - 1)];
+      for (int r = 0; r < kRounds; ++r)
+        if (r == 0 || 64 * r < n) sv[r] = st[min((int)((e[r].x >> kSlotShift) & 0xff), L::NE - 1)];
 #pragma unroll
-      for (int r = 0; r < kRounds; ++r) {
-        const float a = (e[r].x & kResidualFlag)
-                            ? p.inv_nU
-                            : coef_alpha(coef_e(coef_z(__uint_as_float(e[r].y), sv[r].x), sv[r].y), sv[r].z);
-        split_parts<NS>(a, pt[r]);
-      }
+      for (int r = 0; r < kRounds; ++r)
+        if (r == 0 || 64 * r < n) {
+          const float a = (e[r].x & kResidualFlag)
+                              ? p.inv_nU
+                              : coef_alpha(coef_e(coef_z(__uint_as_float(e[r].y), sv[r].x), sv[r].y), sv[r].z);
+          uint16_t pt[NS];
+          split_parts<NS>(a, pt);
+#pragma unroll
+          for (int v = 0; v < NS; ++v) *reinterpret_cast<uint16_t*>(buf + v * L::PART + off[r]) = pt[v];
+        }
     }
-#pragma unroll
-    for (int r = 0; r < kRounds; ++r)
-      if (64 * r + lane < n)
-#pragma unroll
-        for (int v = 0; v < NS; ++v)
-          *reinterpret_cast<uint16_t*>(buf + v * L::PART + (e[r].x & kOffMask)) = pt[r][v];
     for (int q0 = 64 * kRounds; q0 < n; q0 += 64) {
       const uint2 x = eb[min(ofs(t) + q0 + lane, p.cap - 1)];
-      uint16_t px[NS];
-      if (clear) {
-#pragma unroll
-        for (int v = 0; v < NS; ++v) px[v] = 0;
-      } else {
+      uint16_t px[NS] = {0, 0};
+      if (!clear) {
         const float4 s1 = st[min((int)((x.x >> kSlotShift) & 0xff), L::NE - 1)];
         const float a = (x.x & kResidualFlag) ? p.inv_nU
                                               : coef_alpha(coef_e(coef_z(__uint_as_float(x.y), s1.x), s1.y), s1.z);
@@ -559,7 +599,7 @@ const Variant kVariants[] = {
     {4, 4, 2, 1, k_gmix<4, 4, 2, 1>, lds_of<4, 4, 2, 1>},
     {4, 3, 2, 1, k_gmix<4, 3, 2, 1>, lds_of<4, 3, 2, 1>},
     {7, 2, 2, 1, k_gmix<7, 2, 2, 1>, lds_of<7, 2, 2, 1>},
-    {7, 3, 2, 1, k_gmix<7, 3, 2, 1>, lds_of<7, 3, 2, 1>},
+    {5, 3, 2, 1, k_gmix<5, 3, 2, 1>, lds_of<5, 3, 2, 1>},
 };
 
 int cu_count() {

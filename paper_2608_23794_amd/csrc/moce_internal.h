@@ -46,9 +46,24 @@ __device__ __forceinline__ int wave_min_int(int v) {
   return v;
 }
 
-// softplus(t) = log(1 + e^t) without overflow in either direction.
+// softplus(t) = log(1 + e^t) = max(t, 0) + log1p(e), e = e^-|t| in (0, 1],
+// from the hardware base-2 exponential and logarithm.  The rounding error of
+// the exponential's argument -|t| log2(e) is fed back to first order (one
+// FMA); log1p(e) is log(u) e / (u - 1) with u = 1 + e rounded, which cancels
+// the rounding of u (and is e itself where u rounds to 1).  A few ulp over
+// the whole range (relative error below 1e-6), in about 15 instructions
+// where the library's log1pf(expf(.)) takes over a hundred.
 __device__ __forceinline__ float softplusf(float t) {
-  return fmaxf(t, 0.f) + log1pf(expf(-fabsf(t)));
+#pragma clang fp contract(off)
+  constexpr float kL2e = 1.4426950408889634f, kLn2 = 0.6931471805599453f;
+  const float na = -fabsf(t);
+  const float x = na * kL2e;
+  const float dx = __builtin_fmaf(na, kL2e, -x);  // na log2(e) - x, exactly
+  float e = __builtin_amdgcn_exp2f(x);
+  e = __builtin_fmaf(e * kLn2, dx, e);            // e 2^dx to first order
+  const float u = 1.f + e;
+  const float l = u == 1.f ? e : (__builtin_amdgcn_logf(u) * kLn2) * (e * __builtin_amdgcn_rcpf(u - 1.f));
+  return fmaxf(t, 0.f) + l;
 }
 
 // ---- mixing coefficients (Sec. 3.3 Eq. 4) ----------------------------------
@@ -80,13 +95,17 @@ __device__ __forceinline__ float coef_alpha(float e, float rzs) {
 }
 
 // Softmax statistics of the B*R (image, expert) pairs, three planes of n =
-// B*R floats: rt[n], m[n], rzs[n].
+// B*R floats: rt[n], m[n], rzs[n]; pair (b, o) at b sb + o so, so image-major
+// [B][R] (sb = R, so = 1) or expert-major [R][B] (sb = 1, so = B).
 struct Stats {
   float* rt;
   float* m;
   float* rzs;
+  int64_t sb, so;
 };
-__host__ __device__ inline Stats stats_planes(float* base, int64_t n) { return Stats{base, base + n, base + 2 * n}; }
+__host__ __device__ inline Stats stats_planes(float* base, int64_t n, int64_t sb, int64_t so) {
+  return Stats{base, base + n, base + 2 * n, sb, so};
+}
 
 // ---- launch parameters derived from a validated descriptor ---------------
 struct Shape {
@@ -101,10 +120,11 @@ hipError_t launch_prepare(const Shape& sh, const int32_t* s, const float* w, int
                           float* w_out, uint8_t* covered, int32_t* U, int32_t* info,
                           hipStream_t st);
 hipError_t launch_pool(const Shape& sh, const void* x, float* d, hipStream_t st);
-// alpha and the softmax statistics (a block of 3 B R floats, planes as in
-// stats_planes) are optional outputs (nullptr: not written).
+// alpha and the softmax statistics (a block of 3 B R floats, image-major
+// planes as in stats_planes) are optional outputs (nullptr: not written).
 hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const float* w,
                        const moce_gate_params& g, float* tau, float* alpha, float* stats, hipStream_t st);
+
 // alpha != nullptr: coefficients are read from alpha[B][R][k]; otherwise
 // they are rebuilt from the logits w and the softmax statistics (a block of
 // 3 B R floats), with the gate's operations.
@@ -133,7 +153,7 @@ hipError_t launch_mfmamix_gated(const Shape& sh, const void* x, const int32_t* s
                                 const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st);
 
 // Channels-last bfloat16 mixing on the matrix cores from a per-forward
-// channel schedule of the supports (gmix.hip): C a multiple of 64 up to 2048,
+// channel schedule of the supports (gmix.hip): C a multiple of 64 up to 4096,
 // E a multiple of 8.  launch_pool_sched pools x into d and builds the
 // schedule (gmix_sched_bytes(sh) of device workspace) in one launch;
 // launch_gmix then mixes, rebuilding the coefficients from the softmax

@@ -155,7 +155,7 @@ template <typename T>
 __global__ void __launch_bounds__(kPoolThreads)
 k_pool_nhwc_rows(const T* __restrict__ x, float* __restrict__ d, int C, int HW, int nblk) {
   __shared__ float part[kPoolGroups * 32 * PoolVec<T>::EPV];
-  pool_rows_block<T>(x, d, C, HW, blockIdx.x / nblk, blockIdx.x % nblk, part);
+  pool_rows_block<T>(x, d, C, HW, blockIdx.x / nblk, blockIdx.x % nblk, part, C, 1);
 }
 
 template <typename T>

@@ -32,10 +32,11 @@ template <> struct PoolVec<float> {
 
 // Channels of block cb: 32 EPV of them from channel 32 EPV cb (C a multiple of
 // EPV; vectors past C are skipped).  `part` is LDS of
-// kPoolGroups * 32 * EPV floats.
+// kPoolGroups * 32 * EPV floats.  The mean of channel c of image b goes to
+// d[b sb + c sc]: sb = C, sc = 1 for d[B][C], sb = 1, sc = B for its transpose.
 template <typename T>
 __device__ __forceinline__ void pool_rows_block(const T* __restrict__ x, float* __restrict__ d, int C, int HW,
-                                                int64_t b, int cb, float* part) {
+                                                int64_t b, int cb, float* part, int64_t sb, int64_t sc) {
   constexpr int EPV = PoolVec<T>::EPV;
   const int l = threadIdx.x & 31, rg = threadIdx.x >> 5;
   const int c0 = (cb * 32 + l) * EPV;
@@ -65,7 +66,7 @@ __device__ __forceinline__ void pool_rows_block(const T* __restrict__ x, float* 
     if (c < C) {
       float s = 0.f;
       for (int r = 0; r < kPoolGroups; ++r) s += part[r * 32 * EPV + i];
-      d[b * C + c] = s / (float)HW;
+      d[b * sb + c * sc] = s / (float)HW;
     }
   }
 }
