@@ -267,7 +267,30 @@ def roofline_entry(kernels, path, mb, C):
 
 
 FORWARD_NAMES = {0: "pool, gate, mix", 1: "pool, gate, tile mix", 2: "pool, gate, matrix-core mix",
-                 3: "pool, gate inside the matrix-core mix"}
+                 3: "pool, gate inside the matrix-core mix",
+                 4: "pool with the support schedule, gate statistics, scheduled matrix-core mix"}
+
+# workloads whose line carries both gate forms timed through the gate entry point
+GATE_TIMED = ("resnet50_stage1", "resnet50_stage4")
+
+
+def gate_forms_us(bn, n_k):
+    """moce_gate of this workload with the softplus-linear gate and with the
+    paper's MLP gate (batched product), temperatures only, on the pooled
+    descriptor of the first input set."""
+    import torch
+    from paper_2608_23794_amd.layer import MoceLayer
+    mb, wl, B = bn.mb, bn.wl, bn.B
+    R, C = wl.E - 1, wl.C
+    d = torch.empty((B, C), dtype=torch.float32, device="cuda")
+    mb.moce_pool(bn.desc, bn.xs[0], d, torch.cuda.current_stream())
+    tau = torch.empty((B, R), dtype=torch.float32, device="cuda")
+    out = {}
+    for form in ("softplus", "mlp"):
+        L = bn.layer if form == "softplus" else MoceLayer.from_workload(wl, bn.g, bn.layout, gate="mlp")
+        t = launch_time_ms(lambda i, st: mb.moce_gate(bn.desc, d, L.s_c, L.w_c, L.gate, tau, None, st), n_k)
+        out[form] = round(t * 1e3, 2)
+    return out
 
 
 def other_config(name, layout, args, stream):
@@ -290,6 +313,11 @@ def other_config(name, layout, args, stream):
         "dominant_kernel": rf["kernel"], "dominant_kernel_us": round(kernels[rf["kernel"]][0] * 1e3, 2),
         "roofline_frac": rf["frac"],
     }
+    if bn.path == mb.PATH_SCHEDULED:
+        out["stage_entry_points_note"] = ("the entry points time the generic pool, gate and coefficient mix; the "
+                                          "scheduled forward's own kernels are timed in its rocprofv3 summaries")
+    if name in GATE_TIMED:
+        out["gate_entry_point_us"] = gate_forms_us(bn, n_g)
     if not args.no_context:
         out["context"] = bn.dense_context(max(args.steps // 4, 10), stream)
         out["context"]["moce_over_dense_time"] = round(med * 1e3 / out["context"]["dense_1x1_us"], 3)
@@ -396,6 +424,8 @@ def main():
         "stage_entry_points_us": {n: round(v[0] * 1e3, 2) for n, v in stages.items()},
         "roofline": roof,
     }
+    if wl.name in GATE_TIMED:
+        line["gate_entry_point_us"] = gate_forms_us(bn, max(args.steps // 2, 10))
     if not args.no_context:
         line["context"] = bn.dense_context(max(args.steps // 2, 10), stream)
         line["context"]["moce_over_dense_time"] = round(ms * 1e3 / line["context"]["dense_1x1_us"], 3)

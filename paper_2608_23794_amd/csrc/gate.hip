@@ -439,6 +439,283 @@ k_gate_mlp(const float* __restrict__ d, const int32_t* __restrict__ s, const flo
                    o);
 }
 
+// The paper's gate as a batched product on the matrix cores, for k <= 128:
+// H = ReLU(Z W1^T + b1) over the rows Z = d(b)[S'_o] of a block of 128
+// experts of one image, then g = H w2 + b2 and tau as above.  Z and W1 are
+// float32, split exactly into three bf16 parts each (hi + mid + lo, see
+// split3_pair); the
+// product keeps the six part products whose order is at most 2^-16 (hi hi,
+// hi mid, mid hi, hi lo, mid mid, lo hi), accumulated in float32 by
+// v_mfma_f32_16x16x32_bf16.  k is padded to KP (a multiple of 32) with zero
+// inputs, zero weights and zero w2 entries, which add nothing.  W1's parts
+// are staged in LDS once per workgroup, in rows of KP bf16 whose 16-byte
+// chunks are rotated so that the 16 rows one B-fragment read touches fall in
+// distinct bank groups; the workgroup then walks `nbi` images, restaging only
+// the image's descriptor row.  The softmax statistics follow with a group of
+// 8 lanes per expert, as in the softplus gate above.
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 gbf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float gf32x4;
+typedef unsigned int gu32x4 __attribute__((ext_vector_type(4)));
+constexpr int kMlpRows = 128;  // experts of one image per workgroup: 4 waves x 32
+constexpr int kMlpMaxK = 128;
+constexpr size_t kMlpMaxLds = 160 * 1024;  // per CU
+constexpr int kMlpRowRegs = 16;           // descriptor entries per thread: C < 16 x 256
+constexpr int64_t kMlpTargetBlocks = 256;
+
+int mlp_kp(int k) { return k <= 32 ? 32 : k <= 64 ? 64 : 128; }
+size_t mlp_lds_bytes(const Shape& sh) {
+  const size_t kp = (size_t)mlp_kp(sh.k);
+  return 3 * kp * kp * 2 + (size_t)kMlpRows * kp * 2 + (2 * kp + kMlpRows + 2 * ((size_t)sh.C + 1)) * sizeof(float);
+}
+
+// Two floats split exactly into three bf16 parts each, by truncation: the
+// top 16 bits of a float are a bf16 value (8 significant bits); the
+// remainder is exact and holds at most 16 significant bits, whose top 8 are
+// the second part and whose last 8 are the third, each exact in bf16.  The
+// parts come packed in pairs (first float low), one v_perm per pair.
+__device__ __forceinline__ void split3_pair(float f0, float f1, uint32_t& p0, uint32_t& p1, uint32_t& p2) {
+#pragma clang fp contract(off)
+  constexpr uint32_t kHi = 0xffff0000u, kSel = 0x07060302u;  // the high halves of (src1, src0)
+  const uint32_t u0 = __float_as_uint(f0), u1 = __float_as_uint(f1);
+  p0 = __builtin_amdgcn_perm(u1, u0, kSel);
+  const float r0 = f0 - __uint_as_float(u0 & kHi), r1 = f1 - __uint_as_float(u1 & kHi);
+  const uint32_t v0 = __float_as_uint(r0), v1 = __float_as_uint(r1);
+  p1 = __builtin_amdgcn_perm(v1, v0, kSel);
+  const float q0 = r0 - __uint_as_float(v0 & kHi), q1 = r1 - __uint_as_float(v1 & kHi);
+  p2 = __builtin_amdgcn_perm(__float_as_uint(q1), __float_as_uint(q0), kSel);
+}
+
+template <int KP>
+__global__ void __launch_bounds__(kGateWaves * kWave)
+k_gate_mlp_mfma(const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ w,
+                const float* __restrict__ W1, const float* __restrict__ b1, const float* __restrict__ w2, float b2,
+                float tau_min, float tau_max, float* __restrict__ tau, float* __restrict__ alpha, Stats st,
+                int64_t B, int C, int R, int k, int nblk, int nbi) {
+  static_assert(KP % 32 == 0 && KP <= kMlpMaxK, "K padded to whole 32-deep slices");
+  constexpr int kChunks = KP / 8;                       // 16-byte chunks of a W1 row
+  constexpr int kSh = KP == 128 ? 0 : KP == 64 ? 1 : 2;  // rows sharing a 256-byte bank span
+  constexpr int kPer = KP / 8;                          // logits per lane in the softmax (8 lanes an expert)
+  // LDS: W1's parts [3][KP][KP] bf16, the block's supports [kMlpRows][KP] as
+  // 16-bit channels (C marks a padding position), b1 and w2 [KP], the
+  // temperatures [kMlpRows], then the image's descriptor row [C + 1] whose
+  // entry C is 0
+  extern __shared__ float gsm[];
+  uint16_t* wl = reinterpret_cast<uint16_t*>(gsm);
+  uint16_t* sl16 = wl + 3 * KP * KP;
+  float* b1s = reinterpret_cast<float*>(sl16 + kMlpRows * KP);
+  float* w2s = b1s + KP;
+  float* taus = w2s + KP;
+  float* dr = taus + kMlpRows;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int n = lane & 15, gq = lane >> 4;
+  const int64_t b0 = (int64_t)(blockIdx.x / nblk) * nbi;
+  const int o0 = (blockIdx.x % nblk) * kMlpRows;
+  const int64_t b1e = min(b0 + nbi, B);
+  // element (j, i) of a part: chunk i / 8 of row j stored at chunk
+  // (i / 8) ^ ((j >> kSh) & (kChunks - 1))
+  auto wl_at = [&](int part, int j, int chunk) __attribute__((always_inline)) {
+    return wl + (part * KP + j) * KP + ((chunk ^ ((j >> kSh) & (kChunks - 1))) << 3);
+  };
+  // W1 by 8-wide chunks: every thread first reads all of its chunks, then
+  // splits and stores them
+  constexpr int kW1Per = (KP * kChunks + kGateWaves * kWave - 1) / (kGateWaves * kWave);
+  float wv8[kW1Per][8];
+#pragma unroll
+  for (int u = 0; u < kW1Per; ++u) {
+    const int idx = threadIdx.x + kGateWaves * kWave * u;
+    const int j = idx / kChunks, c8 = idx - j * kChunks;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = 8 * c8 + q;
+      // read unconditionally (clamped into W1) and then selected: a read
+      // under a lane condition would be waited for on its own
+      const float v = W1[(int64_t)min(j, k - 1) * k + min(i, k - 1)];
+      wv8[u][q] = idx < KP * kChunks && j < k && i < k ? v : 0.f;
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kW1Per; ++u) {
+    const int idx = threadIdx.x + kGateWaves * kWave * u;
+    if (idx >= KP * kChunks) continue;
+    const int j = idx / kChunks, c8 = idx - j * kChunks;
+    gu32x4 v0, v1, v2;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      uint32_t q0, q1, q2;
+      split3_pair(wv8[u][2 * h], wv8[u][2 * h + 1], q0, q1, q2);
+      v0[h] = q0;
+      v1[h] = q1;
+      v2[h] = q2;
+    }
+    *reinterpret_cast<gu32x4*>(wl_at(0, j, c8)) = v0;
+    *reinterpret_cast<gu32x4*>(wl_at(1, j, c8)) = v1;
+    *reinterpret_cast<gu32x4*>(wl_at(2, j, c8)) = v2;
+  }
+  // the block's supports, as 16-bit channels; padding positions and rows
+  // past R point at the zero entry C
+  // (all of a thread's reads issued before any is used)
+  constexpr int kSPer = kMlpRows * KP / (kGateWaves * kWave);
+  int32_t sv[kSPer];
+#pragma unroll
+  for (int u = 0; u < kSPer; ++u) {
+    const int idx = threadIdx.x + kGateWaves * kWave * u;
+    const int r = idx / KP, i = idx - r * KP;
+    sv[u] = s[(int64_t)min(o0 + r, R - 1) * k + min(i, k - 1)];
+  }
+#pragma unroll
+  for (int u = 0; u < kSPer; ++u) {
+    const int idx = threadIdx.x + kGateWaves * kWave * u;
+    const int r = idx / KP, i = idx - r * KP;
+    sl16[idx] = (uint16_t)(o0 + r < R && i < k ? sv[u] : C);
+  }
+  for (int j = threadIdx.x; j < KP; j += blockDim.x) {
+    const float v1 = b1[min(j, k - 1)], v2 = w2[min(j, k - 1)];
+    b1s[j] = j < k ? v1 : 0.f;
+    w2s[j] = j < k ? v2 : 0.f;
+  }
+  // this wave's 32 rows: blocks mb = 0, 1 of 16; lane (gq, n) builds the A
+  // fragment of row 32 wv + 16 mb + n, supports 32 sl + 8 gq .. + 7
+  // the logits of the wave's 32 experts for the softmax (8 lanes an
+  // expert, 8 experts a pass, 4 passes), held across the images with
+  // their maxima
+  const int h8 = lane & 7;
+  float wr[4][kPer], wmx[4];
+#pragma unroll
+  for (int pass = 0; pass < 4; ++pass) {
+    const int o = min(o0 + 32 * wv + 8 * pass + (lane >> 3), R - 1);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int i = h8 + 8 * t;
+      const float v = w[(int64_t)o * k + min(i, k - 1)];
+      wr[pass][t] = i < k ? v : -INFINITY;
+      mx = fmaxf(mx, wr[pass][t]);
+    }
+    wmx[pass] = row8_max(mx, lane);
+  }
+  // descriptor rows in two buffers of C + 1 floats (entry C is 0): image
+  // b + 1's row is read into registers while image b is formed
+  {
+    float v[kMlpRowRegs];
+#pragma unroll
+    for (int u = 0; u < kMlpRowRegs; ++u) v[u] = d[b0 * C + min((int)threadIdx.x + kGateWaves * kWave * u, C - 1)];
+#pragma unroll
+    for (int u = 0; u < kMlpRowRegs; ++u) {
+      const int c = threadIdx.x + kGateWaves * kWave * u;
+      if (c <= C) dr[c] = c < C ? v[u] : 0.f;
+    }
+  }
+  for (int64_t b = b0; b < b1e; ++b) {
+    const int cur = (int)((b - b0) & 1);
+    const float* drc = dr + cur * (C + 1);  // this image's row (LDS, indexed from the shared base)
+    __syncthreads();  // this image's row is in place; the previous image's reads of taus are done
+    float nxt[kMlpRowRegs];
+    const int64_t bn = b + 1 < b1e ? b + 1 : b;
+#pragma unroll
+    for (int u = 0; u < kMlpRowRegs; ++u) {
+      const int c = threadIdx.x + kGateWaves * kWave * u;
+      const float v = d[bn * C + min(c, C - 1)];
+      nxt[u] = c < C ? v : 0.f;
+    }
+    gf32x4 acc[2][KP / 16];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < KP / 16; ++nb) acc[mb][nb] = gf32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sl = 0; sl < KP / 32; ++sl) {
+      gbf16x8 a[2][3];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        const gu32x4 c8 =
+            *reinterpret_cast<const gu32x4*>(sl16 + (32 * wv + 16 * mb + n) * KP + 32 * sl + 8 * gq);
+        gu32x4 v0, v1, v2;
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          uint32_t q0, q1, q2;
+          split3_pair(drc[c8[h] & 0xffff], drc[c8[h] >> 16], q0, q1, q2);
+          v0[h] = q0;
+          v1[h] = q1;
+          v2[h] = q2;
+        }
+        a[mb][0] = __builtin_bit_cast(gbf16x8, v0);
+        a[mb][1] = __builtin_bit_cast(gbf16x8, v1);
+        a[mb][2] = __builtin_bit_cast(gbf16x8, v2);
+      }
+      // every B fragment of the slice first, then the six part products
+      // each over all 2 KP / 16 accumulators, so that consecutive products
+      // into one accumulator are that many MFMAs apart
+      gbf16x8 bf[KP / 16][3];
+#pragma unroll
+      for (int nb = 0; nb < KP / 16; ++nb)
+#pragma unroll
+        for (int pt = 0; pt < 3; ++pt)
+          bf[nb][pt] =
+              __builtin_bit_cast(gbf16x8, *reinterpret_cast<const gu32x4*>(wl_at(pt, 16 * nb + n, 4 * sl + gq)));
+      constexpr int kPa[6] = {2, 1, 0, 1, 0, 0}, kPb[6] = {0, 1, 2, 0, 1, 0};  // smallest terms first
+#pragma unroll
+      for (int t = 0; t < 6; ++t)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < KP / 16; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mb][kPa[t]], bf[nb][kPb[t]], acc[mb][nb], 0, 0, 0);
+    }
+    // lane (gq, n) holds H[16 mb + 4 gq + r][16 nb + n]: bias, ReLU, w2 and
+    // the sum over the hidden units (its 16 lanes hold the 16 columns)
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float gp = 0.f;
+#pragma unroll
+        for (int nb = 0; nb < KP / 16; ++nb)
+          gp += fmaxf(acc[mb][nb][r] + b1s[16 * nb + n], 0.f) * w2s[16 * nb + n];
+        gp = row16_sum(gp, lane) + b2;
+        if (n == 0) taus[32 * wv + 16 * mb + 4 * gq + r] = tau_min + (tau_max - tau_min) / (1.f + expf(-gp));
+      }
+    __syncthreads();
+    // softmax over each expert's logits
+#pragma unroll
+    for (int pass = 0; pass < 4; ++pass) {
+      const int row = 32 * wv + 8 * pass + (lane >> 3);
+      const int o_raw = o0 + row;
+      const int o = min(o_raw, R - 1);
+      const float tv = taus[row];
+      const float rt = 1.f / tv;
+      const float m = coef_z(wmx[pass], rt);
+      float z[kPer];
+      float zs = 0.f;
+#pragma unroll
+      for (int t = 0; t < kPer; ++t) {
+        z[t] = coef_e(coef_z(wr[pass][t], rt), m);
+        zs += z[t];
+      }
+      zs = row8_sum(zs, lane);
+      const float rzs = 1.f / zs;
+      if (o_raw < R) {
+        const int64_t item = b * R + o;
+        if (h8 == 0) tau[item] = tv;
+        if (alpha) {
+#pragma unroll
+          for (int t = 0; t < kPer; ++t)
+            if (h8 + 8 * t < k) alpha[item * k + h8 + 8 * t] = coef_alpha(z[t], rzs);
+        }
+        if (st.rt && h8 == 0) put_stats(st, b, o, rt, m, rzs);
+      }
+    }
+    // the next image's row into the other buffer (last read two images ago)
+    if (b + 1 < b1e) {
+      float* dn = dr + (1 - cur) * (C + 1);
+#pragma unroll
+      for (int u = 0; u < kMlpRowRegs; ++u) {
+        const int c = threadIdx.x + kGateWaves * kWave * u;
+        if (c <= C) dn[c] = nxt[u];
+      }
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const float* w,
@@ -493,6 +770,23 @@ hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const 
   } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR) {
     hipLaunchKernelGGL(k_gate_softplus, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
                        tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);
+  } else if (sh.k <= kMlpMaxK && mlp_lds_bytes(sh) <= kMlpMaxLds && sh.C < kMlpRowRegs * kGateWaves * kWave) {
+    // the batched product: 128 experts of an image per workgroup, nbi images
+    // each (W1 and the supports staged once), for about one workgroup per CU
+    const int nblk = (int)((sh.R + kMlpRows - 1) / kMlpRows);
+    const int64_t nbi = std::max<int64_t>(1, ((int64_t)nblk * sh.B + kMlpTargetBlocks - 1) / kMlpTargetBlocks);
+    const unsigned grid = (unsigned)(nblk * ((sh.B + nbi - 1) / nbi));
+    const int kp = mlp_kp(sh.k);
+    const size_t lds = mlp_lds_bytes(sh);
+    using K = void (*)(const float*, const int32_t*, const float*, const float*, const float*, const float*, float,
+                       float, float, float*, float*, Stats, int64_t, int, int, int, int, int);
+    const K kern = kp == 32 ? k_gate_mlp_mfma<32> : kp == 64 ? k_gate_mlp_mfma<64> : k_gate_mlp_mfma<128>;
+    if (lds > 64 * 1024) {
+      const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kGateWaves * kWave), lds, st, d, s, w, g.W1, g.b1, g.w2, g.b2,
+                       g.tau_min, g.tau_max, tau, alpha, sp, sh.B, (int)sh.C, sh.R, sh.k, nblk, (int)nbi);
   } else {
     hipLaunchKernelGGL(k_gate_mlp, dim3(blocks), dim3(kGateWaves * kWave), 0, st, d, s, w, g.W1, g.b1, g.w2,
                        g.b2, g.tau_min, g.tau_max, tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);

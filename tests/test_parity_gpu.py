@@ -193,6 +193,35 @@ def test_gate_mlp_isolated(name):
     check_tau_alpha(tau, tau_ref, alpha.cpu().numpy(), alpha_ref)
 
 
+@pytest.mark.parametrize("B,C,E,k", [
+    (301, 300, 257, 40),   # two 128-expert blocks, two images per workgroup, a ragged last group, k padded to 64
+    (7, 160, 130, 32),     # R = 129: a block with one expert
+    (3, 256, 9, 128),      # k = 128 exactly, one block of 8 experts
+    (2, 300, 5, 129),      # k > 128: the per-wave kernel
+    (1, 40, 2, 1),         # one routed expert, k = 1
+])
+def test_gate_mlp_shapes(B, C, E, k):
+    """The batched MLP gate against the oracle off the workload shapes: several images per
+    workgroup with a ragged last group, partial expert blocks, k padded to the next 32 and the
+    fallback beyond k = 128."""
+    rng = np.random.default_rng(B * 1000 + k)
+    R = E - 1
+    s = np.array([rng.choice(C, k, replace=False) for _ in range(R)], np.int32).reshape(R, k)
+    w = rng.standard_normal((R, k)).astype(np.float32)
+    W1 = (rng.standard_normal((k, k)) * k ** -0.5).astype(np.float32)
+    b1 = (rng.standard_normal(k) * 0.1).astype(np.float32)
+    w2 = (rng.standard_normal(k) * k ** -0.5).astype(np.float32)
+    b2, tmin, tmax = np.float32(0.25), np.float32(0.2), np.float32(6.0)
+    d = inputs.random_descriptor(B, C, seed=k + 11)
+    s_c, w_c, _, _, _ = oracle.prepare(C, E, s, w)
+    tau_ref = oracle.gate_mlp(d, s_c, W1, b1, w2, b2, tmin, tmax)
+    alpha_ref = oracle.softmax(w_c, tau_ref)
+    layer = MoceLayer(C, E, k, 1, 1, "f32", "nchw", s, w, gate="mlp", W1=W1, b1=b1, w2=w2, b2=float(b2),
+                      tau_min=float(tmin), tau_max=float(tmax))
+    tau, alpha = layer.gate_tau(torch.from_numpy(d).cuda())
+    check_tau_alpha(tau.cpu().numpy(), tau_ref, alpha.cpu().numpy(), alpha_ref)
+
+
 @pytest.mark.parametrize("name,layout", CASES)
 def test_mix_with_given_coefficients(name, layout):
     wl, g, ref = workload(name, layout)
