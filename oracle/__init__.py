@@ -57,6 +57,10 @@ def _load():
                                              ctypes.c_float, ctypes.c_float, P]
         lib.moce_oracle_softmax.argtypes = [I, I, I, P, P, P]
         lib.moce_oracle_mix.argtypes = [I, I, I, I, I, I, I, P, P, P, P, I, P, P]
+        lib.moce_oracle_router.argtypes = [I, I, I, P, P, P, P]
+        lib.moce_oracle_dynamic_logits.argtypes = [I, I, I, I, P, P, P, P, P]
+        lib.moce_oracle_topk.argtypes = [I, I, I, P, P, P]
+        lib.moce_oracle_dynamic_uncovered.argtypes = [I, I, I, I, P, P, P]
         lib.moce_oracle_threads.restype = I
         lib.moce_oracle_set_threads.argtypes = [I]
         _lib = lib
@@ -208,3 +212,95 @@ def forward(x: np.ndarray, s: np.ndarray, w: np.ndarray, E: int, layout: int = N
     y, mag = mix(x, s_c, alpha, U, E, layout)
     return {"s": s_c, "w": w_c, "covered": covered, "U": U, "nU": nU, "d": d, "tau": tau,
             "alpha": alpha, "y": y, "mag": mag}
+
+
+# ---------------------------------------------------------------------------
+# Input-conditioned (dynamic) support, Sec. 5 Eq. 11
+
+def router(d: np.ndarray, Wh, bh) -> np.ndarray:
+    """The router's bottleneck h = ReLU(Wh d + bh) per example, [B, dd] (float64)."""
+    d = _c(d, np.float64)
+    Wh = _c(Wh, np.float32)
+    bh = _c(bh, np.float32)
+    B, C = d.shape
+    dd = Wh.shape[0]
+    h = np.zeros((B, dd), np.float64)
+    _load().moce_oracle_router(B, C, dd, _ptr(d), _ptr(Wh), _ptr(bh), _ptr(h))
+    return h
+
+
+def dynamic_logits(h: np.ndarray, L, q, v) -> np.ndarray:
+    """Per-example routing logits L(X)[b, e, c] = L[e, c] + <q_e * h_b, v_c>, [B, E-1, C]."""
+    h = _c(h, np.float64)
+    L = _c(L, np.float32)
+    q = _c(q, np.float32)
+    v = _c(v, np.float32)
+    B, dd = h.shape
+    R, C = L.shape
+    Lx = np.zeros((B, R, C), np.float64)
+    _load().moce_oracle_dynamic_logits(B, C, R, dd, _ptr(h), _ptr(L), _ptr(q), _ptr(v), _ptr(Lx))
+    return Lx
+
+
+def topk(Lx: np.ndarray, k: int):
+    """The k largest entries of each row of the last axis, ties to the lower
+    channel, in canonical order: ``(S, W)`` with S the channels (int32) and W
+    their values."""
+    Lx = _c(Lx, np.float64)
+    C = Lx.shape[-1]
+    rows = int(np.prod(Lx.shape[:-1]))
+    S = np.zeros(Lx.shape[:-1] + (k,), np.int32)
+    W = np.zeros(Lx.shape[:-1] + (k,), np.float64)
+    _load().moce_oracle_topk(rows, C, k, _ptr(Lx), _ptr(S), _ptr(W))
+    return S, W
+
+
+def dynamic_uncovered(S: np.ndarray, C: int):
+    """Per example the channels in none of its supports: a list of B ascending arrays."""
+    S = _c(S, np.int32)
+    B, R, k = S.shape
+    U = np.zeros((B, max(C, 1)), np.int32)
+    nU = np.zeros(B, np.int32)
+    _load().moce_oracle_dynamic_uncovered(B, C, R, k, _ptr(S), _ptr(U), _ptr(nU))
+    return [U[b, :nU[b]].copy() for b in range(B)]
+
+
+def dynamic_forward(x: np.ndarray, L, Wh, bh, v, q, k: int, E: int, layout: int = NCHW,
+                    gate: str = "softplus", a=None, c=None, W1=None, b1=None, w2=None, b2=0.0,
+                    tau_min=0.2, tau_max=6.0, S=None, W=None) -> Dict[str, np.ndarray]:
+    """The layer with input-conditioned supports: GAP, router, per-example
+    logits, per-example TopK, and then per example the static layer's
+    temperature (from z at that example's support), softmax over the
+    example's logits at its support, mix and residual over U(X).
+
+    ``S``/``W`` (optional, [B, E-1, k]) replace the selection by a given one,
+    in canonical order, for checking a device selection that differs from this
+    one only on ties and near-ties."""
+    x = np.ascontiguousarray(x)
+    B, C, _ = _layout_dims(x, layout)
+    d = pool(x, layout)
+    h = router(d, Wh, bh)
+    Lx = dynamic_logits(h, L, q, v)
+    S_ref, W_ref = topk(Lx, k)
+    if S is None:
+        S, W = S_ref, W_ref
+    Ulist = dynamic_uncovered(S, C)
+    R = E - 1
+    yshape = (B, E) + x.shape[2:] if layout == NCHW else x.shape[:-1] + (E,)
+    y = np.zeros(yshape, np.float64)
+    mag = np.zeros(yshape, np.float64)
+    tau = np.zeros((B, R), np.float64)
+    alpha = np.zeros((B, R, k), np.float64)
+    for b in range(B):
+        db = d[b:b + 1]
+        if gate == "softplus":
+            tb = gate_softplus(db, S[b], a, c)
+        elif gate == "mlp":
+            tb = gate_mlp(db, S[b], W1, b1, w2, b2, tau_min, tau_max)
+        else:
+            raise ValueError(gate)
+        ab = softmax(W[b].astype(np.float32), tb)
+        yb, mb = mix(x[b:b + 1], S[b], ab, Ulist[b], E, layout)
+        y[b], mag[b], tau[b], alpha[b] = yb[0], mb[0], tb[0], ab[0]
+    return {"d": d, "h": h, "Lx": Lx, "S": S, "W": W, "S_ref": S_ref, "W_ref": W_ref, "U": Ulist,
+            "tau": tau, "alpha": alpha, "y": y, "mag": mag}

@@ -239,3 +239,78 @@ void moce_oracle_mix(int B, int C, int E, int k, int HW, int layout, int elem,
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Input-conditioned (dynamic) support (Sec. 5, Eq. 11)                     */
+
+/* h[b][t] = ReLU(bh[t] + sum_c Wh[t][c] d[b][c]), the router's bottleneck. */
+void moce_oracle_router(int B, int C, int dd, const double* d, const float* Wh,
+                        const float* bh, double* h) {
+    #pragma omp parallel for schedule(static)
+    for (int b = 0; b < B; ++b) {
+        for (int t = 0; t < dd; ++t) {
+            double acc = bh[t];
+            for (int c = 0; c < C; ++c) acc += (double)Wh[(size_t)t * C + c] * d[(size_t)b * C + c];
+            h[(size_t)b * dd + t] = acc > 0.0 ? acc : 0.0;
+        }
+    }
+}
+
+/* Lx[b][e][c] = L[e][c] + sum_t q[e][t] h[b][t] v[c][t]: the static routing
+ * logits plus the rank-dd offset of example b. */
+void moce_oracle_dynamic_logits(int B, int C, int R, int dd, const double* h, const float* L,
+                                const float* q, const float* v, double* Lx) {
+    #pragma omp parallel for schedule(static)
+    for (int b = 0; b < B; ++b) {
+        for (int e = 0; e < R; ++e) {
+            for (int c = 0; c < C; ++c) {
+                double off = 0.0;
+                for (int t = 0; t < dd; ++t)
+                    off += (double)q[(size_t)e * dd + t] * h[(size_t)b * dd + t] * (double)v[(size_t)c * dd + t];
+                Lx[((size_t)b * R + e) * C + c] = (double)L[(size_t)e * C + c] + off;
+            }
+        }
+    }
+}
+
+/* a precedes b: larger logit first, then lower channel */
+static int comes_before_d(double wa, int32_t sa, double wb, int32_t sb) {
+    if (wa > wb) return 1;
+    if (wa < wb) return 0;
+    return sa < sb;
+}
+
+/* Per row of C logits: the k largest (ties to the lower channel), in the
+ * canonical order; S gets their channels and W their logits.  Selection by
+ * k passes of "the first not yet taken" (plain, O(k C) per row). */
+void moce_oracle_topk(int rows, int C, int k, const double* Lx, int32_t* S, double* W) {
+    #pragma omp parallel for schedule(static)
+    for (int r = 0; r < rows; ++r) {
+        const double* row = Lx + (size_t)r * C;
+        unsigned char* taken = (unsigned char*)calloc((size_t)C, 1);
+        for (int i = 0; i < k; ++i) {
+            int best = -1;
+            for (int c = 0; c < C; ++c)
+                if (!taken[c] && (best < 0 || comes_before_d(row[c], c, row[best], best))) best = c;
+            taken[best] = 1;
+            S[(size_t)r * k + i] = best;
+            W[(size_t)r * k + i] = row[best];
+        }
+        free(taken);
+    }
+}
+
+/* Per example: U(X) = the channels in no support of that example, ascending;
+ * U[b][0 .. nU[b]-1]. */
+void moce_oracle_dynamic_uncovered(int B, int C, int R, int k, const int32_t* S, int32_t* U, int32_t* nU) {
+    #pragma omp parallel for schedule(static)
+    for (int b = 0; b < B; ++b) {
+        unsigned char* cov = (unsigned char*)calloc((size_t)C, 1);
+        for (size_t j = 0; j < (size_t)R * k; ++j) cov[S[(size_t)b * R * k + j]] = 1;
+        int n = 0;
+        for (int c = 0; c < C; ++c)
+            if (!cov[c]) U[(size_t)b * C + n++] = c;
+        nU[b] = n;
+        free(cov);
+    }
+}

@@ -67,6 +67,20 @@ void moce_oracle_mix(int B, int C, int E, int k, int HW, int layout, int elem,
 int moce_oracle_threads(void);
 void moce_oracle_set_threads(int n);
 
+
+/* Input-conditioned support (Sec. 5, Eq. 11).  The router's bottleneck
+ * h[B][dd] = ReLU(Wh d + bh) from the descriptor d[B][C]; the example's
+ * routing logits Lx[B][R][C] = L[R][C] + ((q[e] * h[b]) . v[c]); per row the k
+ * largest logits in canonical order (ties to the lower channel) as channels
+ * S[rows][k] and logits W[rows][k]; per example the uncovered channels
+ * U[B][C] (first nU[b] entries, ascending). */
+void moce_oracle_router(int B, int C, int dd, const double* d, const float* Wh,
+                        const float* bh, double* h);
+void moce_oracle_dynamic_logits(int B, int C, int R, int dd, const double* h, const float* L,
+                                const float* q, const float* v, double* Lx);
+void moce_oracle_topk(int rows, int C, int k, const double* Lx, int32_t* S, double* W);
+void moce_oracle_dynamic_uncovered(int B, int C, int R, int k, const int32_t* S, int32_t* U, int32_t* nU);
+
 #ifdef __cplusplus
 }
 #endif

@@ -438,3 +438,127 @@ def test_mag_of_empty_residual_is_zero():
     al = oracle.softmax(w_c, np.ones((B, E - 1)))
     y, mag = oracle.mix(x, s_c, al, U, E, oracle.NCHW)
     assert np.all(mag[:, E - 1] == 0.0) and np.all(y[:, E - 1] == 0.0)
+
+
+# --------------------------------------------------------------------------- input-conditioned supports
+# Sec. 5 Eq. 11: h = ReLU(Wh z + bh), L(X)_{e,c} = L_{e,c} + <q_e * h, v_c>, S_e(X) = TopK(L(X)_e, k),
+# U(X) the channels in no S_e(X); temperature and coefficients then follow the example's support.
+
+def _router_case(B=3, C=40, E=7, dd=5, seed=0):
+    rng = np.random.default_rng(seed)
+    d = rng.standard_normal((B, C))
+    L = rng.standard_normal((E - 1, C)).astype(np.float32)
+    Wh = rng.standard_normal((dd, C)).astype(np.float32)
+    bh = rng.standard_normal(dd).astype(np.float32)
+    v = rng.standard_normal((C, dd)).astype(np.float32)
+    q = rng.standard_normal((E - 1, dd)).astype(np.float32)
+    return d, L, Wh, bh, v, q
+
+
+def test_router_identity_weights_is_relu_of_descriptor():
+    """Wh selecting the first dd channels and bh = 0: h = max(0, z[:dd]) exactly."""
+    d, _, _, _, _, _ = _router_case()
+    dd, C = 5, d.shape[1]
+    Wh = np.zeros((dd, C), np.float32)
+    Wh[np.arange(dd), np.arange(dd)] = 1
+    h = oracle.router(d, Wh, np.zeros(dd, np.float32))
+    np.testing.assert_array_equal(h, np.maximum(d[:, :dd], 0))
+
+
+def test_router_matches_numpy_affine_relu():
+    d, _, Wh, bh, _, _ = _router_case(seed=1)
+    h = oracle.router(d, Wh, bh)
+    ref = np.maximum(d @ Wh.astype(np.float64).T + bh.astype(np.float64), 0)
+    np.testing.assert_allclose(h, ref, rtol=1e-12, atol=1e-12)
+    assert (h == 0).any() and (h > 0).any()
+
+
+def test_dynamic_logits_match_einsum_and_have_rank_dd():
+    d, L, Wh, bh, v, q = _router_case(seed=2)
+    h = oracle.router(d, Wh, bh)
+    Lx = oracle.dynamic_logits(h, L, q, v)
+    ref = L.astype(np.float64)[None] + np.einsum("bt,et,ct->bec", h, q.astype(np.float64), v.astype(np.float64))
+    np.testing.assert_allclose(Lx, ref, rtol=1e-12, atol=1e-12)
+    for b in range(d.shape[0]):
+        assert np.linalg.matrix_rank(Lx[b] - L.astype(np.float64), tol=1e-9) <= v.shape[1]
+
+
+def test_dynamic_logits_closed_forms():
+    """q = 0 leaves the static logits; dd = 1 with q = 1, v_c = c adds h * c to column c."""
+    d, L, Wh, bh, v, q = _router_case(seed=3)
+    h = oracle.router(d, Wh, bh)
+    np.testing.assert_array_equal(oracle.dynamic_logits(h, L, np.zeros_like(q), v), np.broadcast_to(
+        L.astype(np.float64), (d.shape[0],) + L.shape))
+    C = L.shape[1]
+    h1 = np.array([[0.5], [2.0]])
+    Lx = oracle.dynamic_logits(h1, L, np.ones((L.shape[0], 1), np.float32),
+                               np.arange(C, dtype=np.float32)[:, None])
+    np.testing.assert_allclose(Lx, L.astype(np.float64)[None] + h1[:, :, None] * np.arange(C)[None, None, :],
+                               rtol=0, atol=1e-12)
+
+
+def test_topk_against_stable_sort_with_ties():
+    rng = np.random.default_rng(4)
+    Lx = rng.integers(-3, 4, size=(5, 37)).astype(np.float64)   # many ties
+    Lx[0] = 1.0                                                  # all equal: channels 0 .. k-1
+    k = 9
+    S, W = oracle.topk(Lx, k)
+    for r in range(Lx.shape[0]):
+        order = np.lexsort((np.arange(Lx.shape[1]), -Lx[r]))    # value descending, then channel ascending
+        np.testing.assert_array_equal(S[r], order[:k])
+        np.testing.assert_array_equal(W[r], Lx[r, order[:k]])
+    np.testing.assert_array_equal(S[0], np.arange(k))
+
+
+def test_dynamic_uncovered_partitions_channels():
+    rng = np.random.default_rng(5)
+    B, R, k, C = 4, 6, 3, 30
+    S = np.stack([np.stack([rng.choice(C, k, replace=False) for _ in range(R)]) for _ in range(B)]).astype(np.int32)
+    U = oracle.dynamic_uncovered(S, C)
+    for b in range(B):
+        covered = set(S[b].ravel().tolist())
+        assert set(U[b].tolist()) == set(range(C)) - covered
+        assert list(U[b]) == sorted(U[b])
+
+
+@pytest.mark.parametrize("layout", [oracle.NCHW, oracle.NHWC])
+def test_dynamic_forward_without_offset_is_the_static_layer(layout):
+    """q = 0: every example's support is TopK of the static logits, so the layer is the static
+    layer with s = TopK(L) and w = L at s (the static path is pinned on its own)."""
+    rng = np.random.default_rng(6)
+    B, C, E, k, dd, H, W = 2, 20, 5, 4, 3, 3, 4
+    x = rng.standard_normal((B, C, H, W) if layout == oracle.NCHW else (B, H, W, C)).astype(np.float32)
+    L = rng.standard_normal((E - 1, C)).astype(np.float32)
+    Wh = rng.standard_normal((dd, C)).astype(np.float32)
+    bh = rng.standard_normal(dd).astype(np.float32)
+    v = rng.standard_normal((C, dd)).astype(np.float32)
+    a = rng.standard_normal((E - 1, k)).astype(np.float32)
+    c = rng.standard_normal(E - 1).astype(np.float32)
+    dyn = oracle.dynamic_forward(x, L, Wh, bh, v, np.zeros((E - 1, dd), np.float32), k, E, layout, a=a, c=c)
+    s = np.argsort(-L, axis=1, kind="stable")[:, :k].astype(np.int32)
+    w = np.take_along_axis(L, s, axis=1)
+    ref = oracle.forward(x, s, w, E, layout, a=a, c=c)
+    np.testing.assert_allclose(dyn["y"], ref["y"], rtol=1e-12, atol=1e-12)
+    for b in range(B):
+        np.testing.assert_array_equal(dyn["U"][b], ref["U"])
+
+
+def test_dynamic_forward_follows_the_example_support():
+    """With a strong offset the examples pick different supports; each example's output is then
+    the static layer evaluated with that example's support and logits."""
+    rng = np.random.default_rng(7)
+    B, C, E, k, dd = 3, 24, 6, 5, 4
+    x = rng.standard_normal((B, C, 2, 5)).astype(np.float32)
+    L = rng.standard_normal((E - 1, C)).astype(np.float32) * 0.1
+    Wh = rng.standard_normal((dd, C)).astype(np.float32)
+    bh = np.full(dd, 1.0, np.float32)
+    v = rng.standard_normal((C, dd)).astype(np.float32) * 3
+    q = rng.standard_normal((E - 1, dd)).astype(np.float32)
+    a = rng.standard_normal((E - 1, k)).astype(np.float32)
+    c = rng.standard_normal(E - 1).astype(np.float32)
+    dyn = oracle.dynamic_forward(x, L, Wh, bh, v, q, k, E, oracle.NCHW, a=a, c=c)
+    assert any(not np.array_equal(dyn["S"][0], dyn["S"][b]) for b in range(1, B))
+    for b in range(B):
+        ref = oracle.forward(x[b:b + 1], dyn["S"][b], dyn["W"][b].astype(np.float32), E, oracle.NCHW, a=a, c=c)
+        np.testing.assert_allclose(dyn["y"][b:b + 1], ref["y"], rtol=1e-12, atol=1e-12)
+        np.testing.assert_array_equal(dyn["U"][b], ref["U"])
