@@ -214,6 +214,46 @@ moce_status moce_forward_static(const moce_desc* desc, const void* x, const int3
                                 const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
                                 hipStream_t stream);
 
+/* Router of the input-conditioned support variant (Sec. 5 Eq. 11).  From the
+ * pooled descriptor z of an example, h = ReLU(Wh z + bh) (d values), and the
+ * example's routing logits are L(X)[e][c] = L[e][c] + sum_t q[e][t] h[t] v[c][t]
+ * over the full static routing logits L[E-1][C]. */
+typedef struct moce_router {
+    int32_t d;            /* bottleneck width, 1 <= d <= 64 */
+    int32_t reserved;     /* set to 0 */
+    const float* Wh;      /* [d][C] */
+    const float* bh;      /* [d] */
+    const float* v;       /* [C][d] channel embeddings */
+    const float* q;       /* [E-1][d] expert embeddings */
+} moce_router;
+
+/* Bytes of device workspace moce_forward_dynamic needs (0 on an invalid
+ * descriptor or router width). */
+size_t moce_forward_dynamic_workspace_bytes(const moce_desc* desc, int32_t d);
+
+/* The layer with input-conditioned supports (Sec. 5 Eq. 11), inference path.
+ * Per example b: z = GAP(x_b); L(X) as above; S_e(X) = the k channels of
+ * largest L(X)[e][.], equal logits by ascending channel, in canonical order
+ * (logit descending, then channel ascending); the gate reads z at S_e(X) in
+ * that order (gate position i is the i-th channel of S_e(X)); the
+ * coefficients are the softmax of L(X)[e][S_e(X)] over the temperature; the
+ * residual output E-1 is the mean of x over U(X), the channels in no
+ * S_e(X) of that example (0 when U(X) is empty).
+ *
+ * x, y as for moce_forward (16-byte aligned, y fully overwritten);
+ * L: [E-1][C] float32 device; router: host struct of device pointers;
+ * gate: as for moce_forward (gate->a indexed by canonical position);
+ * S_out: optional device [B][E-1][k] int32 receiving S_e(X) (NULL: not
+ * written); ws: device workspace of at least
+ * moce_forward_dynamic_workspace_bytes(desc, router->d) bytes, 256-byte
+ * aligned, contents on return unspecified.
+ * Errors: those of moce_forward; MOCE_ERR_NULL for a missing L, router or
+ * router array; MOCE_ERR_UNSUPPORTED when d > 64, k > 512 or C > 4096.
+ * Asynchronous on `stream`. */
+moce_status moce_forward_dynamic(const moce_desc* desc, const void* x, const float* L, const moce_router* router,
+                                 const moce_gate_params* gate, void* y, int32_t* S_out, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
 /* Static string naming a status code. */
 const char* moce_status_str(int status);
 

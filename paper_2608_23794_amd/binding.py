@@ -30,7 +30,7 @@ STATUS = {
 ENTRY_POINTS = (
     "moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix",
     "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_forward_static",
-    "moce_status_str", "moce_abi_version",
+    "moce_forward_dynamic_workspace_bytes", "moce_forward_dynamic", "moce_status_str", "moce_abi_version",
 )
 
 MOCE_STATIC_SCRATCH_BYTES = 16 << 20
@@ -47,6 +47,11 @@ class moce_desc(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int64), ("C", ctypes.c_int64), ("H", ctypes.c_int64), ("W", ctypes.c_int64),
                 ("E", ctypes.c_int32), ("k", ctypes.c_int32), ("x_dtype", ctypes.c_int32),
                 ("y_dtype", ctypes.c_int32), ("layout", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class moce_router(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("reserved", ctypes.c_int32), ("Wh", ctypes.c_void_p),
+                ("bh", ctypes.c_void_p), ("v", ctypes.c_void_p), ("q", ctypes.c_void_p)]
 
 
 class moce_gate_params(ctypes.Structure):
@@ -83,11 +88,14 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_forward_path.argtypes = [D, ctypes.c_int]
     lib.moce_forward.argtypes = [D, P, P, P, G, P, I32, P, P, SZ, P]
     lib.moce_forward_static.argtypes = [D, P, P, P, G, P, I32, P, P]
+    lib.moce_forward_dynamic_workspace_bytes.argtypes = [D, I32]
+    lib.moce_forward_dynamic_workspace_bytes.restype = SZ
+    lib.moce_forward_dynamic.argtypes = [D, P, P, ctypes.POINTER(moce_router), G, P, P, P, SZ, P]
     lib.moce_status_str.argtypes = [ctypes.c_int]
     lib.moce_status_str.restype = ctypes.c_char_p
     lib.moce_abi_version.restype = ctypes.c_int
     for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward",
-                 "moce_forward_static"):
+                 "moce_forward_static", "moce_forward_dynamic"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -189,6 +197,22 @@ def moce_forward_static(desc: moce_desc, x, s, w, gate: moce_gate_params, U, nU:
     _check("moce_forward_static", load().moce_forward_static(ctypes.byref(desc), _ptr(x), _ptr(s), _ptr(w),
                                                              ctypes.byref(gate), _ptr(U), nU, _ptr(y),
                                                              _stream(stream)))
+
+
+def make_router(d: int, Wh, bh, v, q) -> moce_router:
+    """A router struct over device arrays (they must outlive its use)."""
+    return moce_router(int(d), 0, _ptr(Wh), _ptr(bh), _ptr(v), _ptr(q))
+
+
+def moce_forward_dynamic_workspace_bytes(desc: moce_desc, d: int) -> int:
+    return int(load().moce_forward_dynamic_workspace_bytes(ctypes.byref(desc), int(d)))
+
+
+def moce_forward_dynamic(desc: moce_desc, x, L, router: moce_router, gate: moce_gate_params, y, S_out, ws,
+                         ws_bytes: int, stream=None) -> None:
+    _check("moce_forward_dynamic", load().moce_forward_dynamic(ctypes.byref(desc), _ptr(x), _ptr(L),
+                                                               ctypes.byref(router), ctypes.byref(gate), _ptr(y),
+                                                               _ptr(S_out), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def raw_status(fn: str, *args) -> int:

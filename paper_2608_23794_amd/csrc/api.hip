@@ -335,4 +335,67 @@ moce_status moce_forward_static(const moce_desc* desc, const void* x, const int3
   return forward_launch(sh, x, s, w, gate, U, nU, y, ws, stream);
 }
 
+// ---- input-conditioned supports ------------------------------------------
+
+namespace {
+
+// Dynamic forward workspace: d [B][C], h [B][d], S [B][R][k], W [B][R][k],
+// U [B][C], nU [B], tau [B][R], alpha [B][R][k]; 256-byte aligned regions.
+struct DynLayout {
+  size_t d, h, S, W, U, nU, tau, alpha, total;
+};
+DynLayout dyn_layout(const Shape& sh, int dd) {
+  DynLayout l{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += round_up(bytes);
+    return at;
+  };
+  const size_t brk = (size_t)sh.B * sh.R * sh.k;
+  l.d = take((size_t)sh.B * sh.C * sizeof(float));
+  l.h = take((size_t)sh.B * dd * sizeof(float));
+  l.S = take(brk * sizeof(int32_t));
+  l.W = take(brk * sizeof(float));
+  l.U = take((size_t)sh.B * sh.C * sizeof(int32_t));
+  l.nU = take((size_t)sh.B * sizeof(int32_t));
+  l.tau = take((size_t)sh.B * sh.R * sizeof(float));
+  l.alpha = take(brk * sizeof(float));
+  l.total = off;
+  return l;
+}
+
+}  // namespace
+
+size_t moce_forward_dynamic_workspace_bytes(const moce_desc* desc, int32_t d) {
+  Shape sh;
+  if (check_desc(desc, &sh) != MOCE_OK || d < 1 || !moce::dynamic_supported(sh, d)) return 0;
+  return dyn_layout(sh, d).total;
+}
+
+moce_status moce_forward_dynamic(const moce_desc* desc, const void* x, const float* L, const moce_router* router,
+                                 const moce_gate_params* gate, void* y, int32_t* S_out, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  Shape sh;
+  moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  st = check_gate(sh, gate);
+  if (st != MOCE_OK) return st;
+  if (!x || !y || !router) return MOCE_ERR_NULL;
+  if (router->d < 1) return MOCE_ERR_SHAPE;
+  if (sh.R > 0 && (!L || !router->Wh || !router->bh || !router->v || !router->q)) return MOCE_ERR_NULL;
+  if (!moce::dynamic_supported(sh, router->d)) return MOCE_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(y, 16)) return MOCE_ERR_ALIGN;
+  const DynLayout l = dyn_layout(sh, router->d);
+  if (!ws || ws_bytes < l.total) return MOCE_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return MOCE_ERR_ALIGN;
+  char* base = static_cast<char*>(ws);
+  int32_t* S = S_out ? S_out : reinterpret_cast<int32_t*>(base + l.S);
+  return device_status(moce::launch_dynamic(
+      sh, x, L, *router, *gate, y, reinterpret_cast<float*>(base + l.d), reinterpret_cast<float*>(base + l.h), S,
+      reinterpret_cast<float*>(base + l.W), reinterpret_cast<int32_t*>(base + l.U),
+      reinterpret_cast<int32_t*>(base + l.nU), reinterpret_cast<float*>(base + l.tau),
+      reinterpret_cast<float*>(base + l.alpha), stream));
+}
+
 }  // extern "C"

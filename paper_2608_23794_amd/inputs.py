@@ -195,6 +195,25 @@ def generate(wl: Workload, layout: Optional[str] = None, with_x: bool = True,
     return out
 
 
+def router_params(wl: Workload, d: int = 32) -> Dict[str, np.ndarray]:
+    """Synthetic parameters of the input-conditioned variant (Sec. 5 Eq. 11)
+    for ``wl``: the full static routing logits ``L[E-1, C] ~ N(0, 1)`` and the
+    router ``Wh[d, C] ~ N(0, 4/C)``, ``bh[d] ~ N(0, 0.1^2)``, channel
+    embeddings ``v[C, d] ~ N(0, 1)`` and expert embeddings
+    ``q[E-1, d] ~ N(0, 1/d)`` (float32), scaled so that the per-example
+    offset is of the order of the logits' spread and the examples' supports
+    differ."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([wl.seed, 11])))
+    R, C = wl.n_routed, wl.C
+    return {
+        "L": rng.standard_normal((R, C), dtype=np.float32),
+        "Wh": (rng.standard_normal((d, C), dtype=np.float32) * np.float32(2.0 / np.sqrt(C))).astype(np.float32),
+        "bh": (rng.standard_normal(d, dtype=np.float32) * np.float32(0.1)).astype(np.float32),
+        "v": rng.standard_normal((C, d), dtype=np.float32),
+        "q": (rng.standard_normal((R, d), dtype=np.float32) * np.float32(1.0 / np.sqrt(d))).astype(np.float32),
+    }
+
+
 def random_descriptor(B: int, C: int, seed: int, signed: bool = False) -> np.ndarray:
     """A synthetic per-(image, channel) descriptor for testing the gate alone."""
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 7])))

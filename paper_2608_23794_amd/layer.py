@@ -148,6 +148,71 @@ class MoceLayer:
         return y
 
 
+class DynamicMoceLayer:
+    """The layer with input-conditioned supports (Sec. 5 Eq. 11): device
+    copies of the full routing logits, the router and the gate, and the
+    library's dynamic forward over them."""
+
+    def __init__(self, C: int, E: int, k: int, H: int, W: int, dtype: str, layout: str, L, Wh, bh, v, q,
+                 gate: str = "softplus", a=None, c=None, W1=None, b1=None, w2=None, b2: float = 0.0,
+                 tau_min: float = 0.2, tau_max: float = 6.0, device: str = "cuda"):
+        self.C, self.E, self.k, self.H, self.W = C, E, k, H, W
+        self.R = R = E - 1
+        self.dtype, self.layout, self.device = dtype, layout, device
+        f32 = torch.float32
+        self.dd = int(np.asarray(Wh).shape[0])
+        self.L = _dev(np.asarray(L, np.float32).reshape(R, C), f32, device)
+        self.Wh = _dev(np.asarray(Wh, np.float32).reshape(self.dd, C), f32, device)
+        self.bh = _dev(np.asarray(bh, np.float32).reshape(self.dd), f32, device)
+        self.v = _dev(np.asarray(v, np.float32).reshape(C, self.dd), f32, device)
+        self.q = _dev(np.asarray(q, np.float32).reshape(R, self.dd), f32, device)
+        self.router = mb.make_router(self.dd, self.Wh, self.bh, self.v, self.q)
+        if gate == "softplus":
+            self.a = _dev(np.asarray(a, np.float32).reshape(R, k), f32, device)
+            self.c = _dev(np.asarray(c, np.float32).reshape(R), f32, device)
+            self.gate = mb.make_gate(mb.MOCE_GATE_SOFTPLUS_LINEAR, a=self.a, c=self.c)
+        elif gate == "mlp":
+            self.W1 = _dev(np.asarray(W1, np.float32).reshape(k, k), f32, device)
+            self.b1 = _dev(np.asarray(b1, np.float32).reshape(k), f32, device)
+            self.w2 = _dev(np.asarray(w2, np.float32).reshape(k), f32, device)
+            self.gate = mb.make_gate(mb.MOCE_GATE_MLP_SIGMOID, W1=self.W1, b1=self.b1, w2=self.w2,
+                                     b2=float(b2), tau_min=float(tau_min), tau_max=float(tau_max))
+        else:
+            raise ValueError(gate)
+
+    @classmethod
+    def from_workload(cls, wl, params: dict, router: dict, layout: Optional[str] = None, gate: str = "softplus",
+                      device: str = "cuda") -> "DynamicMoceLayer":
+        return cls(wl.C, wl.E, wl.k, wl.H, wl.W, wl.dtype, layout or wl.layouts[0], router["L"], router["Wh"],
+                   router["bh"], router["v"], router["q"], gate=gate, a=params.get("a"), c=params.get("c"),
+                   W1=params.get("W1"), b1=params.get("b1"), w2=params.get("w2"), b2=float(params.get("b2", 0.0)),
+                   tau_min=float(params.get("tau_min", 0.2)), tau_max=float(params.get("tau_max", 6.0)),
+                   device=device)
+
+    def desc(self, B: int) -> mb.moce_desc:
+        return mb.make_desc(B, self.C, self.H, self.W, self.E, self.k, _DT[self.dtype], _LAYOUT[self.layout])
+
+    def y_shape(self, B: int):
+        return (B, self.E, self.H, self.W) if self.layout == "nchw" else (B, self.H, self.W, self.E)
+
+    def workspace_bytes(self, B: int) -> int:
+        return mb.moce_forward_dynamic_workspace_bytes(self.desc(B), self.dd)
+
+    def new_workspace(self, B: int) -> torch.Tensor:
+        return torch.empty(max(self.workspace_bytes(B), 1), dtype=torch.uint8, device=self.device)
+
+    def forward(self, x: torch.Tensor, y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                S_out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        B = x.shape[0]
+        if y is None:
+            y = torch.empty(self.y_shape(B), dtype=x.dtype, device=self.device)
+        if ws is None:
+            ws = self.new_workspace(B)
+        mb.moce_forward_dynamic(self.desc(B), x, self.L, self.router, self.gate, y, S_out, ws, ws.numel(),
+                                torch.cuda.current_stream())
+        return y
+
+
 def to_device_x(x: np.ndarray, dtype: str, device: str = "cuda") -> torch.Tensor:
     """Uploads f32 values or bf16 bit patterns (uint16) as a float32/bfloat16 tensor."""
     if dtype == "f32":

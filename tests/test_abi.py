@@ -242,3 +242,42 @@ def test_forward_static_host_errors(lib):
     big = good_desc(B=64, C=4096, E=4096, k=64, H=2, W=2)
     assert lib.moce_forward_workspace_bytes(ctypes.byref(big)) > mb.MOCE_STATIC_SCRATCH_BYTES
     assert _call_static(big, gate) == -7
+
+
+def _call_dynamic(desc, gate, router, x=FAKE, L=FAKE, y=FAKE, S_out=None, ws=FAKE, ws_bytes=1 << 30):
+    r = ctypes.byref(router) if router is not None else None
+    return mb.raw_status("moce_forward_dynamic", ctypes.byref(desc), x, L, r, ctypes.byref(gate), y, S_out, ws,
+                         ws_bytes, None)
+
+
+def test_forward_dynamic_host_errors(lib):
+    """Every host-side check of the input-conditioned forward returns before any launch (all the
+    addresses here are placeholders that are never dereferenced)."""
+    desc = good_desc()
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+    router = mb.moce_router(8, 0, FAKE, FAKE, FAKE, FAKE)
+    assert _call_dynamic(desc, gate, None) == -1
+    assert _call_dynamic(desc, gate, router, L=None) == -1
+    assert _call_dynamic(desc, gate, mb.moce_router(8, 0, FAKE, None, FAKE, FAKE)) == -1
+    assert _call_dynamic(desc, gate, mb.moce_router(0, 0, FAKE, FAKE, FAKE, FAKE)) == -2
+    assert _call_dynamic(desc, gate, mb.moce_router(65, 0, FAKE, FAKE, FAKE, FAKE)) == -10
+    assert _call_dynamic(good_desc(C=5000, k=8), gate, router) == -10
+    assert _call_dynamic(good_desc(C=1024, k=600), gate, router) == -10
+    assert _call_dynamic(desc, gate, router, x=FAKE_UNALIGNED) == -8
+    assert _call_dynamic(desc, gate, router, ws=None) == -7
+    need = lib.moce_forward_dynamic_workspace_bytes(ctypes.byref(desc), 8)
+    assert need > 0
+    assert _call_dynamic(desc, gate, router, ws_bytes=need - 1) == -7
+    assert _call_dynamic(desc, gate, router, ws=FAKE_UNALIGNED, ws_bytes=need) == -8
+    assert lib.moce_forward_dynamic_workspace_bytes(ctypes.byref(desc), 65) == 0
+
+
+def test_forward_dynamic_workspace_layout(lib):
+    """d [B][C], h [B][d], supports and their logits [B][E-1][k], U [B][C], nU [B], tau [B][E-1] and the
+    coefficients [B][E-1][k], each rounded up to 256 bytes."""
+    desc = good_desc()
+    B, C, R, k, d = desc.B, desc.C, desc.E - 1, desc.k, 8
+    r = lambda n: (n + 255) // 256 * 256
+    expect = (r(B * C * 4) + r(B * d * 4) + 2 * r(B * R * k * 4) + r(B * C * 4) + r(B * 4) + r(B * R * 4)
+              + r(B * R * k * 4))
+    assert lib.moce_forward_dynamic_workspace_bytes(ctypes.byref(desc), d) == expect
