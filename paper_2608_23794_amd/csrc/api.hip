@@ -339,10 +339,11 @@ moce_status moce_forward_static(const moce_desc* desc, const void* x, const int3
 
 namespace {
 
-// Dynamic forward workspace: d [B][C], h [B][d], S [B][R][k], W [B][R][k],
-// U [B][C], nU [B], tau [B][R], alpha [B][R][k]; 256-byte aligned regions.
+// Dynamic forward workspace: d [B][C], h [B][d], vT [d][C], S [B][R][k],
+// W [B][R][k], U [B][C], nU [B], tau [B][R], alpha [B][R][k]; 256-byte
+// aligned regions.
 struct DynLayout {
-  size_t d, h, S, W, U, nU, tau, alpha, total;
+  size_t d, h, vT, S, W, U, nU, tau, alpha, total;
 };
 DynLayout dyn_layout(const Shape& sh, int dd) {
   DynLayout l{};
@@ -355,6 +356,7 @@ DynLayout dyn_layout(const Shape& sh, int dd) {
   const size_t brk = (size_t)sh.B * sh.R * sh.k;
   l.d = take((size_t)sh.B * sh.C * sizeof(float));
   l.h = take((size_t)sh.B * dd * sizeof(float));
+  l.vT = take((size_t)dd * sh.C * sizeof(float));
   l.S = take(brk * sizeof(int32_t));
   l.W = take(brk * sizeof(float));
   l.U = take((size_t)sh.B * sh.C * sizeof(int32_t));
@@ -392,7 +394,8 @@ moce_status moce_forward_dynamic(const moce_desc* desc, const void* x, const flo
   char* base = static_cast<char*>(ws);
   int32_t* S = S_out ? S_out : reinterpret_cast<int32_t*>(base + l.S);
   return device_status(moce::launch_dynamic(
-      sh, x, L, *router, *gate, y, reinterpret_cast<float*>(base + l.d), reinterpret_cast<float*>(base + l.h), S,
+      sh, x, L, *router, *gate, y, reinterpret_cast<float*>(base + l.d), reinterpret_cast<float*>(base + l.h),
+      reinterpret_cast<float*>(base + l.vT), S,
       reinterpret_cast<float*>(base + l.W), reinterpret_cast<int32_t*>(base + l.U),
       reinterpret_cast<int32_t*>(base + l.nU), reinterpret_cast<float*>(base + l.tau),
       reinterpret_cast<float*>(base + l.alpha), stream));

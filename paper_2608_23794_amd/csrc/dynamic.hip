@@ -47,6 +47,18 @@ k_dyn_router(const float* __restrict__ d, const float* __restrict__ Wh, const fl
   if (lane == 0) h[wave] = fmaxf(acc + bh[t], 0.f);
 }
 
+// vT[t][c] = v[c][t]: the channel embeddings transposed, 32 x 32 tiles
+// through LDS
+__global__ void __launch_bounds__(1024)
+k_dyn_transpose(const float* __restrict__ v, float* __restrict__ vT, int C, int dd) {
+  __shared__ float tile[32][33];
+  const int c0 = blockIdx.x * 32, t0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  if (c0 + ty < C && t0 + tx < dd) tile[ty][tx] = v[(int64_t)(c0 + ty) * dd + t0 + tx];
+  __syncthreads();
+  if (t0 + ty < dd && c0 + tx < C) vT[(int64_t)(t0 + ty) * C + c0 + tx] = tile[tx][ty];
+}
+
 // ---------------------------------------------------------------- selection
 // Order-preserving key of a float (larger float, larger key); -0 is taken as
 // +0 first, so that equal logits have equal keys.
@@ -65,23 +77,30 @@ __device__ __forceinline__ bool before(uint32_t ka, int ca, uint32_t kb, int cb)
 __device__ __forceinline__ void lds_wait() { __builtin_amdgcn_s_waitcnt(0xc07f); }  // lgkmcnt(0)
 
 // LDS per wave for one row's selection: the radix histogram and the list of
-// the selected (key, channel) pairs
+// the selected (key, channel) pairs, kl = the power of two >= k entries
 constexpr int kDynMaxK = 512;
-constexpr int kWaveWords = 256 + 2 * kDynMaxK;
+__host__ __device__ inline int list_len(int k) {
+  int P = 1;
+  while (P < k) P <<= 1;
+  return P;
+}
+__host__ __device__ inline int wave_words(int k) { return 256 + 2 * list_len(k); }
 
-// EB experts of one image per workgroup; DD >= the bottleneck width
+// EB experts of one image per workgroup of EB waves (a row each); DD >= the
+// bottleneck width
 template <int EB, int DD>
-__global__ void __launch_bounds__(kDynThreads)
+__global__ void __launch_bounds__(EB * kWave)
 k_dyn_select(const float* __restrict__ h, const float* __restrict__ L, const float* __restrict__ q,
-             const float* __restrict__ v, int32_t* __restrict__ S, float* __restrict__ W, int C, int R, int k,
+             const float* __restrict__ vT, int32_t* __restrict__ S, float* __restrict__ W, int C, int R, int k,
              int dd, int nblk) {
   extern __shared__ float sm[];
   float* rows = sm;              // [EB][C] the block's logit rows of this image
   float* qh = rows + EB * C;     // [EB][DD] q_e * h, zero past dd
-  uint32_t* wsm = reinterpret_cast<uint32_t*>(qh + EB * DD) + (threadIdx.x >> 6) * kWaveWords;
+  const int P = list_len(k);
+  uint32_t* wsm = reinterpret_cast<uint32_t*>(qh + EB * DD) + (threadIdx.x >> 6) * (256 + 2 * P);
   uint32_t* hist = wsm;
   uint32_t* lkey = hist + 256;
-  int32_t* lch = reinterpret_cast<int32_t*>(lkey + kDynMaxK);
+  int32_t* lch = reinterpret_cast<int32_t*>(lkey + P);
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int64_t b = blockIdx.x / nblk;
   const int e0 = (int)(blockIdx.x % nblk) * EB;
@@ -93,12 +112,14 @@ k_dyn_select(const float* __restrict__ h, const float* __restrict__ L, const flo
     qh[i] = t < dd ? qv * hv : 0.f;
   }
   __syncthreads();
-  // logits: a thread per channel, v_c in registers, every expert of the block
+  // logits: a thread per channel, v_c in registers (from the transposed
+  // embeddings vT[d][C], so a wave's reads of one t are consecutive), every
+  // expert of the block
   for (int c = threadIdx.x; c < C; c += blockDim.x) {
     float vr[DD];
 #pragma unroll
     for (int t = 0; t < DD; ++t) {
-      const float x = v[(int64_t)c * dd + min(t, dd - 1)];
+      const float x = vT[(int64_t)min(t, dd - 1) * C + c];
       vr[t] = t < dd ? x : 0.f;
     }
 #pragma unroll 4
@@ -110,8 +131,8 @@ k_dyn_select(const float* __restrict__ h, const float* __restrict__ L, const flo
     }
   }
   __syncthreads();
-  // each wave: whole rows
-  for (int e = wv; e < ne; e += kDynWaves) {
+  // each wave: one row
+  for (int e = wv; e < ne; e += EB) {
     const float* row = rows + e * C;
     // the k-th largest key, most significant byte first: after each round,
     // `prefix` holds the known high bytes and kk the rank still to find
@@ -172,7 +193,7 @@ k_dyn_select(const float* __restrict__ h, const float* __restrict__ L, const flo
       const uint64_t beq = __ballot(eq);
       const bool sel = (c < C && key > kstar) || (eq && eq_seen + __popcll(beq & below) < kk);
       const uint64_t bsel = __ballot(sel);
-      if (sel && taken + __popcll(bsel & below) < kDynMaxK) {
+      if (sel && taken + __popcll(bsel & below) < P) {
         const int pos = taken + __popcll(bsel & below);
         lkey[pos] = key;
         lch[pos] = c;
@@ -182,8 +203,6 @@ k_dyn_select(const float* __restrict__ h, const float* __restrict__ L, const flo
     }
     // bitonic sort of the k (padded to a power of two with entries that sort
     // last) into the canonical order
-    int P = 1;
-    while (P < k) P <<= 1;
     for (int i = k + lane; i < P; i += kWave) {
       lkey[i] = 0u;
       lch[i] = INT_MAX;
@@ -229,6 +248,7 @@ k_dyn_uncovered(const int32_t* __restrict__ S, int32_t* __restrict__ U, int32_t*
   for (int c = threadIdx.x; c < C; c += blockDim.x) cov[c] = 0;
   __syncthreads();
   const int64_t n = (int64_t)R * k;
+#pragma unroll 8
   for (int64_t j = threadIdx.x; j < n; j += blockDim.x) {
     const int32_t c = S[b * n + j];
     if ((uint32_t)c < (uint32_t)C) cov[c] = 1;
@@ -340,6 +360,7 @@ k_dyn_mix(const T* __restrict__ x, const int32_t* __restrict__ S, const float* _
     for (int j = 0; j < kDynTP; ++j) acc[j] = 0.f;
     if (o < R) {
       const int64_t item = b * R + o;
+#pragma unroll 8
       for (int i = 0; i < k; ++i) {
         const float a = alpha[item * k + i];
         const float4* r = reinterpret_cast<const float4*>(xs + min(max(S[item * k + i], 0), C - 1) * kDynTP);
@@ -354,6 +375,7 @@ k_dyn_mix(const T* __restrict__ x, const int32_t* __restrict__ S, const float* _
       }
     } else {
       const int n = nU[b];
+#pragma unroll 8
       for (int u = 0; u < n; ++u) {
         const float4* r = reinterpret_cast<const float4*>(xs + U[b * C + u] * kDynTP);
 #pragma unroll
@@ -377,29 +399,33 @@ k_dyn_mix(const T* __restrict__ x, const int32_t* __restrict__ S, const float* _
   }
 }
 
-// experts per selection workgroup: as many (up to 16) as the LDS holds
+// experts (and waves) per selection workgroup: 8 where two workgroups fit
+// a CU's LDS, else as many as one fits
+size_t select_lds(const Shape& sh, int eb, int DD) {
+  return ((size_t)eb * sh.C + (size_t)eb * DD) * 4 + (size_t)eb * wave_words(sh.k) * 4;
+}
 int select_eb(const Shape& sh, int DD) {
-  for (int eb : {16, 8, 4, 2, 1}) {
-    const size_t need = ((size_t)eb * sh.C + (size_t)eb * DD) * 4 + (size_t)kDynWaves * kWaveWords * 4;
-    if (need <= kDynLds) return eb;
-  }
+  for (int eb : {8, 4, 2, 1})
+    if (2 * select_lds(sh, eb, DD) <= kDynLds) return eb;
+  for (int eb : {8, 4, 2, 1})
+    if (select_lds(sh, eb, DD) <= kDynLds) return eb;
   return 0;
 }
 
 template <int DD>
-hipError_t launch_select_dd(const Shape& sh, const float* h, const float* L, const float* q, const float* v,
+hipError_t launch_select_dd(const Shape& sh, const float* h, const float* L, const float* q, const float* vT,
                             int32_t* S, float* W, int dd, hipStream_t st) {
   const int eb = select_eb(sh, DD);
   if (eb == 0) return hipErrorInvalidValue;
   const int nblk = (sh.R + eb - 1) / eb;
-  const size_t lds = ((size_t)eb * sh.C + (size_t)eb * DD) * 4 + (size_t)kDynWaves * kWaveWords * 4;
+  const size_t lds = select_lds(sh, eb, DD);
   using K = void (*)(const float*, const float*, const float*, const float*, int32_t*, float*, int, int, int, int,
                      int);
-  const K kern = eb == 16 ? k_dyn_select<16, DD> : eb == 8 ? k_dyn_select<8, DD> : eb == 4 ? k_dyn_select<4, DD>
-               : eb == 2 ? k_dyn_select<2, DD> : k_dyn_select<1, DD>;
+  const K kern = eb == 8 ? k_dyn_select<8, DD> : eb == 4 ? k_dyn_select<4, DD> : eb == 2 ? k_dyn_select<2, DD>
+                                                                                       : k_dyn_select<1, DD>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * nblk)), dim3(kDynThreads), lds, st, h, L, q, v, S, W, (int)sh.C,
+  hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * nblk)), dim3(eb * kWave), lds, st, h, L, q, vT, S, W, (int)sh.C,
                      sh.R, sh.k, dd, nblk);
   return hipGetLastError();
 }
@@ -413,8 +439,8 @@ bool dynamic_supported(const Shape& sh, int dd) {
 }
 
 hipError_t launch_dynamic(const Shape& sh, const void* x, const float* L, const moce_router& r,
-                          const moce_gate_params& g, void* y, float* d, float* h, int32_t* S, float* W, int32_t* U,
-                          int32_t* nU, float* tau, float* alpha, hipStream_t st) {
+                          const moce_gate_params& g, void* y, float* d, float* h, float* vT, int32_t* S, float* W,
+                          int32_t* U, int32_t* nU, float* tau, float* alpha, hipStream_t st) {
   hipError_t e = launch_pool(sh, x, d, st);
   if (e != hipSuccess) return e;
   if (sh.R > 0) {
@@ -423,8 +449,12 @@ hipError_t launch_dynamic(const Shape& sh, const void* x, const float* L, const 
                        st, d, r.Wh, r.bh, h, sh.B, (int)sh.C, r.d);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = r.d <= 32 ? launch_select_dd<32>(sh, h, L, r.q, r.v, S, W, r.d, st)
-                  : launch_select_dd<64>(sh, h, L, r.q, r.v, S, W, r.d, st);
+    hipLaunchKernelGGL(k_dyn_transpose, dim3((unsigned)((sh.C + 31) / 32), (unsigned)((r.d + 31) / 32)), dim3(1024),
+                       0, st, r.v, vT, (int)sh.C, r.d);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = r.d <= 32 ? launch_select_dd<32>(sh, h, L, r.q, vT, S, W, r.d, st)
+                  : launch_select_dd<64>(sh, h, L, r.q, vT, S, W, r.d, st);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(k_dyn_uncovered, dim3((unsigned)sh.B), dim3(1024), ((sh.C + 15) & ~15) + 16 * 4, st, S, U, nU,

@@ -166,12 +166,14 @@ hipError_t launch_gmix(const Shape& sh, const void* x, const float* stats, int n
                        hipStream_t st);
 
 // Input-conditioned supports (dynamic.hip): the whole inference path from x
-// to y with per-example supports S [B][R][k] and their logits W, per-example
+// to y over workspace arrays: the router output h [B][d], the transposed
+// channel embeddings vT [d][C], per-example supports S [B][R][k] and their
+// logits W, per-example
 // uncovered sets U [B][C] with counts nU [B], temperatures and coefficients,
 // over the workspace arrays passed in.
 bool dynamic_supported(const Shape& sh, int d);
 hipError_t launch_dynamic(const Shape& sh, const void* x, const float* L, const moce_router& r,
-                          const moce_gate_params& g, void* y, float* d, float* h, int32_t* S, float* W, int32_t* U,
-                          int32_t* nU, float* tau, float* alpha, hipStream_t st);
+                          const moce_gate_params& g, void* y, float* d, float* h, float* vT, int32_t* S, float* W,
+                          int32_t* U, int32_t* nU, float* tau, float* alpha, hipStream_t st);
 
 }  // namespace moce

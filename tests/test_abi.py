@@ -273,11 +273,12 @@ def test_forward_dynamic_host_errors(lib):
 
 
 def test_forward_dynamic_workspace_layout(lib):
-    """d [B][C], h [B][d], supports and their logits [B][E-1][k], U [B][C], nU [B], tau [B][E-1] and the
-    coefficients [B][E-1][k], each rounded up to 256 bytes."""
+    """d [B][C], h [B][d], the transposed channel embeddings [d][C], supports and their logits
+    [B][E-1][k], U [B][C], nU [B], tau [B][E-1] and the coefficients [B][E-1][k], each rounded up to
+    256 bytes."""
     desc = good_desc()
     B, C, R, k, d = desc.B, desc.C, desc.E - 1, desc.k, 8
     r = lambda n: (n + 255) // 256 * 256
-    expect = (r(B * C * 4) + r(B * d * 4) + 2 * r(B * R * k * 4) + r(B * C * 4) + r(B * 4) + r(B * R * 4)
-              + r(B * R * k * 4))
+    expect = (r(B * C * 4) + r(B * d * 4) + r(d * C * 4) + 2 * r(B * R * k * 4) + r(B * C * 4) + r(B * 4)
+              + r(B * R * 4) + r(B * R * k * 4))
     assert lib.moce_forward_dynamic_workspace_bytes(ctypes.byref(desc), d) == expect
