@@ -4,8 +4,10 @@ TEST INFRASTRUCTURE ONLY.  Only the test suite, ``__graft_entry__.smoke()`` and
 the benchmark's CPU-baseline leg may import this package.  The HIP library and
 its Python binding never import it, and it never imports them.
 
-The arithmetic lives in ``moce_oracle.c`` (plain double-precision loops); this
-module only compiles that file and marshals numpy arrays through ctypes.
+The forward arithmetic lives in ``moce_oracle.c`` (plain double-precision loops);
+this module only compiles that file and marshals numpy arrays through ctypes.
+The gradients (``backward.py``) are plain float64 numpy, pinned by finite
+differences through the C forward.
 """
 from __future__ import annotations
 
