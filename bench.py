@@ -293,6 +293,20 @@ def gate_forms_us(bn, n_k):
     return out
 
 
+def dynamic_us(bn, n_g=10, reps=5):
+    """The input-conditioned variant (router width 32, synthetic router of the workload's
+    shape) timed like the static forward: HIP graph of n_g forwards, median of reps replays."""
+    import torch
+    from paper_2608_23794_amd import inputs
+    from paper_2608_23794_amd.layer import DynamicMoceLayer
+    dl = DynamicMoceLayer.from_workload(bn.wl, bn.g, inputs.router_params(bn.wl), bn.layout)
+    ws = dl.new_workspace(bn.B)
+    t = quartiles(graph_times_ms(lambda i, st=None: dl.forward(bn.xs[i % bn.nsets], bn.ys[i % bn.nsets], ws), n_g, reps))[1]
+    del ws
+    torch.cuda.empty_cache()
+    return t
+
+
 def other_config(name, layout, args, stream):
     bn = Bench(name, layout, args.rotate_gib)
     mb, wl = bn.mb, bn.wl
@@ -318,6 +332,9 @@ def other_config(name, layout, args, stream):
                                           "scheduled forward's own kernels are timed in its rocprofv3 summaries")
     if name in GATE_TIMED:
         out["gate_entry_point_us"] = gate_forms_us(bn, n_g)
+    t_dyn = dynamic_us(bn)
+    out["dynamic_supports"] = {"latency_us": round(t_dyn * 1e3, 2), "over_static": round(t_dyn / med, 2),
+                               "router_width": 32}
     if not args.no_context:
         out["context"] = bn.dense_context(max(args.steps // 4, 10), stream)
         out["context"]["moce_over_dense_time"] = round(med * 1e3 / out["context"]["dense_1x1_us"], 3)
@@ -426,6 +443,10 @@ def main():
     }
     if wl.name in GATE_TIMED:
         line["gate_entry_point_us"] = gate_forms_us(bn, max(args.steps // 2, 10))
+    t_dyn = dynamic_us(bn)
+    line["dynamic_supports"] = {"latency_us": round(t_dyn * 1e3, 2), "over_static": round(t_dyn / fwd_graph, 2),
+                                "router_width": 32,
+                                "timing": "HIP graph of 10 forwards, median of 5 replays; over the static graph latency"}
     if not args.no_context:
         line["context"] = bn.dense_context(max(args.steps // 2, 10), stream)
         line["context"]["moce_over_dense_time"] = round(ms * 1e3 / line["context"]["dense_1x1_us"], 3)
