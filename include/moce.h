@@ -254,6 +254,68 @@ moce_status moce_forward_dynamic(const moce_desc* desc, const void* x, const flo
                                  const moce_gate_params* gate, void* y, int32_t* S_out, void* ws, size_t ws_bytes,
                                  hipStream_t stream);
 
+/* Gradient outputs of the gate's parameters (device arrays, float32, fully
+ * overwritten); only those of the gate's own kind are read and written.
+ *  MOCE_GATE_SOFTPLUS_LINEAR: da [E-1][k] (canonical positions, as a), dc [E-1];
+ *  MOCE_GATE_MLP_SIGMOID: dW1 [k][k], db1 [k], dw2 [k], db2 [1]. */
+typedef struct moce_gate_grads {
+    float* da;
+    float* dc;
+    float* dW1;
+    float* db1;
+    float* dw2;
+    float* db2;
+} moce_gate_grads;
+
+/* Bytes of device workspace moce_backward needs for `desc` with a gate of
+ * kind `gate_kind` (0 on an invalid descriptor or kind, or a shape beyond the
+ * backward's limits). */
+size_t moce_backward_workspace_bytes(const moce_desc* desc, int gate_kind);
+
+/* Gradients of the static layer (Secs. 3.2-3.4) for an upstream gradient dy
+ * of y = moce_forward(x).  The supports are fixed (Sec. 3.2: no gradient
+ * through the selection); the loss reaches the routing logits only through
+ * the selected values w (Eq. 4), the gate through the temperature, and x
+ * both through the routed and residual sums (Eqs. 5-6) and through the
+ * pooled descriptor that feeds the gate (Sec. 3.3):
+ *   dx:  d loss / d x, layout and element type of x, fully overwritten;
+ *   dw:  [E-1][k] float32, d loss / d w[e][i] for the prepared rows
+ *        (canonical order), fully overwritten;
+ *   the gate's parameter gradients into *grads (moce_gate_grads).
+ * x, s, w, gate as for moce_forward (prepared rows; the uncovered set is
+ * derived from s); dy: the layout and element type of y; x, dy and dx
+ * 16-byte aligned; ws: device workspace of at least
+ * moce_backward_workspace_bytes(desc, gate->kind) bytes, 256-byte aligned,
+ * contents on return unspecified.  Gradients are accumulated in float32.
+ * Errors: those of moce_forward; MOCE_ERR_NULL for a missing dy, dx, dw or
+ * gradient array of the gate's kind; MOCE_ERR_UNSUPPORTED when k > 1024, or
+ * k > 128 with the MLP gate.  Asynchronous on `stream`. */
+moce_status moce_backward(const moce_desc* desc, const void* x, const void* dy, const int32_t* s, const float* w,
+                          const moce_gate_params* gate, void* dx, float* dw, const moce_gate_grads* grads,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Bytes of device workspace moce_logit_backward needs (0 when R < 1 or C is
+ * outside [1, 32768]). */
+size_t moce_logit_backward_workspace_bytes(int32_t R, int64_t C);
+
+/* The coverage loss over the full routing logits (Sec. 3.4 Eq. 7) and the
+ * whole gradient of the routing logits (Sec. 3.2: the task loss reaches the
+ * selected entries, the coverage term every entry):
+ *   p[e][c] = softmax_c(L[e]), u[c] = (1/R) sum_e p[e][c], ub = mean_c u[c],
+ *   loss = sum_c (u[c] - ub)^2 / (ub^2 + eps),
+ *   dL[e][c] = lambda d loss / d L[e][c] + (dw[e][i] where c = s[e][i]).
+ * L: [R][C] float32 (R = E-1 routed experts); s, dw: prepared rows and the
+ * dw of moce_backward, [R][k], or both NULL for the coverage term alone;
+ * loss: device float, or NULL; dL: [R][C] float32, fully overwritten;
+ * eps >= 0 (the paper leaves it unstated); ws as sized above.
+ * Errors: MOCE_ERR_NULL (L, dL, ws; s without dw or dw without s),
+ * MOCE_ERR_SHAPE (R < 1, C < 1, k outside [1, C] with dw given),
+ * MOCE_ERR_UNSUPPORTED (C > 32768), MOCE_ERR_WORKSPACE, MOCE_ERR_ALIGN
+ * (ws not 256-byte aligned); eps < 0 or not finite: MOCE_ERR_SHAPE. */
+moce_status moce_logit_backward(int32_t R, int64_t C, int32_t k, const float* L, const int32_t* s, const float* dw,
+                                float eps, float lambda, float* loss, float* dL, void* ws, size_t ws_bytes,
+                                hipStream_t stream);
+
 /* Static string naming a status code. */
 const char* moce_status_str(int status);
 

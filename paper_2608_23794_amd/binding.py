@@ -30,7 +30,9 @@ STATUS = {
 ENTRY_POINTS = (
     "moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix",
     "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_forward_static",
-    "moce_forward_dynamic_workspace_bytes", "moce_forward_dynamic", "moce_status_str", "moce_abi_version",
+    "moce_forward_dynamic_workspace_bytes", "moce_forward_dynamic", "moce_backward_workspace_bytes",
+    "moce_backward", "moce_logit_backward_workspace_bytes", "moce_logit_backward", "moce_status_str",
+    "moce_abi_version",
 )
 
 MOCE_STATIC_SCRATCH_BYTES = 16 << 20
@@ -59,6 +61,11 @@ class moce_gate_params(ctypes.Structure):
                 ("a", ctypes.c_void_p), ("c", ctypes.c_void_p), ("W1", ctypes.c_void_p),
                 ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
                 ("b2", ctypes.c_float), ("tau_min", ctypes.c_float), ("tau_max", ctypes.c_float)]
+
+
+class moce_gate_grads(ctypes.Structure):
+    _fields_ = [("da", ctypes.c_void_p), ("dc", ctypes.c_void_p), ("dW1", ctypes.c_void_p),
+                ("db1", ctypes.c_void_p), ("dw2", ctypes.c_void_p), ("db2", ctypes.c_void_p)]
 
 
 _lib = None
@@ -91,11 +98,18 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_forward_dynamic_workspace_bytes.argtypes = [D, I32]
     lib.moce_forward_dynamic_workspace_bytes.restype = SZ
     lib.moce_forward_dynamic.argtypes = [D, P, P, ctypes.POINTER(moce_router), G, P, P, P, SZ, P]
+    lib.moce_backward_workspace_bytes.argtypes = [D, ctypes.c_int]
+    lib.moce_backward_workspace_bytes.restype = SZ
+    lib.moce_backward.argtypes = [D, P, P, P, P, G, P, P, ctypes.POINTER(moce_gate_grads), P, SZ, P]
+    lib.moce_logit_backward_workspace_bytes.argtypes = [I32, ctypes.c_int64]
+    lib.moce_logit_backward_workspace_bytes.restype = SZ
+    lib.moce_logit_backward.argtypes = [I32, ctypes.c_int64, I32, P, P, P, ctypes.c_float, ctypes.c_float, P, P,
+                                        P, SZ, P]
     lib.moce_status_str.argtypes = [ctypes.c_int]
     lib.moce_status_str.restype = ctypes.c_char_p
     lib.moce_abi_version.restype = ctypes.c_int
     for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward",
-                 "moce_forward_static", "moce_forward_dynamic"):
+                 "moce_forward_static", "moce_forward_dynamic", "moce_backward", "moce_logit_backward"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -213,6 +227,33 @@ def moce_forward_dynamic(desc: moce_desc, x, L, router: moce_router, gate: moce_
     _check("moce_forward_dynamic", load().moce_forward_dynamic(ctypes.byref(desc), _ptr(x), _ptr(L),
                                                                ctypes.byref(router), ctypes.byref(gate), _ptr(y),
                                                                _ptr(S_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def make_gate_grads(da=None, dc=None, dW1=None, db1=None, dw2=None, db2=None) -> moce_gate_grads:
+    """A gate-gradient struct over device arrays (they must outlive its use)."""
+    return moce_gate_grads(_ptr(da), _ptr(dc), _ptr(dW1), _ptr(db1), _ptr(dw2), _ptr(db2))
+
+
+def moce_backward_workspace_bytes(desc: moce_desc, gate_kind: int) -> int:
+    return int(load().moce_backward_workspace_bytes(ctypes.byref(desc), int(gate_kind)))
+
+
+def moce_backward(desc: moce_desc, x, dy, s, w, gate: moce_gate_params, dx, dw, grads: moce_gate_grads, ws,
+                  ws_bytes: int, stream=None) -> None:
+    _check("moce_backward", load().moce_backward(ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(s), _ptr(w),
+                                                 ctypes.byref(gate), _ptr(dx), _ptr(dw), ctypes.byref(grads),
+                                                 _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def moce_logit_backward_workspace_bytes(R: int, C: int) -> int:
+    return int(load().moce_logit_backward_workspace_bytes(int(R), int(C)))
+
+
+def moce_logit_backward(R: int, C: int, k: int, L, s, dw, eps: float, lam: float, loss, dL, ws, ws_bytes: int,
+                        stream=None) -> None:
+    _check("moce_logit_backward", load().moce_logit_backward(int(R), int(C), int(k), _ptr(L), _ptr(s), _ptr(dw),
+                                                             float(eps), float(lam), _ptr(loss), _ptr(dL),
+                                                             _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def raw_status(fn: str, *args) -> int:

@@ -401,4 +401,99 @@ moce_status moce_forward_dynamic(const moce_desc* desc, const void* x, const flo
       reinterpret_cast<float*>(base + l.alpha), stream));
 }
 
+// ---- backward ----------------------------------------------------------------
+
+namespace {
+
+struct BwdLayout {
+  size_t d, tau, stats, alpha, dal, S1, dtau, dg, dd, cnt, cur, off, inv, nU, dzg, part, total;
+};
+BwdLayout bwd_layout(const Shape& sh, int gate_kind) {
+  BwdLayout l{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += round_up(std::max<size_t>(bytes, 4));
+    return at;
+  };
+  const size_t br = (size_t)sh.B * sh.R, brk = br * sh.k;
+  l.d = take((size_t)sh.B * sh.C * sizeof(float));
+  l.tau = take(br * sizeof(float));
+  l.stats = take(3 * br * sizeof(float));
+  l.alpha = take(brk * sizeof(float));
+  l.dal = take(brk * sizeof(float));
+  l.S1 = take(br * sizeof(float));
+  l.dtau = take(br * sizeof(float));
+  l.dg = take(br * sizeof(float));
+  l.dd = take((size_t)sh.B * sh.C * sizeof(float));
+  l.cnt = take((size_t)(sh.C + 1) * sizeof(int32_t));
+  l.cur = take((size_t)sh.C * sizeof(int32_t));
+  l.off = take((size_t)(sh.C + 1) * sizeof(int32_t));
+  l.inv = take((size_t)sh.R * sh.k * sizeof(int32_t));
+  l.nU = take(sizeof(int32_t));
+  const bool mlp = gate_kind == MOCE_GATE_MLP_SIGMOID;
+  l.dzg = take(mlp ? brk * sizeof(float) : 0);
+  l.part = take(mlp ? moce::backward_mlp_parts(sh) * moce::backward_mlp_part_floats(sh) * sizeof(float) : 0);
+  l.total = off;
+  return l;
+}
+
+}  // namespace
+
+size_t moce_backward_workspace_bytes(const moce_desc* desc, int gate_kind) {
+  Shape sh;
+  if (check_desc(desc, &sh) != MOCE_OK) return 0;
+  if (gate_kind != MOCE_GATE_SOFTPLUS_LINEAR && gate_kind != MOCE_GATE_MLP_SIGMOID) return 0;
+  if (!moce::backward_supported(sh, gate_kind)) return 0;
+  return bwd_layout(sh, gate_kind).total;
+}
+
+moce_status moce_backward(const moce_desc* desc, const void* x, const void* dy, const int32_t* s, const float* w,
+                          const moce_gate_params* gate, void* dx, float* dw, const moce_gate_grads* grads,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  Shape sh;
+  moce_status st = check_desc(desc, &sh);
+  if (st != MOCE_OK) return st;
+  st = check_gate(sh, gate);
+  if (st != MOCE_OK) return st;
+  if (!x || !dy || !dx || !grads) return MOCE_ERR_NULL;
+  const bool mlp = gate->kind == MOCE_GATE_MLP_SIGMOID;
+  if (sh.R > 0) {
+    if (!s || !w || !dw) return MOCE_ERR_NULL;
+    if (mlp ? (!grads->dW1 || !grads->db1 || !grads->dw2 || !grads->db2) : (!grads->da || !grads->dc))
+      return MOCE_ERR_NULL;
+  }
+  if (!moce::backward_supported(sh, gate->kind)) return MOCE_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(dy, 16) || !aligned(dx, 16)) return MOCE_ERR_ALIGN;
+  const BwdLayout l = bwd_layout(sh, gate->kind);
+  if (!ws || ws_bytes < l.total) return MOCE_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return MOCE_ERR_ALIGN;
+  char* base = static_cast<char*>(ws);
+  auto F = [&](size_t o) { return reinterpret_cast<float*>(base + o); };
+  auto I = [&](size_t o) { return reinterpret_cast<int32_t*>(base + o); };
+  const moce::BwdWs b{F(l.d),   F(l.tau),   F(l.stats), F(l.alpha), F(l.dal), F(l.S1),  F(l.dtau), F(l.dg),  F(l.dd),
+                      I(l.cnt), I(l.cur),   I(l.off),   I(l.inv), I(l.nU),  F(l.dzg),  F(l.part)};
+  return device_status(moce::launch_backward(sh, x, dy, s, w, *gate, dx, dw, *grads, b, stream));
+}
+
+size_t moce_logit_backward_workspace_bytes(int32_t R, int64_t C) {
+  if (R < 1 || !moce::logit_backward_supported(C)) return 0;
+  return round_up((2 * (size_t)R + (size_t)C + 3) * sizeof(float));
+}
+
+moce_status moce_logit_backward(int32_t R, int64_t C, int32_t k, const float* L, const int32_t* s, const float* dw,
+                                float eps, float lambda, float* loss, float* dL, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
+  if (!L || !dL || !ws) return MOCE_ERR_NULL;
+  if ((s == nullptr) != (dw == nullptr)) return MOCE_ERR_NULL;
+  if (R < 1 || C < 1) return MOCE_ERR_SHAPE;
+  if (dw && (k < 1 || (int64_t)k > C)) return MOCE_ERR_SHAPE;
+  if (!std::isfinite(eps) || eps < 0.f || !std::isfinite(lambda)) return MOCE_ERR_SHAPE;
+  if (!moce::logit_backward_supported(C)) return MOCE_ERR_UNSUPPORTED;
+  if (ws_bytes < moce_logit_backward_workspace_bytes(R, C)) return MOCE_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return MOCE_ERR_ALIGN;
+  return device_status(moce::launch_logit_backward(R, (int)C, k, L, s, dw, eps, lambda, loss, dL,
+                                                   static_cast<float*>(ws), stream));
+}
+
 }  // extern "C"

@@ -120,8 +120,9 @@ hipError_t launch_prepare(const Shape& sh, const int32_t* s, const float* w, int
                           float* w_out, uint8_t* covered, int32_t* U, int32_t* info,
                           hipStream_t st);
 hipError_t launch_pool(const Shape& sh, const void* x, float* d, hipStream_t st);
-// alpha and the softmax statistics (a block of 3 B R floats, image-major
-// planes as in stats_planes) are optional outputs (nullptr: not written).
+// tau [B][R] is always written; alpha and the softmax statistics (a block of
+// 3 B R floats, image-major planes as in stats_planes) are optional outputs
+// (nullptr: not written).
 hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const float* w,
                        const moce_gate_params& g, float* tau, float* alpha, float* stats, hipStream_t st);
 
@@ -175,5 +176,46 @@ bool dynamic_supported(const Shape& sh, int d);
 hipError_t launch_dynamic(const Shape& sh, const void* x, const float* L, const moce_router& r,
                           const moce_gate_params& g, void* y, float* d, float* h, float* vT, int32_t* S, float* W,
                           int32_t* U, int32_t* nU, float* tau, float* alpha, hipStream_t st);
+
+// Backward (backward.hip, bwdmfma.hip).  Device arrays of the workspace:
+// d [B][C], tau [B][R], stats [3][B][R] (image-major planes), alpha, dal [B][R][k],
+// S1, dtau, dg [B][R], dd [B][C], the inverse support map (cnt, cur [C],
+// off [C+1], inv [R k], nU [1]), and for the MLP gate dzg [B][R][k] and
+// part (the per-workgroup partial sums).
+struct BwdWs {
+  float* d;
+  float* tau;
+  float* stats;
+  float* alpha;
+  float* dal;
+  float* S1;
+  float* dtau;
+  float* dg;
+  float* dd;
+  int32_t* cnt;
+  int32_t* cur;
+  int32_t* off;
+  int32_t* inv;
+  int32_t* nU;
+  float* dzg;
+  float* part;
+};
+bool backward_supported(const Shape& sh, int gate_kind);
+size_t backward_mlp_parts(const Shape& sh);
+size_t backward_mlp_part_floats(const Shape& sh);
+hipError_t launch_backward(const Shape& sh, const void* x, const void* dy, const int32_t* s, const float* w,
+                           const moce_gate_params& g, void* dx, float* dw, const moce_gate_grads& gg,
+                           const BwdWs& ws, hipStream_t st);
+// The matrix-core kernels of the backward: each returns false (and launches
+// nothing) where the shape does not suit it, else true with the launch status
+// in *err.
+bool bwd_mfma_dalpha(const Shape& sh, const void* x, const void* dy, const int32_t* s, const BwdWs& ws,
+                     hipStream_t st, hipError_t* err);
+bool bwd_mfma_dx(const Shape& sh, const void* dy, const BwdWs& ws, void* dx, hipStream_t st, hipError_t* err);
+
+// Coverage loss and the full routing-logit gradient; ws holds 2 R + C + 3 floats.
+bool logit_backward_supported(int64_t C);
+hipError_t launch_logit_backward(int R, int C, int k, const float* L, const int32_t* s, const float* dw, float eps,
+                                 float lambda, float* loss, float* dL, float* ws, hipStream_t st);
 
 }  // namespace moce

@@ -147,6 +147,53 @@ class MoceLayer:
                         y, ws, ws.numel(), self._stream())
         return y
 
+    # -- backward --------------------------------------------------------------
+    def backward_workspace_bytes(self, B: int) -> int:
+        return mb.moce_backward_workspace_bytes(self.desc(B), self.gate.kind)
+
+    def new_backward_workspace(self, B: int) -> torch.Tensor:
+        n = self.backward_workspace_bytes(B)
+        if n == 0:
+            raise mb.MoceError("moce_backward_workspace_bytes", -10, "(shape beyond the backward's limits)")
+        return torch.empty(n, dtype=torch.uint8, device=self.device)
+
+    def backward(self, x: torch.Tensor, dy: torch.Tensor, dx: Optional[torch.Tensor] = None,
+                 ws: Optional[torch.Tensor] = None) -> dict:
+        """moce_backward: dx, dw [E-1][k] (prepared rows) and the gate's parameter gradients."""
+        self._ready()
+        B = x.shape[0]
+        f32, dev = torch.float32, self.device
+        if dx is None:
+            dx = torch.empty_like(x)
+        if ws is None:
+            ws = self.new_backward_workspace(B)
+        R, k = self.R, self.k
+        out = {"dx": dx, "dw": torch.empty((R, k), dtype=f32, device=dev)}
+        if self.gate.kind == mb.MOCE_GATE_SOFTPLUS_LINEAR:
+            out["da"] = torch.empty((R, k), dtype=f32, device=dev)
+            out["dc"] = torch.empty(max(R, 1), dtype=f32, device=dev)
+            grads = mb.make_gate_grads(da=out["da"], dc=out["dc"])
+        else:
+            out["dW1"] = torch.empty((k, k), dtype=f32, device=dev)
+            out["db1"] = torch.empty(k, dtype=f32, device=dev)
+            out["dw2"] = torch.empty(k, dtype=f32, device=dev)
+            out["db2"] = torch.empty(1, dtype=f32, device=dev)
+            grads = mb.make_gate_grads(dW1=out["dW1"], db1=out["db1"], dw2=out["dw2"], db2=out["db2"])
+        mb.moce_backward(self.desc(B), x, dy, self.s_c, self.w_c, self.gate, dx, out["dw"], grads, ws, ws.numel(),
+                         self._stream())
+        return out
+
+    def logit_backward(self, L: torch.Tensor, dw: Optional[torch.Tensor], eps: float, lam: float):
+        """moce_logit_backward over the full logits L [E-1][C]: (loss, dL)."""
+        R, C = self.R, self.C
+        n = mb.moce_logit_backward_workspace_bytes(R, C)
+        ws = torch.empty(max(n, 1), dtype=torch.uint8, device=self.device)
+        loss = torch.empty(1, dtype=torch.float32, device=self.device)
+        dL = torch.empty((R, C), dtype=torch.float32, device=self.device)
+        mb.moce_logit_backward(R, C, self.k, L, self.s_c if dw is not None else None, dw, eps, lam, loss, dL, ws, n,
+                               self._stream())
+        return loss, dL
+
 
 class DynamicMoceLayer:
     """The layer with input-conditioned supports (Sec. 5 Eq. 11): device

@@ -282,3 +282,63 @@ def test_forward_dynamic_workspace_layout(lib):
     expect = (r(B * C * 4) + r(B * d * 4) + r(d * C * 4) + 2 * r(B * R * k * 4) + r(B * C * 4) + r(B * 4)
               + r(B * R * 4) + r(B * R * k * 4))
     assert lib.moce_forward_dynamic_workspace_bytes(ctypes.byref(desc), d) == expect
+
+
+def _call_backward(desc, gate, grads, x=FAKE, dy=FAKE, s=FAKE, w=FAKE, dx=FAKE, dw=FAKE, ws=FAKE,
+                   ws_bytes=1 << 30):
+    g = ctypes.byref(grads) if grads is not None else None
+    return mb.raw_status("moce_backward", ctypes.byref(desc), x, dy, s, w, ctypes.byref(gate), dx, dw, g, ws,
+                         ws_bytes, None)
+
+
+def test_backward_host_errors(lib):
+    """Every host-side check of the backward returns before any launch."""
+    desc = good_desc()
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+    grads = mb.moce_gate_grads(FAKE, FAKE, None, None, None, None)
+    for kw, code in BAD_DESCS:
+        assert _call_backward(good_desc(**kw), gate, grads) == code, kw
+    assert _call_backward(desc, gate, None) == -1
+    assert _call_backward(desc, gate, grads, dy=None) == -1
+    assert _call_backward(desc, gate, grads, dx=None) == -1
+    assert _call_backward(desc, gate, grads, dw=None) == -1
+    assert _call_backward(desc, gate, mb.moce_gate_grads(FAKE, None, None, None, None, None)) == -1
+    mlp = mb.make_gate(mb.MOCE_GATE_MLP_SIGMOID, W1=FAKE, b1=FAKE, w2=FAKE)
+    assert _call_backward(desc, mlp, grads) == -1          # the MLP's gradient arrays are missing
+    assert _call_backward(desc, mb.make_gate(7), grads) == -6
+    assert _call_backward(good_desc(C=1200, k=1025, E=16), gate, grads) == -10
+    mlp_all = mb.moce_gate_grads(None, None, FAKE, FAKE, FAKE, FAKE)
+    assert _call_backward(good_desc(C=256, k=129), mlp, mlp_all) == -10
+    assert _call_backward(desc, gate, grads, dy=FAKE_UNALIGNED) == -8
+    assert _call_backward(desc, gate, grads, ws=None) == -7
+    need = lib.moce_backward_workspace_bytes(ctypes.byref(desc), mb.MOCE_GATE_SOFTPLUS_LINEAR)
+    assert need > 0
+    assert _call_backward(desc, gate, grads, ws_bytes=need - 1) == -7
+    assert _call_backward(desc, gate, grads, ws=FAKE_UNALIGNED, ws_bytes=need) == -8
+    assert lib.moce_backward_workspace_bytes(ctypes.byref(desc), 7) == 0
+    assert lib.moce_backward_workspace_bytes(ctypes.byref(good_desc(C=256, k=129)), mb.MOCE_GATE_MLP_SIGMOID) == 0
+
+
+def test_backward_workspace_grows_with_the_mlp_gate(lib):
+    desc = good_desc()
+    sp = lib.moce_backward_workspace_bytes(ctypes.byref(desc), mb.MOCE_GATE_SOFTPLUS_LINEAR)
+    ml = lib.moce_backward_workspace_bytes(ctypes.byref(desc), mb.MOCE_GATE_MLP_SIGMOID)
+    B, R, k = desc.B, desc.E - 1, desc.k
+    assert ml >= sp + B * R * k * 4 and sp % 256 == 0 and ml % 256 == 0
+
+
+def test_logit_backward_host_errors(lib):
+    def call(R=4, C=64, k=8, L=FAKE, s=FAKE, dw=FAKE, eps=1e-8, lam=1.0, dL=FAKE, ws=FAKE, ws_bytes=1 << 20):
+        return mb.raw_status("moce_logit_backward", R, C, k, L, s, dw, ctypes.c_float(eps), ctypes.c_float(lam),
+                             None, dL, ws, ws_bytes, None)
+    assert call(L=None) == -1 and call(dL=None) == -1 and call(ws=None) == -1
+    assert call(s=None) == -1 and call(dw=None) == -1
+    assert call(R=0) == -2 and call(C=0) == -2 and call(k=0) == -2 and call(k=65) == -2
+    assert call(eps=-1.0) == -2 and call(eps=float("nan")) == -2
+    assert call(C=32769) == -10
+    need = lib.moce_logit_backward_workspace_bytes(4, 64)
+    assert need == (2 * 4 + 64 + 3) * 4 + 256 - (2 * 4 + 64 + 3) * 4 % 256
+    assert call(ws_bytes=need - 1) == -7
+    assert call(ws=FAKE_UNALIGNED) == -8
+    assert lib.moce_logit_backward_workspace_bytes(0, 64) == 0
+    assert lib.moce_logit_backward_workspace_bytes(4, 40000) == 0
