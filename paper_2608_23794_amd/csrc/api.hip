@@ -406,7 +406,8 @@ moce_status moce_forward_dynamic(const moce_desc* desc, const void* x, const flo
 namespace {
 
 struct BwdLayout {
-  size_t d, tau, stats, alpha, dal, S1, dtau, dg, dd, cnt, cur, off, inv, nU, dzg, part, total;
+  size_t d, tau, stats, alpha, dal, S1, dtau, dg, dd, cnt, cur, off, inv, nU, dzg, part;
+  size_t dxs_cnt, dxs_off, dxs_cur, dxs_w0, dxs_w1, dxs_coef, total;
 };
 BwdLayout bwd_layout(const Shape& sh, int gate_kind) {
   BwdLayout l{};
@@ -420,8 +421,13 @@ BwdLayout bwd_layout(const Shape& sh, int gate_kind) {
   l.d = take((size_t)sh.B * sh.C * sizeof(float));
   l.tau = take(br * sizeof(float));
   l.stats = take(3 * br * sizeof(float));
-  l.alpha = take(brk * sizeof(float));
-  l.dal = take(brk * sizeof(float));
+  int nbk = 0;
+  int64_t nek = 0;
+  moce::bwd_dx_sched_sizes(sh, &nbk, &nek);
+  l.alpha = take(nbk > 0 ? 0 : brk * sizeof(float));
+  int nsplit = 1, split_len = 0;
+  moce::bwd_dalpha_splits(sh, &nsplit, &split_len);
+  l.dal = take((size_t)nsplit * brk * sizeof(float));
   l.S1 = take(br * sizeof(float));
   l.dtau = take(br * sizeof(float));
   l.dg = take(br * sizeof(float));
@@ -434,6 +440,15 @@ BwdLayout bwd_layout(const Shape& sh, int gate_kind) {
   const bool mlp = gate_kind == MOCE_GATE_MLP_SIGMOID;
   l.dzg = take(mlp ? brk * sizeof(float) : 0);
   l.part = take(mlp ? moce::backward_mlp_parts(sh) * moce::backward_mlp_part_floats(sh) * sizeof(float) : 0);
+  int nb = 0;
+  int64_t ne = 0;
+  moce::bwd_dx_sched_sizes(sh, &nb, &ne);
+  l.dxs_cnt = take((size_t)nb * sizeof(int32_t));
+  l.dxs_off = take((size_t)(nb + 1) * sizeof(int32_t));
+  l.dxs_cur = take((size_t)nb * sizeof(int32_t));
+  l.dxs_w0 = take((size_t)ne * sizeof(uint32_t));
+  l.dxs_w1 = take((size_t)ne * sizeof(int32_t));
+  l.dxs_coef = take((size_t)sh.B * ne * sizeof(uint32_t));
   l.total = off;
   return l;
 }
@@ -472,7 +487,10 @@ moce_status moce_backward(const moce_desc* desc, const void* x, const void* dy, 
   auto F = [&](size_t o) { return reinterpret_cast<float*>(base + o); };
   auto I = [&](size_t o) { return reinterpret_cast<int32_t*>(base + o); };
   const moce::BwdWs b{F(l.d),   F(l.tau),   F(l.stats), F(l.alpha), F(l.dal), F(l.S1),  F(l.dtau), F(l.dg),  F(l.dd),
-                      I(l.cnt), I(l.cur),   I(l.off),   I(l.inv), I(l.nU),  F(l.dzg),  F(l.part)};
+                      I(l.cnt), I(l.cur),   I(l.off),   I(l.inv), I(l.nU),  F(l.dzg),  F(l.part),
+                      I(l.dxs_cnt), I(l.dxs_off), I(l.dxs_cur),
+                      reinterpret_cast<uint32_t*>(base + l.dxs_w0), I(l.dxs_w1),
+                      reinterpret_cast<uint32_t*>(base + l.dxs_coef)};
   return device_status(moce::launch_backward(sh, x, dy, s, w, *gate, dx, dw, *grads, b, stream));
 }
 

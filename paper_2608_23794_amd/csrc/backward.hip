@@ -152,16 +152,17 @@ k_bw_dalpha(const T* __restrict__ x, const T* __restrict__ dy, const int32_t* __
 }
 
 // ---------------------------------------------------------------- rows: S1, dtau, dg
-// A wave per (image, routed expert).  S1 = sum_i alpha_i dalpha_i; with
+// A wave per (image, routed expert); dalpha arrives as nsplit partial sums,
+// whose total replaces the first.  S1 = sum_i alpha_i dalpha_i; with
 // Aw = sum_i alpha_i w_i, sum_i dz_i w_i = sum_i alpha_i (dalpha_i - S1) (w_i - Aw),
 // centred twice so that nothing cancels; dtau = -that / tau^2 (rt = 1/tau).
 // Softplus-linear gate: g = c_e + sum_i a_ei z_i, dg = dtau sigmoid(g).
 template <int NPL>
 __global__ void __launch_bounds__(kBwThreads)
-k_bw_rows(const float* __restrict__ dal, const float* __restrict__ w, const float* __restrict__ stats,
+k_bw_rows(float* __restrict__ dal, const float* __restrict__ w, const float* __restrict__ stats,
           const float* __restrict__ d, const int32_t* __restrict__ s, const float* __restrict__ a,
           const float* __restrict__ cc, float* __restrict__ S1o, float* __restrict__ dtau_o,
-          float* __restrict__ dg_o, int64_t B, int C, int R, int k) {
+          float* __restrict__ dg_o, int64_t B, int C, int R, int k, int nsplit) {
   const int64_t row = (int64_t)blockIdx.x * kBwWaves + (threadIdx.x >> 6);
   if (row >= B * R) return;
   const int lane = threadIdx.x & 63;
@@ -181,6 +182,10 @@ k_bw_rows(const float* __restrict__ dal, const float* __restrict__ w, const floa
       wv[j] = w[(int64_t)e * k + i];
       al[j] = alpha_of(wv[j], rt, m, rzs);
       da[j] = dal[row * k + i];
+      if (nsplit > 1) {  // partial sums along the positions: total into the first block
+        for (int sp = 1; sp < nsplit; ++sp) da[j] += dal[(sp * n + row) * k + i];
+        dal[row * k + i] = da[j];
+      }
       s1 += al[j] * da[j];
       aw += al[j] * wv[j];
     }
@@ -589,7 +594,13 @@ hipError_t launch_backward(const Shape& sh, const void* x, const void* dy, const
     if ((err = hipGetLastError()) != hipSuccess) return err;
     // forward quantities: d, the softmax statistics and the coefficients
     if ((err = launch_pool(sh, x, ws.d, st)) != hipSuccess) return err;
-    if ((err = launch_gate(sh, ws.d, s, w, g, ws.tau, ws.alpha, ws.stats, st)) != hipSuccess) return err;
+    // the coefficients themselves only for the generic dx (the matrix-core dx
+    // rebuilds them from the statistics)
+    int nbk;
+    int64_t nem;
+    bwd_dx_sched_sizes(sh, &nbk, &nem);
+    float* alpha_out = nbk > 0 ? nullptr : ws.alpha;
+    if ((err = launch_gate(sh, ws.d, s, w, g, ws.tau, alpha_out, ws.stats, st)) != hipSuccess) return err;
     // dalpha
     if (!bwd_mfma_dalpha(sh, x, dy, s, ws, st, &err)) {
       const unsigned nb = blocks_for(B * R, kBwWaves);
@@ -613,12 +624,15 @@ hipError_t launch_backward(const Shape& sh, const void* x, const void* dy, const
     if (err != hipSuccess) return err;
     // rows
     {
+      int nsplit = 1, split_len = 0;
+      bwd_dalpha_splits(sh, &nsplit, &split_len);
       const unsigned nb = blocks_for(B * R, kBwWaves);
       const float* a = mlp ? nullptr : g.a;
       const float* cc = mlp ? nullptr : g.c;
       const int npl = (k + kWave - 1) / kWave;
 #define MOCE_BW_ROWS(N) \
-  k_bw_rows<N><<<nb, kBwThreads, 0, st>>>(ws.dal, w, ws.stats, ws.d, s, a, cc, ws.S1, ws.dtau, ws.dg, B, C, R, k)
+  k_bw_rows<N><<<nb, kBwThreads, 0, st>>>(ws.dal, w, ws.stats, ws.d, s, a, cc, ws.S1, ws.dtau, ws.dg, B, C, R, k, \
+                                          nsplit)
       if (npl <= 1)
         MOCE_BW_ROWS(1);
       else if (npl <= 2)
@@ -653,7 +667,7 @@ hipError_t launch_backward(const Shape& sh, const void* x, const void* dy, const
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   // dx
-  if (bwd_mfma_dx(sh, dy, ws, dx, st, &err)) return err;
+  if (bwd_mfma_dx(sh, dy, s, w, ws, dx, st, &err)) return err;
   const unsigned nb = blocks_for(B * C * HW, kBwThreads);
   if (bf) {
     auto gy = static_cast<const uint16_t*>(dy);

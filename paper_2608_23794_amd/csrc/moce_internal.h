@@ -199,6 +199,14 @@ struct BwdWs {
   int32_t* nU;
   float* dzg;
   float* part;
+  // the matrix-core dx: bucket counts, offsets [nb + 1] and cursors, the
+  // scheduled entries (w0, w1) and their coefficients per image [B][NEmax]
+  int32_t* dxs_cnt;
+  int32_t* dxs_off;
+  int32_t* dxs_cur;
+  uint32_t* dxs_w0;
+  int32_t* dxs_w1;
+  uint32_t* dxs_coef;
 };
 bool backward_supported(const Shape& sh, int gate_kind);
 size_t backward_mlp_parts(const Shape& sh);
@@ -211,7 +219,13 @@ hipError_t launch_backward(const Shape& sh, const void* x, const void* dy, const
 // in *err.
 bool bwd_mfma_dalpha(const Shape& sh, const void* x, const void* dy, const int32_t* s, const BwdWs& ws,
                      hipStream_t st, hipError_t* err);
-bool bwd_mfma_dx(const Shape& sh, const void* dy, const BwdWs& ws, void* dx, hipStream_t st, hipError_t* err);
+// Partial sums of dalpha along the positions: dal holds nsplit blocks of
+// B R k floats (nsplit = 1 except for the matrix-core NCHW product).
+void bwd_dalpha_splits(const Shape& sh, int* nsplit, int* split_len);
+bool bwd_mfma_dx(const Shape& sh, const void* dy, const int32_t* s, const float* w, const BwdWs& ws, void* dx,
+                 hipStream_t st, hipError_t* err);
+// sizes of the dx schedule (0 where the matrix-core dx does not apply)
+void bwd_dx_sched_sizes(const Shape& sh, int* nbuckets, int64_t* ne_max);
 
 // Coverage loss and the full routing-logit gradient; ws holds 2 R + C + 3 floats.
 bool logit_backward_supported(int64_t C);

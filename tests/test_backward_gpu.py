@@ -154,6 +154,13 @@ def rand_layer(seed, B, C, E, k, H, W, dtype, layout, gate="softplus"):
     (3, 37, 9, 7, 3, 5, "bf16", "nchw"),       # C not a multiple of 8, odd plane
     (2, 130, 17, 70, 1, 1, "bf16", "nhwc"),    # one position, k past 64
     (1, 300, 33, 200, 2, 7, "f32", "nhwc"),    # k past 128
+    (2, 264, 72, 9, 5, 8, "bf16", "nhwc"),     # matrix-core dalpha: ragged channel and expert blocks, 2 steps
+    (2, 72, 16, 7, 9, 8, "bf16", "nchw"),      # matrix-core dalpha, NCHW: 72 positions, a ragged last step
+    (1, 48, 24, 6, 5, 4, "bf16", "nchw"),      # NCHW with 4-position loads
+    (2, 512, 9, 255, 2, 3, "bf16", "nhwc"),    # the byte table's limit k = 255
+    (2, 512, 9, 256, 2, 3, "bf16", "nhwc"),    # k = 256: the generic kernel
+    (1, 264, 136, 9, 7, 10, "bf16", "nhwc"),   # matrix-core dx: 2 channel blocks, 3 expert chunks, 2 position tiles
+    (1, 300, 136, 5, 6, 6, "bf16", "nchw"),    # the same, NCHW with 4-position loads
 ])
 def test_backward_edge_shapes(B, C, E, k, H, W, dtype, layout):
     layer, x, p = rand_layer(B * 1000 + C, B, C, E, k, H, W, dtype, layout)
