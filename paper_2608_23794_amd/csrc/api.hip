@@ -407,7 +407,7 @@ namespace {
 
 struct BwdLayout {
   size_t d, tau, stats, alpha, dal, S1, dtau, dg, dd, cnt, cur, off, inv, nU, dzg, part;
-  size_t dxs_cnt, dxs_off, dxs_cur, dxs_w0, dxs_w1, dxs_coef, total;
+  size_t dxs_cnt, dxs_off, dxs_cur, dxs_w0, dxs_w1, dxs_coef, psum, total;
 };
 BwdLayout bwd_layout(const Shape& sh, int gate_kind) {
   BwdLayout l{};
@@ -449,6 +449,9 @@ BwdLayout bwd_layout(const Shape& sh, int gate_kind) {
   l.dxs_w0 = take((size_t)ne * sizeof(uint32_t));
   l.dxs_w1 = take((size_t)ne * sizeof(int32_t));
   l.dxs_coef = take((size_t)sh.B * ne * sizeof(uint32_t));
+  int ng = 1, gs = 1;
+  moce::backward_sum_groups(sh, &ng, &gs);
+  l.psum = take((size_t)ng * (2 * (size_t)sh.R * sh.k + sh.R) * sizeof(float));
   l.total = off;
   return l;
 }
@@ -490,7 +493,7 @@ moce_status moce_backward(const moce_desc* desc, const void* x, const void* dy, 
                       I(l.cnt), I(l.cur),   I(l.off),   I(l.inv), I(l.nU),  F(l.dzg),  F(l.part),
                       I(l.dxs_cnt), I(l.dxs_off), I(l.dxs_cur),
                       reinterpret_cast<uint32_t*>(base + l.dxs_w0), I(l.dxs_w1),
-                      reinterpret_cast<uint32_t*>(base + l.dxs_coef)};
+                      reinterpret_cast<uint32_t*>(base + l.dxs_coef), F(l.psum)};
   return device_status(moce::launch_backward(sh, x, dy, s, w, *gate, dx, dw, *grads, b, stream));
 }
 

@@ -112,12 +112,24 @@ __global__ void k_inv_fill(const int32_t* __restrict__ s, int64_t n, int32_t* __
   if (t < n) inv[atomicAdd(&cur[s[t]], 1)] = (int32_t)t;
 }
 
-// each channel's entries ascending (by expert, as a row holds a channel once)
-__global__ void k_inv_sort(const int32_t* __restrict__ off, int32_t* __restrict__ inv, int C) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+// each channel's entries ascending (by expert, as a row holds a channel once):
+// a wave per channel; up to 64 entries by rank (each entry's place is the
+// number of smaller ones), longer lists by insertion on one lane
+__global__ void __launch_bounds__(256)
+k_inv_sort(const int32_t* __restrict__ off, int32_t* __restrict__ inv, int C) {
+  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (c >= C) return;
-  const int a = off[c], z = off[c + 1];
-  for (int j = a + 1; j < z; ++j) {
+  const int lane = threadIdx.x & 63;
+  const int a = off[c], n = off[c + 1] - a;
+  if (n <= 64) {
+    const int32_t v = lane < n ? inv[a + lane] : INT_MAX;
+    int rank = 0;
+    for (int j = 0; j < n; ++j) rank += __shfl(v, j) < v;
+    if (lane < n) inv[a + rank] = v;
+    return;
+  }
+  if (lane != 0) return;
+  for (int j = a + 1; j < a + n; ++j) {
     const int32_t v = inv[j];
     int q = j - 1;
     while (q >= a && inv[q] > v) {
@@ -216,40 +228,64 @@ k_bw_rows(float* __restrict__ dal, const float* __restrict__ w, const float* __r
 }
 
 // ---------------------------------------------------------------- sums over images
-// A thread per (routed expert, support position):
+// Partial sums over groups of images (grid.y = group g of gs images), a thread
+// per (routed expert, support position):
 //   dw[e][i] = sum_b alpha_bei (dalpha_bei - S1_be) rt_be,
-//   da[e][i] = sum_b dg_be d[b][s_ei]  (softplus-linear gate only).
+//   da[e][i] = sum_b dg_be d[b][s_ei]  (softplus-linear gate only),
+// and, on the threads of position 0, dc[e] = sum_b dg_be; then one pass sums
+// the groups in order.
 __global__ void __launch_bounds__(kBwThreads)
 k_bw_sums(const float* __restrict__ dal, const float* __restrict__ w, const float* __restrict__ stats,
           const float* __restrict__ S1, const float* __restrict__ dg, const float* __restrict__ d,
-          const int32_t* __restrict__ s, float* __restrict__ dw, float* __restrict__ da, int64_t B, int C, int R,
-          int k) {
+          const int32_t* __restrict__ s, float* __restrict__ pdw, float* __restrict__ pda, float* __restrict__ pdc,
+          int64_t B, int C, int R, int k, int gs, bool gate_sums) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t rk = (int64_t)R * k;
   if (t >= rk) return;
+  const int g = blockIdx.y;
   const int e = (int)(t / k);
   const int64_t n = B * R;
   const float wv = w[t];
   const int c = s[t];
-  float sw = 0.f, sa = 0.f;
-  for (int64_t b = 0; b < B; ++b) {
+  float sw = 0.f, sa = 0.f, sc = 0.f;
+  const int64_t b1 = min<int64_t>(B, (int64_t)(g + 1) * gs);
+  for (int64_t b = (int64_t)g * gs; b < b1; ++b) {
     const int64_t row = b * R + e;
     const float rt = stats[row];
     const float al = alpha_of(wv, rt, stats[n + row], stats[2 * n + row]);
     sw += al * (dal[b * rk + t] - S1[row]) * rt;
-    if (da) sa += dg[row] * d[b * C + c];
+    if (gate_sums) {
+      sa += dg[row] * d[b * C + c];
+      sc += dg[row];
+    }
   }
-  dw[t] = sw;
-  if (da) da[t] = sa;
+  pdw[g * rk + t] = sw;
+  if (gate_sums) {
+    pda[g * rk + t] = sa;
+    if (t % k == 0) pdc[(int64_t)g * R + e] = sc;
+  }
 }
 
-// dc[e] = sum_b dg_be
-__global__ void k_bw_dc(const float* __restrict__ dg, float* __restrict__ dc, int64_t B, int R) {
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= R) return;
-  float acc = 0.f;
-  for (int64_t b = 0; b < B; ++b) acc += dg[b * R + e];
-  dc[e] = acc;
+__global__ void k_bw_sums_reduce(const float* __restrict__ pdw, const float* __restrict__ pda,
+                                 const float* __restrict__ pdc, int ng, int64_t rk, int R, float* __restrict__ dw,
+                                 float* __restrict__ da, float* __restrict__ dc) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < rk) {
+    float sw = 0.f, sa = 0.f;
+#pragma unroll 8
+    for (int g = 0; g < ng; ++g) {
+      sw += pdw[g * rk + t];
+      if (da) sa += pda[g * rk + t];
+    }
+    dw[t] = sw;
+    if (da) da[t] = sa;
+  }
+  if (dc && t < R) {
+    float sc = 0.f;
+#pragma unroll 8
+    for (int g = 0; g < ng; ++g) sc += pdc[(int64_t)g * R + t];
+    dc[t] = sc;
+  }
 }
 
 // ---------------------------------------------------------------- dd
@@ -265,6 +301,7 @@ k_bw_dd(const int32_t* __restrict__ off, const int32_t* __restrict__ inv, const 
   const int c = (int)(t - b * C);
   const int64_t rk = (int64_t)R * k;
   float acc = 0.f;
+#pragma unroll 8
   for (int j = off[c]; j < off[c + 1]; ++j) {
     const int ent = inv[j];
     if (a)
@@ -561,6 +598,15 @@ unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per)
 
 }  // namespace
 
+// image groups of the sums over images: about 2048 workgroups, at most 64
+// groups
+void backward_sum_groups(const Shape& sh, int* ng, int* gs) {
+  const int64_t blocks = std::max<int64_t>(1, ((int64_t)sh.R * sh.k + kBwThreads - 1) / kBwThreads);
+  const int64_t want = std::max<int64_t>(1, std::min<int64_t>({sh.B, (int64_t)64, (2048 + blocks - 1) / blocks}));
+  *gs = (int)((sh.B + want - 1) / want);
+  *ng = (int)((sh.B + *gs - 1) / *gs);
+}
+
 bool backward_supported(const Shape& sh, int gate_kind) {
   return sh.k <= kBwMaxK && (gate_kind != MOCE_GATE_MLP_SIGMOID || sh.k <= kMlpBwMaxK);
 }
@@ -590,7 +636,7 @@ hipError_t launch_backward(const Shape& sh, const void* x, const void* dy, const
   if (R > 0) {
     const int64_t n = (int64_t)R * k;
     k_inv_fill<<<blocks_for(n, 256), 256, 0, st>>>(s, n, ws.cur, ws.inv);
-    k_inv_sort<<<blocks_for(C, 256), 256, 0, st>>>(ws.off, ws.inv, C);
+    k_inv_sort<<<blocks_for(C, 4), 256, 0, st>>>(ws.off, ws.inv, C);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     // forward quantities: d, the softmax statistics and the coefficients
     if ((err = launch_pool(sh, x, ws.d, st)) != hipSuccess) return err;
@@ -659,9 +705,17 @@ hipError_t launch_backward(const Shape& sh, const void* x, const void* dy, const
       k_bw_mlp_reduce<<<blocks_for(nq, 256), 256, 0, st>>>(ws.part, nparts, k, gg.dW1, gg.db1, gg.dw2, gg.db2);
       if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    k_bw_sums<<<blocks_for((int64_t)R * k, kBwThreads), kBwThreads, 0, st>>>(
-        ws.dal, w, ws.stats, ws.S1, ws.dg, ws.d, s, dw, mlp ? nullptr : gg.da, B, C, R, k);
-    if (!mlp) k_bw_dc<<<blocks_for(R, 256), 256, 0, st>>>(ws.dg, gg.dc, B, R);
+    {
+      int ng, gs;
+      backward_sum_groups(sh, &ng, &gs);
+      const int64_t rk = (int64_t)R * k;
+      k_bw_sums<<<dim3(blocks_for(rk, kBwThreads), ng), kBwThreads, 0, st>>>(
+          ws.dal, w, ws.stats, ws.S1, ws.dg, ws.d, s, ws.psum, ws.psum + ng * rk, ws.psum + 2 * ng * rk, B, C, R, k,
+          gs, !mlp);
+      k_bw_sums_reduce<<<blocks_for(std::max<int64_t>(rk, R), 256), 256, 0, st>>>(
+          ws.psum, ws.psum + ng * rk, ws.psum + 2 * ng * rk, ng, rk, R, dw, mlp ? nullptr : gg.da,
+          mlp ? nullptr : gg.dc);
+    }
     k_bw_dd<<<blocks_for(B * C, kBwThreads), kBwThreads, 0, st>>>(ws.off, ws.inv, ws.dg, mlp ? nullptr : g.a,
                                                                    ws.dzg, ws.dd, B, C, R, k);
     if ((err = hipGetLastError()) != hipSuccess) return err;

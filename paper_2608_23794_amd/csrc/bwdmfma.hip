@@ -399,12 +399,27 @@ __device__ __forceinline__ bool dxs_entry(int64_t t, const int32_t* s, const int
   return true;
 }
 
-__global__ void k_dxs_count(const int32_t* __restrict__ s, const int32_t* __restrict__ cnt, int R, int k, int C,
-                            int nEC, int32_t* __restrict__ bcnt) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)R * k + C) return;
-  int key, c, e;
-  if (dxs_entry(t, s, cnt, R, k, nEC, &key, &c, &e)) atomicAdd(&bcnt[key], 1);
+// Bucket counts, aggregated per workgroup in LDS (one global atomic per
+// bucket and workgroup): kDxEntPerBlock entries per workgroup.
+constexpr int kDxEntPerBlock = 4096;
+constexpr int kDxMaxBuckets = 4096;
+
+__global__ void __launch_bounds__(256)
+k_dxs_count(const int32_t* __restrict__ s, const int32_t* __restrict__ cnt, int R, int k, int C, int nEC, int nb,
+            int32_t* __restrict__ bcnt) {
+  __shared__ int32_t local[kDxMaxBuckets];
+  for (int i = threadIdx.x; i < nb; i += 256) local[i] = 0;
+  __syncthreads();
+  const int64_t n = (int64_t)R * k + C;
+  const int64_t t0 = (int64_t)blockIdx.x * kDxEntPerBlock;
+  for (int j = threadIdx.x; j < kDxEntPerBlock; j += 256) {
+    const int64_t t = t0 + j;
+    int key, c, e;
+    if (t < n && dxs_entry(t, s, cnt, R, k, nEC, &key, &c, &e)) atomicAdd(&local[key], 1);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nb; i += 256)
+    if (local[i]) atomicAdd(&bcnt[i], local[i]);
 }
 
 // one thread: exclusive scan of the bucket counts into boff[0..nb], bcur = boff
@@ -420,16 +435,35 @@ __global__ void k_dxs_scan(const int32_t* __restrict__ bcnt, int nb, int32_t* __
   boff[nb] = run;
 }
 
-// w0 = channel within the block | expert within the chunk << 8; w1 = entry (e k + i) or -1 (residual)
-__global__ void k_dxs_place(const int32_t* __restrict__ s, const int32_t* __restrict__ cnt, int R, int k, int C,
-                            int nEC, int32_t* __restrict__ bcur, uint32_t* __restrict__ w0, int32_t* __restrict__ w1) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)R * k + C) return;
-  int key, c, e;
-  if (!dxs_entry(t, s, cnt, R, k, nEC, &key, &c, &e)) return;
-  const int pos = atomicAdd(&bcur[key], 1);
-  w0[pos] = (uint32_t)(c % kDxCt) | ((uint32_t)(e % kDxEk) << 8);
-  w1[pos] = t < (int64_t)R * k ? (int32_t)t : -1;
+// w0 = channel within the block | expert within the chunk << 8; w1 = entry
+// (e k + i) or -1 (residual).  Each workgroup reserves one range per bucket
+// and places its entries inside it (the order within a bucket is free: every
+// entry has its own place in the coefficient tile).
+__global__ void __launch_bounds__(256)
+k_dxs_place(const int32_t* __restrict__ s, const int32_t* __restrict__ cnt, int R, int k, int C, int nEC, int nb,
+            int32_t* __restrict__ bcur, uint32_t* __restrict__ w0, int32_t* __restrict__ w1) {
+  __shared__ int32_t local[kDxMaxBuckets];
+  for (int i = threadIdx.x; i < nb; i += 256) local[i] = 0;
+  __syncthreads();
+  const int64_t n = (int64_t)R * k + C;
+  const int64_t t0 = (int64_t)blockIdx.x * kDxEntPerBlock;
+  for (int j = threadIdx.x; j < kDxEntPerBlock; j += 256) {
+    const int64_t t = t0 + j;
+    int key, c, e;
+    if (t < n && dxs_entry(t, s, cnt, R, k, nEC, &key, &c, &e)) atomicAdd(&local[key], 1);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nb; i += 256) local[i] = local[i] ? atomicAdd(&bcur[i], local[i]) : 0;
+  __syncthreads();
+  for (int j = threadIdx.x; j < kDxEntPerBlock; j += 256) {
+    const int64_t t = t0 + j;
+    int key, c, e;
+    if (t < n && dxs_entry(t, s, cnt, R, k, nEC, &key, &c, &e)) {
+      const int pos = atomicAdd(&local[key], 1);
+      w0[pos] = (uint32_t)(c % kDxCt) | ((uint32_t)(e % kDxEk) << 8);
+      w1[pos] = t < (int64_t)R * k ? (int32_t)t : -1;
+    }
+  }
 }
 
 // the two bf16 parts of each scheduled entry's coefficient, per image
@@ -714,6 +748,7 @@ k_bwd_dx_mfma(const uint16_t* __restrict__ dy, uint16_t* __restrict__ dx, const 
 
 bool dx_mfma_eligible(const Shape& sh) {
   if (sh.elem != MOCE_BF16 || sh.R < 1) return false;
+  if ((sh.C + kDxCt - 1) / kDxCt * ((sh.E + kDxEk - 1) / kDxEk) > kDxMaxBuckets) return false;
   if (sh.layout == MOCE_NHWC) return sh.E % 8 == 0;
   return sh.HW % 4 == 0;
 }
@@ -737,10 +772,10 @@ bool bwd_mfma_dx(const Shape& sh, const void* dy, const int32_t* s, const float*
   const int nCB = (int)((sh.C + kDxCt - 1) / kDxCt);
   k_dxs_fill<<<(nb + 255) / 256, 256, 0, st>>>(ws.dxs_cnt, nb);
   const int64_t nt = NEmax;
-  k_dxs_count<<<(unsigned)((nt + 255) / 256), 256, 0, st>>>(s, ws.cnt, sh.R, sh.k, (int)sh.C, nECb, ws.dxs_cnt);
+  const unsigned gb = (unsigned)((nt + kDxEntPerBlock - 1) / kDxEntPerBlock);
+  k_dxs_count<<<gb, 256, 0, st>>>(s, ws.cnt, sh.R, sh.k, (int)sh.C, nECb, nb, ws.dxs_cnt);
   k_dxs_scan<<<1, 64, 0, st>>>(ws.dxs_cnt, nb, ws.dxs_off, ws.dxs_cur);
-  k_dxs_place<<<(unsigned)((nt + 255) / 256), 256, 0, st>>>(s, ws.cnt, sh.R, sh.k, (int)sh.C, nECb, ws.dxs_cur,
-                                                            ws.dxs_w0, ws.dxs_w1);
+  k_dxs_place<<<gb, 256, 0, st>>>(s, ws.cnt, sh.R, sh.k, (int)sh.C, nECb, nb, ws.dxs_cur, ws.dxs_w0, ws.dxs_w1);
   k_dxs_alpha<<<dim3((unsigned)((NEmax + 255) / 256), (unsigned)sh.B), 256, 0, st>>>(
       ws.dxs_w1, ws.dxs_off, nb, w, ws.stats, ws.nU, sh.B, sh.R, sh.k, NEmax, ws.dxs_coef);
   if ((*err = hipGetLastError()) != hipSuccess) return true;

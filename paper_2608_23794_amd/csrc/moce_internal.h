@@ -207,7 +207,10 @@ struct BwdWs {
   uint32_t* dxs_w0;
   int32_t* dxs_w1;
   uint32_t* dxs_coef;
+  // partial sums over image groups: dw, da [ng][R k], dc [ng][R]
+  float* psum;
 };
+void backward_sum_groups(const Shape& sh, int* ng, int* gs);
 bool backward_supported(const Shape& sh, int gate_kind);
 size_t backward_mlp_parts(const Shape& sh);
 size_t backward_mlp_part_floats(const Shape& sh);
