@@ -307,6 +307,30 @@ def dynamic_us(bn, n_g=10, reps=5):
     return t
 
 
+def backward_us(bn, n_g=5, reps=5):
+    """moce_backward (dx, dw and the gate's gradients for a random upstream dy) timed like the
+    forward: HIP graph of n_g calls over the rotating input sets, median of reps replays.
+    Returns (latency in ms, compulsory bytes: x and dy read once, dx written once)."""
+    import torch
+    layer = bn.layer
+    x0 = bn.xs[0]
+    dy = torch.randn(layer.y_shape(bn.B), device="cuda").to(x0.dtype)
+    dx = torch.empty_like(x0)
+    ws = layer.new_backward_workspace(bn.B)
+    t = quartiles(graph_times_ms(lambda i, st=None: layer.backward(bn.xs[i % bn.nsets], dy, dx, ws), n_g, reps))[1]
+    nbytes = 2 * x0.numel() * x0.element_size() + dy.numel() * dy.element_size()
+    del ws, dx, dy
+    torch.cuda.empty_cache()
+    return t, nbytes
+
+
+def backward_entry(bn, fwd_ms):
+    t, nbytes = backward_us(bn)
+    return {"latency_us": round(t * 1e3, 2), "compulsory_bytes": nbytes, "GBps": round(nbytes / (t * 1e-3) / 1e9, 1),
+            "over_forward": round(t / fwd_ms, 2),
+            "timing": "HIP graph of 5 calls, median of 5 replays; dx, dw and the softplus-linear gate's gradients"}
+
+
 def other_config(name, layout, args, stream):
     bn = Bench(name, layout, args.rotate_gib)
     mb, wl = bn.mb, bn.wl
@@ -335,6 +359,7 @@ def other_config(name, layout, args, stream):
     t_dyn = dynamic_us(bn)
     out["dynamic_supports"] = {"latency_us": round(t_dyn * 1e3, 2), "over_static": round(t_dyn / med, 2),
                                "router_width": 32}
+    out["backward"] = backward_entry(bn, med)
     if not args.no_context:
         out["context"] = bn.dense_context(max(args.steps // 4, 10), stream)
         out["context"]["moce_over_dense_time"] = round(med * 1e3 / out["context"]["dense_1x1_us"], 3)
@@ -447,6 +472,7 @@ def main():
     line["dynamic_supports"] = {"latency_us": round(t_dyn * 1e3, 2), "over_static": round(t_dyn / fwd_graph, 2),
                                 "router_width": 32,
                                 "timing": "HIP graph of 10 forwards, median of 5 replays; over the static graph latency"}
+    line["backward"] = backward_entry(bn, fwd_graph)
     if not args.no_context:
         line["context"] = bn.dense_context(max(args.steps // 2, 10), stream)
         line["context"]["moce_over_dense_time"] = round(ms * 1e3 / line["context"]["dense_1x1_us"], 3)
