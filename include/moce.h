@@ -163,8 +163,8 @@ enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1, MOCE_PATH_MFMA = 2, MOCE_PATH_
  * MOCE_PATH_MFMA for MOCE_PATH_MFMA_GATE, MOCE_PATH_GENERIC for
  * MOCE_PATH_SCHEDULED):
  *  MOCE_PATH_SCHEDULED: channels-last bfloat16 (C a multiple of 64 up to
- *     8192, E a multiple of 8): pooling, the gate's softmax statistics, then
- *     a schedule of the supports by 32-channel step (Sec. 3.2: static
+ *     4096, E a multiple of 8): pooling, the gate's softmax statistics, then
+ *     a schedule of the supports by 64-channel step (Sec. 3.2: static
  *     supports) and the routed and residual outputs as a dense bf16 product
  *     on the matrix cores whose coefficient operand is written step by step
  *     from the schedule (coefficients split into two bf16 parts: 16
@@ -214,7 +214,7 @@ moce_status moce_forward_static(const moce_desc* desc, const void* x, const int3
                                 const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
                                 hipStream_t stream);
 
-/* Router of the input-conditioned support variant (Sec. 5 Eq. 11).  From the
+/* Router of the input-conditioned support variant (Sec. 4.5 Eq. 11).  From the
  * pooled descriptor z of an example, h = ReLU(Wh z + bh) (d values), and the
  * example's routing logits are L(X)[e][c] = L[e][c] + sum_t q[e][t] h[t] v[c][t]
  * over the full static routing logits L[E-1][C]. */
@@ -231,7 +231,7 @@ typedef struct moce_router {
  * descriptor or router width). */
 size_t moce_forward_dynamic_workspace_bytes(const moce_desc* desc, int32_t d);
 
-/* The layer with input-conditioned supports (Sec. 5 Eq. 11), inference path.
+/* The layer with input-conditioned supports (Sec. 4.5 Eq. 11), inference path.
  * Per example b: z = GAP(x_b); L(X) as above; S_e(X) = the k channels of
  * largest L(X)[e][.], equal logits by ascending channel, in canonical order
  * (logit descending, then channel ascending); the gate reads z at S_e(X) in

@@ -217,7 +217,7 @@ def forward(x: np.ndarray, s: np.ndarray, w: np.ndarray, E: int, layout: int = N
 
 
 # ---------------------------------------------------------------------------
-# Input-conditioned (dynamic) support, Sec. 5 Eq. 11
+# Input-conditioned (dynamic) support, Sec. 4.5 Eq. 11
 
 def router(d: np.ndarray, Wh, bh) -> np.ndarray:
     """The router's bottleneck h = ReLU(Wh d + bh) per example, [B, dd] (float64)."""

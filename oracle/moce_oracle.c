@@ -241,7 +241,7 @@ void moce_oracle_mix(int B, int C, int E, int k, int HW, int layout, int elem,
 }
 
 /* ------------------------------------------------------------------------ */
-/* Input-conditioned (dynamic) support (Sec. 5, Eq. 11)                     */
+/* Input-conditioned (dynamic) support (Sec. 4.5, Eq. 11)                     */
 
 /* h[b][t] = ReLU(bh[t] + sum_c Wh[t][c] d[b][c]), the router's bottleneck. */
 void moce_oracle_router(int B, int C, int dd, const double* d, const float* Wh,

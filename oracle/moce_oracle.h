@@ -68,7 +68,7 @@ int moce_oracle_threads(void);
 void moce_oracle_set_threads(int n);
 
 
-/* Input-conditioned support (Sec. 5, Eq. 11).  The router's bottleneck
+/* Input-conditioned support (Sec. 4.5, Eq. 11).  The router's bottleneck
  * h[B][dd] = ReLU(Wh d + bh) from the descriptor d[B][C]; the example's
  * routing logits Lx[B][R][C] = L[R][C] + ((q[e] * h[b]) . v[c]); per row the k
  * largest logits in canonical order (ties to the lower channel) as channels

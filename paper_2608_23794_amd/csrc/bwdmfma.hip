@@ -121,9 +121,9 @@ k_bwd_dalpha_mfma(const uint16_t* __restrict__ x, const uint16_t* __restrict__ d
     const int pb = sp * split_len, pe = min(HW, pb + split_len);
     return (pe - pb + kDaKs - 1) / kDaKs;
   };
-  uint32_t reg[Cf::LPT][Cf::WORDS];
+  typedef uint32_t Regs[Cf::LPT][Cf::WORDS];
   // global -> registers for step ks of unit u (zeros outside the positions, experts and channels)
-  auto load = [&](int u, int ks) {
+  auto load = [&](int u, int ks, Regs& reg) {
     const int b = u / nsplit, sp = u - b * nsplit;
     const int pb = sp * split_len, pe = min(HW, pb + split_len);
     const int p0 = pb + ks * kDaKs;
@@ -176,7 +176,7 @@ k_bwd_dalpha_mfma(const uint16_t* __restrict__ x, const uint16_t* __restrict__ d
     }
   };
   // registers -> LDS stage buffer
-  auto store = [&](unsigned char* stg) {
+  auto store = [&](unsigned char* stg, const Regs& reg) {
 #pragma unroll
     for (int j = 0; j < Cf::LPT; ++j) {
       const int q = tid + j * T;
@@ -230,21 +230,29 @@ k_bwd_dalpha_mfma(const uint16_t* __restrict__ x, const uint16_t* __restrict__ d
 #pragma unroll
     for (int nc = 0; nc < 4; ++nc) acc[me][nc] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  int u = g, ks = 0, cur = 0;
-  if (u < nunits) {
-    load(u, 0);
-    store(stage0);
-  }
-  __syncthreads();  // the table and the first step
-  while (u < nunits) {
-    const int nks = unit_steps(u);
-    int nu = u, nks1 = ks + 1;
-    if (nks1 >= nks) {
-      nu = u + G;
-      nks1 = 0;
+  // steps as (unit, step within the unit); u >= nunits: past the end
+  auto advance = [&](int& su, int& sk) {
+    if (su >= nunits) return;
+    if (++sk >= unit_steps(su)) {
+      su += G;
+      sk = 0;
     }
-    const bool more = nu < nunits;
-    if (more) load(nu, nks1);
+  };
+  // step i is multiplied from LDS buffer i & 1 while step i + 1 waits in
+  // registers (loaded an iteration earlier) and step i + 2 is being loaded
+  Regs r0, r1;
+  int u = g, ks = 0;             // step i
+  int u1 = u, k1 = ks;           // step i + 1
+  advance(u1, k1);
+  int u2 = u1, k2 = k1;          // step i + 2
+  advance(u2, k2);
+  load(u, ks, r0);
+  store(stage0, r0);
+  if (u1 < nunits) load(u1, k1, r1);
+  __syncthreads();  // the table and the first step
+  int cur = 0;
+  auto body = [&](Regs& rfree, Regs& rnext) {
+    if (u2 < nunits) load(u2, k2, rfree);
     const unsigned char* stg = stage0 + cur * Cf::Stage;
     bf16x8 a[4], bb[4];
 #pragma unroll
@@ -256,7 +264,7 @@ k_bwd_dalpha_mfma(const uint16_t* __restrict__ x, const uint16_t* __restrict__ d
 #pragma unroll
       for (int nc = 0; nc < 4; ++nc)
         acc[me][nc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[me], bb[nc], acc[me][nc], 0, 0, 0);
-    if (ks + 1 == nks) {
+    if (ks + 1 == unit_steps(u)) {
       // ---- the support entries of unit u out of the accumulators
       const int b = u / nsplit, sp = u - b * nsplit;
       float* out = dal + (((int64_t)sp * B + b) * R) * k;
@@ -276,11 +284,19 @@ k_bwd_dalpha_mfma(const uint16_t* __restrict__ x, const uint16_t* __restrict__ d
           acc[me][nc] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
     }
-    if (more) store(stage0 + (cur ^ 1) * Cf::Stage);
+    if (u1 < nunits) store(stage0 + (cur ^ 1) * Cf::Stage, rnext);
     __syncthreads();
     cur ^= 1;
-    u = nu;
-    ks = nks1;
+    u = u1;
+    ks = k1;
+    u1 = u2;
+    k1 = k2;
+    advance(u2, k2);
+  };
+  while (u < nunits) {
+    body(r0, r1);   // r0 held step i (already in LDS); step i + 1 sits in r1
+    if (u >= nunits) break;
+    body(r1, r0);
   }
 }
 

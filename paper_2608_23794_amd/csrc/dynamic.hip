@@ -1,4 +1,4 @@
-// Input-conditioned supports (Sec. 5, Eq. 11), the inference path.
+// Input-conditioned supports (Sec. 4.5, Eq. 11), the inference path.
 //
 // The variant keeps the temperature gate and the residual, and replaces the
 // static supports by per-example ones: a router reads the whole pooled

@@ -6,14 +6,14 @@
 // For one image b the routed outputs (Sec. 3.3 Eq. 5) and the residual output
 // (Sec. 3.4 Eq. 6) are y_b = A_b x_b, with row o < E-1 of A_b holding
 // alpha[b][o][i] at column s[o][i] and row E-1 holding 1/|U| at the uncovered
-// channels.  With x channels-last, a tile of positions x 32 channels is
-// already the layout of the MFMA's A operand, so this kernel evaluates
-// y^T = x^T A_b^T with 16x16x32 bf16 MFMAs over 32-channel steps, positions
+// channels.  With x channels-last, a tile of positions x 64 channels is
+// already the layout of the MFMA's A operand (two K slices), so this kernel
+// evaluates y^T = x^T A_b^T with 16x16x32 bf16 MFMAs over 64-channel steps, positions
 // as M and experts as N.  A_b is 1/16 dense at the ResNet-50 stage-3/4 and
 // ViT shapes; the matrix cores still run the dense product faster than the
 // vector ALUs run the gather form.
 //
-// The schedule.  Dense A_b is never built: per 32-channel step only the
+// The schedule.  Dense A_b is never built: per 64-channel step only the
 // support entries whose channel falls in the step are written into zeroed LDS
 // rows of A_b^T (the B operand), and they are cleared again two steps later,
 // before the next entries go into the same buffer.  A small kernel (k_sched)

@@ -196,7 +196,7 @@ def generate(wl: Workload, layout: Optional[str] = None, with_x: bool = True,
 
 
 def router_params(wl: Workload, d: int = 32) -> Dict[str, np.ndarray]:
-    """Synthetic parameters of the input-conditioned variant (Sec. 5 Eq. 11)
+    """Synthetic parameters of the input-conditioned variant (Sec. 4.5 Eq. 11)
     for ``wl``: the full static routing logits ``L[E-1, C] ~ N(0, 1)`` and the
     router ``Wh[d, C] ~ N(0, 4/C)``, ``bh[d] ~ N(0, 0.1^2)``, channel
     embeddings ``v[C, d] ~ N(0, 1)`` and expert embeddings

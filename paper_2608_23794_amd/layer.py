@@ -196,7 +196,7 @@ class MoceLayer:
 
 
 class DynamicMoceLayer:
-    """The layer with input-conditioned supports (Sec. 5 Eq. 11): device
+    """The layer with input-conditioned supports (Sec. 4.5 Eq. 11): device
     copies of the full routing logits, the router and the gate, and the
     library's dynamic forward over them."""
 

@@ -1,4 +1,4 @@
-"""GPU parity of the input-conditioned (dynamic) support path (Sec. 5 Eq. 11) against the oracle.
+"""GPU parity of the input-conditioned (dynamic) support path (Sec. 4.5 Eq. 11) against the oracle.
 
 The selection is an integer decision taken from floating-point logits: the device forms the
 example's logits in float32 from its own pooled descriptor, the oracle in float64 from the exact one.

@@ -441,7 +441,7 @@ def test_mag_of_empty_residual_is_zero():
 
 
 # --------------------------------------------------------------------------- input-conditioned supports
-# Sec. 5 Eq. 11: h = ReLU(Wh z + bh), L(X)_{e,c} = L_{e,c} + <q_e * h, v_c>, S_e(X) = TopK(L(X)_e, k),
+# Sec. 4.5 Eq. 11: h = ReLU(Wh z + bh), L(X)_{e,c} = L_{e,c} + <q_e * h, v_c>, S_e(X) = TopK(L(X)_e, k),
 # U(X) the channels in no S_e(X); temperature and coefficients then follow the example's support.
 
 def _router_case(B=3, C=40, E=7, dd=5, seed=0):
