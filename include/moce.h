@@ -194,6 +194,32 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
                          const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y,
                          void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Output epilogue of moce_forward_ex: each output value v of channel o
+ * (routed or residual) becomes act(scale[o] v + shift[o]) before it is
+ * rounded and stored, act = ReLU when relu != 0 and the identity otherwise.
+ * scale, shift: device float32 [E], both given or both NULL (no affine map).
+ * The replaced projection is followed by batch normalisation and the block's
+ * nonlinearity, which the paper leaves unchanged (Sec. 4.1); at inference the
+ * normalisation is this affine map (scale = gamma / sqrt(var + eps),
+ * shift = beta - mean scale), and applying it as the output is written avoids
+ * a second pass over y, the memory-traffic fusion Sec. 4.7 points to. */
+typedef struct moce_epilogue {
+    const float* scale;
+    const float* shift;
+    int32_t relu;
+    int32_t reserved;     /* set to 0 */
+} moce_epilogue;
+
+/* moce_forward followed by the epilogue `ep` (NULL: none, then identical to
+ * moce_forward).  On the matrix-core paths (MOCE_PATH_MFMA, MOCE_PATH_MFMA_GATE,
+ * MOCE_PATH_SCHEDULED) the mix kernel applies it to the float32 accumulators
+ * before rounding; on the others a second kernel applies it to y in place
+ * (for bf16 y, to the rounded value).  Errors: those of moce_forward, and
+ * MOCE_ERR_NULL when exactly one of scale and shift is NULL. */
+moce_status moce_forward_ex(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
+                            const moce_gate_params* gate, const int32_t* U, int32_t nU, const moce_epilogue* ep,
+                            void* y, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Bytes of the device array that moce_forward_static uses as its workspace. */
 #define MOCE_STATIC_SCRATCH_BYTES ((size_t)16 << 20)
 

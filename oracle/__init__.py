@@ -216,6 +216,22 @@ def forward(x: np.ndarray, s: np.ndarray, w: np.ndarray, E: int, layout: int = N
             "alpha": alpha, "y": y, "mag": mag}
 
 
+def epilogue(y: np.ndarray, scale, shift, relu: bool, layout: int = NCHW) -> np.ndarray:
+    """The output epilogue of the replaced projection's block (Sec. 4.1: batch normalisation and the
+    block's nonlinearity follow the layer): per output channel o, act(scale[o] y + shift[o]) with act
+    = ReLU when ``relu``, in float64 on top of ``y`` (the layer's output, channel axis 1 for NCHW and
+    last for channels-last).  ``scale`` None means no affine map."""
+    y = np.asarray(y, np.float64)
+    if scale is not None:
+        sh = [1] * y.ndim
+        ax = 1 if layout == NCHW else y.ndim - 1
+        sh[ax] = -1
+        y = y * np.asarray(scale, np.float64).reshape(sh) + np.asarray(shift, np.float64).reshape(sh)
+    if relu:
+        y = np.maximum(y, 0.0)
+    return y
+
+
 # ---------------------------------------------------------------------------
 # Input-conditioned (dynamic) support, Sec. 4.5 Eq. 11
 

@@ -29,7 +29,7 @@ STATUS = {
 # Every function include/moce.h declares, in declaration order.
 ENTRY_POINTS = (
     "moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix",
-    "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_forward_static",
+    "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_forward_ex", "moce_forward_static",
     "moce_forward_dynamic_workspace_bytes", "moce_forward_dynamic", "moce_backward_workspace_bytes",
     "moce_backward", "moce_logit_backward_workspace_bytes", "moce_logit_backward", "moce_status_str",
     "moce_abi_version",
@@ -63,6 +63,11 @@ class moce_gate_params(ctypes.Structure):
                 ("b2", ctypes.c_float), ("tau_min", ctypes.c_float), ("tau_max", ctypes.c_float)]
 
 
+class moce_epilogue(ctypes.Structure):
+    _fields_ = [("scale", ctypes.c_void_p), ("shift", ctypes.c_void_p), ("relu", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
 class moce_gate_grads(ctypes.Structure):
     _fields_ = [("da", ctypes.c_void_p), ("dc", ctypes.c_void_p), ("dW1", ctypes.c_void_p),
                 ("db1", ctypes.c_void_p), ("dw2", ctypes.c_void_p), ("db2", ctypes.c_void_p)]
@@ -94,6 +99,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_forward_workspace_bytes.restype = SZ
     lib.moce_forward_path.argtypes = [D, ctypes.c_int]
     lib.moce_forward.argtypes = [D, P, P, P, G, P, I32, P, P, SZ, P]
+    lib.moce_forward_ex.argtypes = [D, P, P, P, G, P, I32, ctypes.POINTER(moce_epilogue), P, P, SZ, P]
     lib.moce_forward_static.argtypes = [D, P, P, P, G, P, I32, P, P]
     lib.moce_forward_dynamic_workspace_bytes.argtypes = [D, I32]
     lib.moce_forward_dynamic_workspace_bytes.restype = SZ
@@ -108,7 +114,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_status_str.argtypes = [ctypes.c_int]
     lib.moce_status_str.restype = ctypes.c_char_p
     lib.moce_abi_version.restype = ctypes.c_int
-    for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward",
+    for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward", "moce_forward_ex",
                  "moce_forward_static", "moce_forward_dynamic", "moce_backward", "moce_logit_backward"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
@@ -205,6 +211,19 @@ def moce_forward(desc: moce_desc, x, s, w, gate: moce_gate_params, U, nU: int, y
     _check("moce_forward", load().moce_forward(ctypes.byref(desc), _ptr(x), _ptr(s), _ptr(w),
                                                ctypes.byref(gate), _ptr(U), nU, _ptr(y), _ptr(ws),
                                                ws_bytes, _stream(stream)))
+
+
+def make_epilogue(scale=None, shift=None, relu: bool = False) -> moce_epilogue:
+    """An epilogue struct over device arrays (they must outlive its use)."""
+    return moce_epilogue(_ptr(scale), _ptr(shift), 1 if relu else 0, 0)
+
+
+def moce_forward_ex(desc: moce_desc, x, s, w, gate: moce_gate_params, U, nU: int, ep: Optional[moce_epilogue], y, ws,
+                    ws_bytes: int, stream=None) -> None:
+    _check("moce_forward_ex", load().moce_forward_ex(ctypes.byref(desc), _ptr(x), _ptr(s), _ptr(w),
+                                                     ctypes.byref(gate), _ptr(U), nU,
+                                                     ctypes.byref(ep) if ep is not None else None, _ptr(y),
+                                                     _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def moce_forward_static(desc: moce_desc, x, s, w, gate: moce_gate_params, U, nU: int, y, stream=None) -> None:

@@ -229,7 +229,7 @@ moce_status check_forward(const moce_desc* desc, const void* x, const int32_t* s
 // (device memory of at least ws_layout(sh).total bytes, 256-byte aligned).
 moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, const float* w,
                            const moce_gate_params* gate, const int32_t* U, int32_t nU, void* y, void* ws,
-                           hipStream_t stream) {
+                           hipStream_t stream, const moce::Epi& ep = moce::Epi{}) {
   const WsLayout l = ws_layout(sh);
   char* base = static_cast<char*>(ws);
   float* d = reinterpret_cast<float*>(base + l.d);
@@ -246,17 +246,19 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
     // k = 32 with the softplus-linear gate: the mix kernel evaluates the
     // gate itself, in the gate kernel's layout and operations
     if (moce::mfmamix_gate_fusable(sh, gate->kind))
-      return device_status(moce::launch_mfmamix_gated(sh, x, s, w, d, gate->a, gate->c, U, nU, y, stream));
+      return device_status(moce::launch_mfmamix_gated(sh, x, s, w, d, gate->a, gate->c, U, nU, y, stream, ep));
     e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, nullptr, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
-    return device_status(moce::launch_mfmamix(sh, x, s, alpha, U, nU, y, stream));
+    return device_status(moce::launch_mfmamix(sh, x, s, alpha, U, nU, y, stream, ep));
   }
   if (sh.R > 0 && moce::tilemix_eligible(sh)) {
     hipError_t e = moce::launch_pool(sh, x, d, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
     e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, nullptr, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
-    return device_status(moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream));
+    e = moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    return device_status(moce::launch_epilogue(sh, y, ep, stream));
   }
   if (moce::gmix_eligible(sh)) {
     // channels-last on the matrix cores: pooling with the support schedule
@@ -265,7 +267,7 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
     e = moce::launch_gate(sh, d, s, w, *gate, tau, nullptr, stats, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
-    return device_status(moce::launch_gmix(sh, x, stats, nU, base + l.sched, y, stream));
+    return device_status(moce::launch_gmix(sh, x, stats, nU, base + l.sched, y, stream, ep));
   }
   hipError_t e = moce::launch_pool(sh, x, d, stream);
   if (e != hipSuccess) return MOCE_ERR_DEVICE;
@@ -274,7 +276,8 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
   }
   e = moce::launch_mix(sh, x, s, alpha, w, stats, U, nU, y, stream);
-  return device_status(e);
+  if (e != hipSuccess) return MOCE_ERR_DEVICE;
+  return device_status(moce::launch_epilogue(sh, y, ep, stream));
 }
 
 // ---- the forward without a workspace argument ------------------------------
@@ -318,6 +321,22 @@ moce_status moce_forward(const moce_desc* desc, const void* x, const int32_t* s,
   if (!ws || ws_bytes < ws_layout(sh).total) return MOCE_ERR_WORKSPACE;
   if (!aligned(ws, kAlign)) return MOCE_ERR_ALIGN;
   return forward_launch(sh, x, s, w, gate, U, nU, y, ws, stream);
+}
+
+moce_status moce_forward_ex(const moce_desc* desc, const void* x, const int32_t* s, const float* w,
+                            const moce_gate_params* gate, const int32_t* U, int32_t nU, const moce_epilogue* ep,
+                            void* y, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Shape sh;
+  const moce_status st = check_forward(desc, x, s, w, gate, U, nU, y, &sh);
+  if (st != MOCE_OK) return st;
+  moce::Epi e{};
+  if (ep) {
+    if ((ep->scale == nullptr) != (ep->shift == nullptr)) return MOCE_ERR_NULL;
+    e = moce::Epi{ep->scale, ep->shift, ep->relu != 0 ? 1 : 0};
+  }
+  if (!ws || ws_bytes < ws_layout(sh).total) return MOCE_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return MOCE_ERR_ALIGN;
+  return forward_launch(sh, x, s, w, gate, U, nU, y, ws, stream, e);
 }
 
 moce_status moce_forward_static(const moce_desc* desc, const void* x, const int32_t* s, const float* w,

@@ -113,6 +113,7 @@ struct GmArgs {
   int nt, nq;           // position tiles per image, expert ranges per image
   int units, per;       // work units, units per XCD slot
   float inv_nU;
+  Epi ep;               // output epilogue, applied to the accumulators before rounding
 };
 
 // ---------------------------------------------------------------- schedule
@@ -272,7 +273,7 @@ __device__ __forceinline__ int unit_of(const GmArgs& p) {
 }
 
 template <int MB, int NB, int NS, int OCC>
-__device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, int wv) {
+__device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, int wv, int o0) {
   using L = Layout<MB, NB, NS, OCC>;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, n = lane & 15;
@@ -358,7 +359,8 @@ __device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, i
       for (int r = 0; r < 4; ++r) {
         const int row = 16 * mb + 4 * g + r;
         const int col = 16 * (NB * wv + nb) + n;
-        *reinterpret_cast<uint16_t*>(stg + row * L::OROW + col * 2) = f32_to_bf16(acc[mb][nb][r]);
+        *reinterpret_cast<uint16_t*>(stg + row * L::OROW + col * 2) =
+            f32_to_bf16(epi_apply(p.ep, acc[mb][nb][r], min(o0 + col, p.E - 1)));
       }
 }
 
@@ -564,7 +566,7 @@ k_gmix(GmArgs p) {
   const int p0 = jt * L::MT, o0 = q * L::NE;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (wv < kConsumers)
-    consumer<MB, NB, NS, OCC>(p, smem, wv);
+    consumer<MB, NB, NS, OCC>(p, smem, wv, o0);
   else if (wv < kConsumers + kBuilders)
     builder<MB, NB, NS, OCC>(p, smem, wv - kConsumers, b, q);
   else
@@ -691,7 +693,7 @@ hipError_t launch_pool_sched(const Shape& sh, const void* x, float* d, const int
 }
 
 hipError_t launch_gmix(const Shape& sh, const void* x, const float* stats, int nU, const void* sched, void* y,
-                       hipStream_t st) {
+                       hipStream_t st, const Epi& ep) {
   const Variant* v = pick(sh);
   if (!v) return hipErrorInvalidValue;
   const SchedShape ss = sched_shape(sh, *v);
@@ -715,6 +717,7 @@ hipError_t launch_gmix(const Shape& sh, const void* x, const float* stats, int n
   p.units = (int)(sh.B * p.nt * p.nq);
   p.per = (p.units + 7) / 8;
   p.inv_nU = nU > 0 ? 1.f / (float)nU : 0.f;
+  p.ep = ep;
   const size_t lds = v->lds();
   hipError_t e = hipFuncSetAttribute((const void*)v->k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;

@@ -85,6 +85,7 @@ constexpr int kCachePolicyNT = 2;
 
 struct MixArgs {
   int C, HW, E, R, k, nU, nt, ntiles;
+  Epi ep;   // output epilogue, applied to the accumulators before rounding
 };
 
 // LDS: the ring of x tiles [C][kTile] bf16, each consumer wave's A_b staging
@@ -586,6 +587,10 @@ __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __rest
   // results: row sl of the wave's block, bytes 32 pb + 8 g (chunk 2 pb +
   // (g >> 1) before the row's swizzle)
   const int cres = cw * kOutWave + sl * kRow + 8 * (g & 1);
+  // the output epilogue's constants of this lane's expert
+  const bool epi = epi_active(p.ep);
+  const int eo = min(kExpertsPerWave * cw + sl, p.E - 1);
+  const float esc = p.ep.scale ? p.ep.scale[eo] : 1.f, esh = p.ep.scale ? p.ep.shift[eo] : 0.f;
 
   bf16x8 bfr[NS][NR];
   // the first build stages in the last ring buffer (4 x 16 rows of 2 C bytes)
@@ -659,6 +664,15 @@ __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __rest
       __builtin_amdgcn_sched_barrier(0);
     }
     unsigned char* ob = out_buffer(r, n) + cres;
+    if (epi) {
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float v = p.ep.scale ? __builtin_fmaf(acc[pb][q], esc, esh) : acc[pb][q];
+          acc[pb][q] = p.ep.relu ? fmaxf(v, 0.f) : v;
+        }
+    }
 #pragma unroll
     for (int pb = 0; pb < 4; ++pb)
       *reinterpret_cast<u32x2*>(ob + (((2 * pb + (g >> 1)) ^ (sl & 7)) << 4)) =
@@ -815,8 +829,9 @@ int cu_count() {
 namespace {
 
 hipError_t launch_mix_kernel(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
-                             int nU, const GateArgs* ga, void* y, hipStream_t st) {
-  const MixArgs p = mix_args(sh, nU);
+                             int nU, const GateArgs* ga, void* y, hipStream_t st, const Epi& ep) {
+  MixArgs p = mix_args(sh, nU);
+  p.ep = ep;
   if (p.ntiles == 0) return hipSuccess;
   const int grid = std::min(cu_count(), p.ntiles);
   const size_t lds = mfma_lds(p.C);
@@ -833,8 +848,8 @@ hipError_t launch_mix_kernel(const Shape& sh, const void* x, const int32_t* s, c
 }  // namespace
 
 hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
-                          int nU, void* y, hipStream_t st) {
-  return launch_mix_kernel(sh, x, s, alpha, U, nU, nullptr, y, st);
+                          int nU, void* y, hipStream_t st, const Epi& ep) {
+  return launch_mix_kernel(sh, x, s, alpha, U, nU, nullptr, y, st, ep);
 }
 
 bool mfmamix_gate_fusable(const Shape& sh, int gate_kind) {
@@ -842,9 +857,9 @@ bool mfmamix_gate_fusable(const Shape& sh, int gate_kind) {
 }
 
 hipError_t launch_mfmamix_gated(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* d,
-                                const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st) {
+                                const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st, const Epi& ep) {
   const GateArgs ga{d, w, a, c};
-  return launch_mix_kernel(sh, x, s, nullptr, U, nU, &ga, y, st);
+  return launch_mix_kernel(sh, x, s, nullptr, U, nU, &ga, y, st, ep);
 }
 
 }  // namespace moce

@@ -398,4 +398,40 @@ hipError_t launch_mix(const Shape& sh, const void* x, const int32_t* s, const fl
   return mix_typed(sh, static_cast<const uint16_t*>(x), static_cast<uint16_t*>(y), a, st);
 }
 
+namespace {
+
+// In place: y = act(scale[o] y + shift[o]) with o the output channel of each
+// element, a thread per element.
+template <typename T, bool NHWC>
+__global__ void k_epilogue(T* __restrict__ y, int64_t n, int E, int64_t HW, Epi ep) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int o = NHWC ? (int)(i % E) : (int)((i / HW) % E);
+    Elem<T>::store(y + i, epi_apply(ep, Elem<T>::load(y + i), o));
+  }
+}
+
+}  // namespace
+
+hipError_t launch_epilogue(const Shape& sh, void* y, const Epi& ep, hipStream_t st) {
+  if (!epi_active(ep)) return hipSuccess;
+  const int64_t n = sh.B * sh.E * sh.HW;
+  const unsigned grid = (unsigned)std::min<int64_t>((n + 255) / 256, 65536);
+  const bool nhwc = sh.layout == MOCE_NHWC;
+  if (sh.elem == MOCE_BF16) {
+    auto p = static_cast<uint16_t*>(y);
+    if (nhwc)
+      k_epilogue<uint16_t, true><<<grid, 256, 0, st>>>(p, n, sh.E, sh.HW, ep);
+    else
+      k_epilogue<uint16_t, false><<<grid, 256, 0, st>>>(p, n, sh.E, sh.HW, ep);
+  } else {
+    auto p = static_cast<float*>(y);
+    if (nhwc)
+      k_epilogue<float, true><<<grid, 256, 0, st>>>(p, n, sh.E, sh.HW, ep);
+    else
+      k_epilogue<float, false><<<grid, 256, 0, st>>>(p, n, sh.E, sh.HW, ep);
+  }
+  return hipGetLastError();
+}
+
 }  // namespace moce

@@ -107,6 +107,23 @@ __host__ __device__ inline Stats stats_planes(float* base, int64_t n, int64_t sb
   return Stats{base, base + n, base + 2 * n, sb, so};
 }
 
+// ---- output epilogue -------------------------------------------------------
+// y[.][o][.] = act(scale[o] v + shift[o]) applied to a float32 output value v
+// before it is rounded and stored: a per-output-channel affine map (a folded
+// inference batch norm) and an optional ReLU.  scale == nullptr: no affine
+// map.
+struct Epi {
+  const float* scale;
+  const float* shift;
+  int relu;
+};
+__device__ __forceinline__ float epi_apply(const Epi& e, float v, int o) {
+  if (e.scale) v = __builtin_fmaf(v, e.scale[o], e.shift[o]);
+  if (e.relu) v = fmaxf(v, 0.f);
+  return v;
+}
+__host__ __device__ inline bool epi_active(const Epi& e) { return e.scale != nullptr || e.relu != 0; }
+
 // ---- launch parameters derived from a validated descriptor ---------------
 struct Shape {
   int64_t B, C, HW;
@@ -145,13 +162,15 @@ hipError_t launch_tilemix(const Shape& sh, const void* x, const int32_t* s, cons
 // multiple of 8; supports must hold distinct channels (prepared rows).
 bool mfmamix_eligible(const Shape& sh);
 hipError_t launch_mfmamix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
-                          int nU, void* y, hipStream_t st);
+                          int nU, void* y, hipStream_t st,
+                   const Epi& ep = Epi{});
 // The same product with the softplus-linear gate evaluated inside the mix
 // kernel from the pooled descriptors d (bit-identical coefficients, no
 // temperatures or coefficients written), for k = 32.
 bool mfmamix_gate_fusable(const Shape& sh, int gate_kind);
 hipError_t launch_mfmamix_gated(const Shape& sh, const void* x, const int32_t* s, const float* w, const float* d,
-                                const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st);
+                                const float* a, const float* c, const int32_t* U, int nU, void* y, hipStream_t st,
+                   const Epi& ep = Epi{});
 
 // Channels-last bfloat16 mixing on the matrix cores from a per-forward
 // channel schedule of the supports (gmix.hip): C a multiple of 64 up to 4096,
@@ -163,8 +182,12 @@ bool gmix_eligible(const Shape& sh);
 size_t gmix_sched_bytes(const Shape& sh);
 hipError_t launch_pool_sched(const Shape& sh, const void* x, float* d, const int32_t* s, const float* w,
                              const int32_t* U, int nU, void* sched, hipStream_t st);
+// The epilogue applied in place to a finished y (the paths whose mix kernels
+// do not apply it themselves).
+hipError_t launch_epilogue(const Shape& sh, void* y, const Epi& ep, hipStream_t st);
 hipError_t launch_gmix(const Shape& sh, const void* x, const float* stats, int nU, const void* sched, void* y,
-                       hipStream_t st);
+                       hipStream_t st,
+                   const Epi& ep = Epi{});
 
 // Input-conditioned supports (dynamic.hip): the whole inference path from x
 // to y over workspace arrays: the router output h [B][d], the transposed

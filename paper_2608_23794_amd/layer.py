@@ -136,15 +136,23 @@ class MoceLayer:
         return torch.empty(max(self.workspace_bytes(B), 1), dtype=torch.uint8, device=self.device)
 
     def forward(self, x: torch.Tensor, y: Optional[torch.Tensor] = None,
-                ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+                ws: Optional[torch.Tensor] = None, epilogue=None) -> torch.Tensor:
+        """moce_forward, or with epilogue = (scale, shift, relu) moce_forward_ex (scale and shift: device
+        float32 [E] or both None)."""
         self._ready()
         B = x.shape[0]
         if y is None:
             y = torch.empty(self.y_shape(B), dtype=x.dtype, device=self.device)
         if ws is None:
             ws = self.new_workspace(B)
-        mb.moce_forward(self.desc(B), x, self.s_c, self.w_c, self.gate, self.U if self.nU else None, self.nU,
-                        y, ws, ws.numel(), self._stream())
+        if epilogue is None:
+            mb.moce_forward(self.desc(B), x, self.s_c, self.w_c, self.gate, self.U if self.nU else None, self.nU,
+                            y, ws, ws.numel(), self._stream())
+        else:
+            scale, shift, relu = epilogue
+            ep = mb.make_epilogue(scale, shift, relu)
+            mb.moce_forward_ex(self.desc(B), x, self.s_c, self.w_c, self.gate, self.U if self.nU else None,
+                               self.nU, ep, y, ws, ws.numel(), self._stream())
         return y
 
     # -- backward --------------------------------------------------------------

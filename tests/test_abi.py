@@ -342,3 +342,21 @@ def test_logit_backward_host_errors(lib):
     assert call(ws=FAKE_UNALIGNED) == -8
     assert lib.moce_logit_backward_workspace_bytes(0, 64) == 0
     assert lib.moce_logit_backward_workspace_bytes(4, 40000) == 0
+
+
+def test_forward_ex_host_errors(lib):
+    desc = good_desc()
+    gate = mb.make_gate(a=FAKE, c=FAKE)
+
+    def call(ep, ws=FAKE, ws_bytes=1 << 30):
+        e = ctypes.byref(ep) if ep is not None else None
+        return mb.raw_status("moce_forward_ex", ctypes.byref(desc), FAKE, FAKE, FAKE, ctypes.byref(gate), FAKE, 4, e,
+                             FAKE, ws, ws_bytes, None)
+    assert call(mb.moce_epilogue(FAKE, None, 0, 0)) == -1
+    assert call(mb.moce_epilogue(None, FAKE, 1, 0)) == -1
+    assert call(mb.moce_epilogue(FAKE, FAKE, 1, 0), ws=None) == -7
+    assert call(None, ws=None) == -7
+    for kw, code in BAD_DESCS:
+        d = good_desc(**kw)
+        assert mb.raw_status("moce_forward_ex", ctypes.byref(d), FAKE, FAKE, FAKE, ctypes.byref(gate), FAKE, 4, None,
+                             FAKE, FAKE, 1 << 30, None) == code, kw

@@ -562,3 +562,34 @@ def test_dynamic_forward_follows_the_example_support():
         ref = oracle.forward(x[b:b + 1], dyn["S"][b], dyn["W"][b].astype(np.float32), E, oracle.NCHW, a=a, c=c)
         np.testing.assert_allclose(dyn["y"][b:b + 1], ref["y"], rtol=1e-12, atol=1e-12)
         np.testing.assert_array_equal(dyn["U"][b], ref["U"])
+
+
+# --------------------------------------------------------------------------
+# Output epilogue (Sec. 4.1: batch normalisation and the nonlinearity after the layer)
+
+@pytest.mark.parametrize("layout", [oracle.NCHW, oracle.NHWC])
+def test_epilogue_identity_and_relu(layout):
+    rng = np.random.default_rng(0)
+    y = rng.standard_normal((2, 5, 3, 4) if layout == oracle.NCHW else (2, 3, 4, 5))
+    np.testing.assert_array_equal(oracle.epilogue(y, None, None, False, layout), y)
+    np.testing.assert_array_equal(oracle.epilogue(y, np.ones(5), np.zeros(5), False, layout), y)
+    np.testing.assert_array_equal(oracle.epilogue(y, None, None, True, layout), np.where(y > 0, y, 0.0))
+
+
+@pytest.mark.parametrize("layout", [oracle.NCHW, oracle.NHWC])
+def test_epilogue_acts_per_output_channel(layout):
+    """Channel o of the output gets scale[o] and shift[o], nothing else (one-hot scales pick one
+    channel in either layout)."""
+    rng = np.random.default_rng(1)
+    E = 6
+    y = rng.standard_normal((2, E, 3, 2) if layout == oracle.NCHW else (2, 3, 2, E))
+    for o in range(E):
+        sc = np.zeros(E)
+        sc[o] = 2.0
+        sf = np.zeros(E)
+        sf[o] = -1.0
+        out = oracle.epilogue(y, sc, sf, False, layout)
+        chan = (lambda a: a[:, o]) if layout == oracle.NCHW else (lambda a: a[..., o])
+        np.testing.assert_array_equal(chan(out), 2.0 * chan(y) - 1.0)
+        rest = np.delete(out, o, axis=1 if layout == oracle.NCHW else -1)
+        assert np.all(rest == 0.0)
