@@ -118,6 +118,17 @@ moce_status moce_support_prepare(const moce_desc* desc, const int32_t* s, const 
                                  int32_t* info, int32_t* nU_host, int32_t* bad_expert_host,
                                  hipStream_t stream);
 
+/* moce_support_prepare for supports kept in the deployment storage format:
+ * s[E-1][k] as 16-bit unsigned channel indices (Sec. 3.5, Storage: a
+ * deployed layer keeps its (E-1)k selected logits, their indices in 16 bits
+ * and the gate).  Same outputs (int32 prepared rows), checks and errors;
+ * MOCE_ERR_UNSUPPORTED when C > 65536.  This call synchronises `stream`
+ * once. */
+moce_status moce_support_prepare16(const moce_desc* desc, const uint16_t* s, const float* w,
+                                   int32_t* s_out, float* w_out, uint8_t* covered, int32_t* U,
+                                   int32_t* info, int32_t* nU_host, int32_t* bad_expert_host,
+                                   hipStream_t stream);
+
 /* Global average pooling descriptor z = GAP(x) (Sec. 3.3):
  * d[b][c] = (1 / (H W)) sum over positions of x[b][c][.]; d is [B][C] float32. */
 moce_status moce_pool(const moce_desc* desc, const void* x, float* d, hipStream_t stream);

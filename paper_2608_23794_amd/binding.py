@@ -28,7 +28,7 @@ STATUS = {
 
 # Every function include/moce.h declares, in declaration order.
 ENTRY_POINTS = (
-    "moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix",
+    "moce_support_prepare", "moce_support_prepare16", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix",
     "moce_forward_workspace_bytes", "moce_forward_path", "moce_forward", "moce_forward_ex", "moce_forward_static",
     "moce_forward_dynamic_workspace_bytes", "moce_forward_dynamic", "moce_backward_workspace_bytes",
     "moce_backward", "moce_logit_backward_workspace_bytes", "moce_logit_backward", "moce_status_str",
@@ -91,6 +91,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     G = ctypes.POINTER(moce_gate_params)
     IP = ctypes.POINTER(ctypes.c_int32)
     lib.moce_support_prepare.argtypes = [D, P, P, P, P, P, P, P, IP, IP, P]
+    lib.moce_support_prepare16.argtypes = [D, P, P, P, P, P, P, P, IP, IP, P]
     lib.moce_pool.argtypes = [D, P, P, P]
     lib.moce_gate.argtypes = [D, P, P, P, G, P, P, P]
     lib.moce_gate_mix.argtypes = [D, P, P, P, P, G, P, I32, P, P]
@@ -114,7 +115,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moce_status_str.argtypes = [ctypes.c_int]
     lib.moce_status_str.restype = ctypes.c_char_p
     lib.moce_abi_version.restype = ctypes.c_int
-    for name in ("moce_support_prepare", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward", "moce_forward_ex",
+    for name in ("moce_support_prepare", "moce_support_prepare16", "moce_pool", "moce_gate", "moce_gate_mix", "moce_mix", "moce_forward", "moce_forward_ex",
                  "moce_forward_static", "moce_forward_dynamic", "moce_backward", "moce_logit_backward"):
         getattr(lib, name).restype = ctypes.c_int
     if path is None:
@@ -168,6 +169,19 @@ def moce_support_prepare(desc: moce_desc, s, w, s_out, w_out, covered, U, info, 
                                      ctypes.byref(bad), _stream(stream))
     if check and st != 0:
         raise MoceError("moce_support_prepare", st, f"(first bad expert {bad.value})")
+    return st, nU.value, bad.value
+
+
+def moce_support_prepare16(desc: moce_desc, s16, w, s_out, w_out, covered, U, info, stream=None,
+                           check: bool = True) -> Tuple[int, int, int]:
+    """moce_support_prepare from 16-bit supports; returns (status, nU, bad_expert)."""
+    nU = ctypes.c_int32(-1)
+    bad = ctypes.c_int32(-1)
+    st = load().moce_support_prepare16(ctypes.byref(desc), _ptr(s16), _ptr(w), _ptr(s_out), _ptr(w_out),
+                                       _ptr(covered), _ptr(U), _ptr(info), ctypes.byref(nU),
+                                       ctypes.byref(bad), _stream(stream))
+    if check and st != 0:
+        raise MoceError("moce_support_prepare16", st, f"(first bad expert {bad.value})")
     return st, nU.value, bad.value
 
 

@@ -111,19 +111,20 @@ const char* moce_status_str(int status) {
   }
 }
 
-moce_status moce_support_prepare(const moce_desc* desc, const int32_t* s, const float* w,
-                                 int32_t* s_out, float* w_out, uint8_t* covered, int32_t* U,
-                                 int32_t* info, int32_t* nU_host, int32_t* bad_expert_host,
-                                 hipStream_t stream) {
+namespace {
+
+moce_status support_prepare(const moce_desc* desc, const void* s, bool s16, const float* w, int32_t* s_out,
+                            float* w_out, uint8_t* covered, int32_t* U, int32_t* info, int32_t* nU_host,
+                            int32_t* bad_expert_host, hipStream_t stream) {
   Shape sh;
   moce_status st = check_desc(desc, &sh);
   if (st != MOCE_OK) return st;
   if (!covered || !U || !info || !nU_host || !bad_expert_host) return MOCE_ERR_NULL;
   if (sh.R > 0 && (!s || !w || !s_out || !w_out)) return MOCE_ERR_NULL;
-  if (sh.C > (1 << 24) || sh.k > 4096) return MOCE_ERR_UNSUPPORTED;
-  if (sh.R > 0 && (static_cast<const void*>(s) == s_out || static_cast<const void*>(w) == w_out))
+  if (sh.C > (s16 ? (1 << 16) : (1 << 24)) || sh.k > 4096) return MOCE_ERR_UNSUPPORTED;
+  if (sh.R > 0 && (s == static_cast<const void*>(s_out) || static_cast<const void*>(w) == w_out))
     return MOCE_ERR_NULL;
-  hipError_t e = moce::launch_prepare(sh, s, w, s_out, w_out, covered, U, info, stream);
+  hipError_t e = moce::launch_prepare(sh, s, s16, w, s_out, w_out, covered, U, info, stream);
   if (e != hipSuccess) return MOCE_ERR_DEVICE;
   int32_t host[2] = {0, 0};
   e = hipMemcpyAsync(host, info, sizeof host, hipMemcpyDeviceToHost, stream);
@@ -133,6 +134,22 @@ moce_status moce_support_prepare(const moce_desc* desc, const int32_t* s, const 
   *nU_host = host[0];
   *bad_expert_host = host[1];
   return host[1] >= 0 ? MOCE_ERR_SUPPORT : MOCE_OK;
+}
+
+}  // namespace
+
+moce_status moce_support_prepare(const moce_desc* desc, const int32_t* s, const float* w,
+                                 int32_t* s_out, float* w_out, uint8_t* covered, int32_t* U,
+                                 int32_t* info, int32_t* nU_host, int32_t* bad_expert_host,
+                                 hipStream_t stream) {
+  return support_prepare(desc, s, false, w, s_out, w_out, covered, U, info, nU_host, bad_expert_host, stream);
+}
+
+moce_status moce_support_prepare16(const moce_desc* desc, const uint16_t* s, const float* w,
+                                   int32_t* s_out, float* w_out, uint8_t* covered, int32_t* U,
+                                   int32_t* info, int32_t* nU_host, int32_t* bad_expert_host,
+                                   hipStream_t stream) {
+  return support_prepare(desc, s, true, w, s_out, w_out, covered, U, info, nU_host, bad_expert_host, stream);
 }
 
 moce_status moce_pool(const moce_desc* desc, const void* x, float* d, hipStream_t stream) {

@@ -133,7 +133,9 @@ struct Shape {
 };
 
 // ---- launchers (return hipSuccess or the launch error) --------------------
-hipError_t launch_prepare(const Shape& sh, const int32_t* s, const float* w, int32_t* s_out,
+// s: int32 channel indices, or uint16 ones when s16 (the 16-bit storage of
+// deployed supports)
+hipError_t launch_prepare(const Shape& sh, const void* s, bool s16, const float* w, int32_t* s_out,
                           float* w_out, uint8_t* covered, int32_t* U, int32_t* info,
                           hipStream_t st);
 hipError_t launch_pool(const Shape& sh, const void* x, float* d, hipStream_t st);

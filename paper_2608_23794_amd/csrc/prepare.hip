@@ -24,8 +24,10 @@ __global__ void k_prepare_clear(uint8_t* covered, int64_t C, int32_t* info) {
 // its rank under "larger logit first, equal logits by lower channel"; one
 // O(k^2) sweep also detects repeated channels.  Invalid rows report their
 // index through an atomic minimum and write nothing.
+// Idx: int32_t, or uint16_t for the 16-bit storage of deployed supports.
+template <typename Idx>
 __global__ void __launch_bounds__(kPrepThreads)
-k_prepare_rows(const int32_t* __restrict__ s, const float* __restrict__ w, int32_t* __restrict__ s_out,
+k_prepare_rows(const Idx* __restrict__ s, const float* __restrict__ w, int32_t* __restrict__ s_out,
                float* __restrict__ w_out, uint8_t* __restrict__ covered, int32_t* info, int C, int k) {
   extern __shared__ unsigned char smem[];
   int32_t* rs = reinterpret_cast<int32_t*>(smem);
@@ -35,7 +37,7 @@ k_prepare_rows(const int32_t* __restrict__ s, const float* __restrict__ w, int32
   const int o = blockIdx.x;
   if (threadIdx.x == 0) bad = 0;
   for (int i = threadIdx.x; i < k; i += blockDim.x) {
-    rs[i] = s[(int64_t)o * k + i];
+    rs[i] = (int32_t)s[(int64_t)o * k + i];
     rw[i] = w[(int64_t)o * k + i];
   }
   __syncthreads();
@@ -105,7 +107,7 @@ k_prepare_compact(const uint8_t* __restrict__ covered, int64_t C, int32_t* __res
 
 }  // namespace
 
-hipError_t launch_prepare(const Shape& sh, const int32_t* s, const float* w, int32_t* s_out,
+hipError_t launch_prepare(const Shape& sh, const void* s, bool s16, const float* w, int32_t* s_out,
                           float* w_out, uint8_t* covered, int32_t* U, int32_t* info,
                           hipStream_t st) {
   const int64_t C = sh.C;
@@ -117,8 +119,12 @@ hipError_t launch_prepare(const Shape& sh, const int32_t* s, const float* w, int
   if (e != hipSuccess) return e;
   if (sh.R > 0) {
     const size_t lds = (size_t)sh.k * (sizeof(int32_t) + sizeof(float));
-    hipLaunchKernelGGL(k_prepare_rows, dim3(sh.R), dim3(kPrepThreads), lds, st, s, w, s_out, w_out,
-                       covered, info, (int)C, sh.k);
+    if (s16)
+      hipLaunchKernelGGL(k_prepare_rows<uint16_t>, dim3(sh.R), dim3(kPrepThreads), lds, st,
+                         static_cast<const uint16_t*>(s), w, s_out, w_out, covered, info, (int)C, sh.k);
+    else
+      hipLaunchKernelGGL(k_prepare_rows<int32_t>, dim3(sh.R), dim3(kPrepThreads), lds, st,
+                         static_cast<const int32_t*>(s), w, s_out, w_out, covered, info, (int)C, sh.k);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -360,3 +360,17 @@ def test_forward_ex_host_errors(lib):
         d = good_desc(**kw)
         assert mb.raw_status("moce_forward_ex", ctypes.byref(d), FAKE, FAKE, FAKE, ctypes.byref(gate), FAKE, 4, None,
                              FAKE, FAKE, 1 << 30, None) == code, kw
+
+
+def test_support_prepare16_host_errors(lib):
+    nU = ctypes.c_int32(0)
+    bad = ctypes.c_int32(0)
+
+    def call(desc, s=FAKE, info=FAKE):
+        return mb.raw_status("moce_support_prepare16", ctypes.byref(desc), s, FAKE, FAKE + 4096, FAKE + 8192, FAKE,
+                             FAKE, info, ctypes.byref(nU), ctypes.byref(bad), None)
+    assert call(good_desc(), s=None) == -1
+    assert call(good_desc(), info=None) == -1
+    assert call(good_desc(C=70000, k=8, E=16)) == -10    # 16-bit indices reach 65535
+    for kw, code in BAD_DESCS:
+        assert call(good_desc(**kw)) == code, kw
