@@ -269,7 +269,8 @@ def roofline_entry(kernels, path, mb, C):
 
 FORWARD_NAMES = {0: "pool, gate, mix", 1: "pool, gate, tile mix", 2: "pool, gate, matrix-core mix",
                  3: "pool, gate inside the matrix-core mix",
-                 4: "pool with the support schedule, gate statistics, scheduled matrix-core mix"}
+                 4: "pool with the support schedule, gate statistics, scheduled matrix-core mix",
+                 5: "pool, gate, channels-last gather"}
 
 # workloads whose line carries both gate forms timed through the gate entry point
 GATE_TIMED = ("resnet50_stage1", "resnet50_stage4")
@@ -369,6 +370,7 @@ def replaced_ops(batch=512, k=8, n_g=3, reps=5):
     replays.  The dense projection is one GEMM [B H W, C] x [C, E] through torch (hipBLASLt)."""
     import numpy as np
     import torch
+    from paper_2608_23794_amd import binding as mb
     from paper_2608_23794_amd.layer import MoceLayer
     rng = np.random.default_rng(2608)
     rows, t_moce, t_dense = [], 0.0, 0.0
@@ -386,8 +388,9 @@ def replaced_ops(batch=512, k=8, n_g=3, reps=5):
         x2 = x.view(-1, C)
         yd = torch.empty((x2.shape[0], E), dtype=torch.bfloat16, device="cuda")
         td = quartiles(graph_times_ms(lambda i, st=None: torch.matmul(x2, Wd, out=yd), n_g, reps))[1]
-        path = layer.desc(batch)
-        rows.append({"shape": f"{C}->{E} @{S}x{S}", "blocks": nblk, "moce_us": round(tm * 1e3, 1),
+        path = mb.moce_forward_path(layer.desc(batch), mb.MOCE_GATE_SOFTPLUS_LINEAR)
+        rows.append({"shape": f"{C}->{E} @{S}x{S}", "blocks": nblk, "forward": FORWARD_NAMES.get(path, str(path)),
+                     "moce_us": round(tm * 1e3, 1),
                      "dense_us": round(td * 1e3, 1), "moce_over_dense": round(tm / td, 3)})
         t_moce += nblk * tm
         t_dense += nblk * td

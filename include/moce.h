@@ -168,11 +168,15 @@ size_t moce_forward_workspace_bytes(const moce_desc* desc);
 
 /* Paths moce_forward can take. */
 enum { MOCE_PATH_GENERIC = 0, MOCE_PATH_TILE = 1, MOCE_PATH_MFMA = 2, MOCE_PATH_MFMA_GATE = 3,
-       MOCE_PATH_SCHEDULED = 4 };
+       MOCE_PATH_SCHEDULED = 4, MOCE_PATH_GATHER = 5 };
 
 /* The path moce_forward takes for `desc` (moce_mix takes the same kernels,
  * MOCE_PATH_MFMA for MOCE_PATH_MFMA_GATE, MOCE_PATH_GENERIC for
- * MOCE_PATH_SCHEDULED):
+ * MOCE_PATH_SCHEDULED, the gather for MOCE_PATH_GATHER):
+ *  MOCE_PATH_GATHER: channels-last bfloat16 with small supports (k <= 16,
+ *     C a multiple of 8 up to 4096, E-1 <= 1024, or 512 for k > 8): pooling, the gate's
+ *     coefficients, then a gather whose work scales with k (x staged in LDS
+ *     transposed, 8 positions per read);
  *  MOCE_PATH_SCHEDULED: channels-last bfloat16 (C a multiple of 64 up to
  *     4096, E a multiple of 8): pooling, the gate's softmax statistics, then
  *     a schedule of the supports by 64-channel step (Sec. 3.2: static
@@ -223,7 +227,7 @@ typedef struct moce_epilogue {
 
 /* moce_forward followed by the epilogue `ep` (NULL: none, then identical to
  * moce_forward).  On the matrix-core paths (MOCE_PATH_MFMA, MOCE_PATH_MFMA_GATE,
- * MOCE_PATH_SCHEDULED) the mix kernel applies it to the float32 accumulators
+ * MOCE_PATH_SCHEDULED) and MOCE_PATH_GATHER the mix kernel applies it to the float32 accumulators
  * before rounding; on the others a second kernel applies it to y in place
  * (for bf16 y, to the rounded value).  Errors: those of moce_forward, and
  * MOCE_ERR_NULL when exactly one of scale and shift is NULL. */

@@ -208,11 +208,12 @@ def moce_forward_workspace_bytes(desc: moce_desc) -> int:
     return int(load().moce_forward_workspace_bytes(ctypes.byref(desc)))
 
 
-PATH_GENERIC, PATH_TILE, PATH_MFMA, PATH_MFMA_GATE, PATH_SCHEDULED = 0, 1, 2, 3, 4
+PATH_GENERIC, PATH_TILE, PATH_MFMA, PATH_MFMA_GATE, PATH_SCHEDULED, PATH_GATHER = 0, 1, 2, 3, 4, 5
 
 
 def moce_forward_path(desc: moce_desc, gate_kind: int) -> int:
-    """PATH_MFMA_GATE, PATH_MFMA, PATH_TILE or PATH_GENERIC: the kernels moce_forward uses for desc
+    """PATH_GATHER, PATH_SCHEDULED, PATH_MFMA_GATE, PATH_MFMA, PATH_TILE or PATH_GENERIC: the kernels
+    moce_forward uses for desc
     (moce_mix: the same, PATH_MFMA for PATH_MFMA_GATE)."""
     r = int(load().moce_forward_path(ctypes.byref(desc), gate_kind))
     if r < 0:

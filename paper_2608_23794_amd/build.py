@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = ["api.hip", "prepare.hip", "pool.hip", "gate.hip", "mix.hip", "tilemix.hip", "mfmamix.hip",
-           "gmix.hip", "dynamic.hip", "backward.hip", "bwdmfma.hip"]
+           "gmix.hip", "dynamic.hip", "backward.hip", "bwdmfma.hip", "gather.hip"]
 LIB = os.path.join(HERE, "libmoce.so")
 OBJDIR = os.path.join(HERE, "_build")
 

@@ -81,9 +81,9 @@ WsLayout ws_layout(const Shape& sh) {
   l.stats = off;
   off += round_up((size_t)3 * sh.B * sh.R * sizeof(float));
   l.alpha = off;
-  if (sh.layout == MOCE_NCHW) off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
+  if (sh.layout == MOCE_NCHW || moce::gather_eligible(sh)) off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
   l.sched = off;
-  if (moce::gmix_eligible(sh)) off += round_up(moce::gmix_sched_bytes(sh));
+  if (!moce::gather_eligible(sh) && moce::gmix_eligible(sh)) off += round_up(moce::gmix_sched_bytes(sh));
   l.total = off;
   return l;
 }
@@ -183,6 +183,8 @@ moce_status moce_mix(const moce_desc* desc, const void* x, const int32_t* s, con
   if (nU < 0 || (int64_t)nU > sh.C) return MOCE_ERR_SHAPE;
   if (nU > 0 && !U) return MOCE_ERR_NULL;
   if (!aligned(x, 16) || !aligned(y, 16)) return MOCE_ERR_ALIGN;
+  if (moce::gather_eligible(sh))
+    return device_status(moce::launch_gather(sh, x, s, alpha, U, nU, y, stream, moce::Epi{}));
   if (moce::mfmamix_eligible(sh))
     return device_status(moce::launch_mfmamix(sh, x, s, alpha, U, nU, y, stream));
   if (sh.R > 0 && moce::tilemix_eligible(sh))
@@ -217,6 +219,7 @@ int moce_forward_path(const moce_desc* desc, int gate_kind) {
   const moce_status st = check_desc(desc, &sh);
   if (st != MOCE_OK) return st;
   if (gate_kind != MOCE_GATE_SOFTPLUS_LINEAR && gate_kind != MOCE_GATE_MLP_SIGMOID) return MOCE_ERR_GATE;
+  if (moce::gather_eligible(sh)) return MOCE_PATH_GATHER;
   if (moce::gmix_eligible(sh)) return MOCE_PATH_SCHEDULED;
   if (moce::mfmamix_gate_fusable(sh, gate_kind)) return MOCE_PATH_MFMA_GATE;
   if (moce::mfmamix_eligible(sh)) return MOCE_PATH_MFMA;
@@ -252,7 +255,8 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
   float* d = reinterpret_cast<float*>(base + l.d);
   float* tau = reinterpret_cast<float*>(base + l.tau);
   float* stats = reinterpret_cast<float*>(base + l.stats);
-  float* alpha = sh.layout == MOCE_NCHW ? reinterpret_cast<float*>(base + l.alpha) : nullptr;
+  float* alpha = sh.layout == MOCE_NCHW || moce::gather_eligible(sh) ? reinterpret_cast<float*>(base + l.alpha)
+                                                                       : nullptr;
 
   // pooling reads x plane by plane (the order HBM serves best) and leaves it
   // in the infinity cache; the gate kernel writes tau and the coefficients;
@@ -276,6 +280,15 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
     e = moce::launch_tilemix(sh, x, s, alpha, U, nU, y, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
     return device_status(moce::launch_epilogue(sh, y, ep, stream));
+  }
+  if (moce::gather_eligible(sh)) {
+    // channels-last with small supports: pooling, the gate's coefficients,
+    // then the gather, whose work scales with k
+    hipError_t e = moce::launch_pool(sh, x, d, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    e = moce::launch_gate(sh, d, s, w, *gate, tau, alpha, nullptr, stream);
+    if (e != hipSuccess) return MOCE_ERR_DEVICE;
+    return device_status(moce::launch_gather(sh, x, s, alpha, U, nU, y, stream, ep));
   }
   if (moce::gmix_eligible(sh)) {
     // channels-last on the matrix cores: pooling with the support schedule

@@ -184,6 +184,13 @@ bool gmix_eligible(const Shape& sh);
 size_t gmix_sched_bytes(const Shape& sh);
 hipError_t launch_pool_sched(const Shape& sh, const void* x, float* d, const int32_t* s, const float* w,
                              const int32_t* U, int nU, void* sched, hipStream_t st);
+// Channels-last bfloat16 gather mixing for small supports (gather.hip): k <=
+// 16, C a multiple of 8 up to 4096, E-1 <= 1024 (512 for k > 8); coefficients from alpha
+// [B][R][k], the epilogue applied before rounding.
+bool gather_eligible(const Shape& sh);
+hipError_t launch_gather(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
+                         int nU, void* y, hipStream_t st, const Epi& ep);
+
 // The epilogue applied in place to a finished y (the paths whose mix kernels
 // do not apply it themselves).
 hipError_t launch_epilogue(const Shape& sh, void* y, const Epi& ep, hipStream_t st);

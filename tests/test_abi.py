@@ -208,10 +208,15 @@ def test_workspace_size_and_errors(lib):
     assert _call_forward(desc, gate, ws=None) == -7
     assert _call_forward(desc, gate, ws_bytes=need - 1) == -7
     nhwc = good_desc(layout=mb.MOCE_NHWC)
-    # bf16 channels-last with C a multiple of 64 takes the scheduled mix: no coefficients, but the support
+    # bf16 channels-last with k <= 16 takes the gather: the coefficients as in the channels-first layout
+    assert mb.moce_forward_path(nhwc, mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_GATHER
+    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 512 + 1024
+    # with larger supports and C a multiple of 64 it takes the scheduled mix: no coefficients, but the support
     # schedule of one expert range with eight builder buckets (offsets [8][1 step + 1] in 256 bytes, entries
     # [8][2 * 16 k + C] of 8 bytes)
-    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 512 + 256 + 8 * (32 * 8 + 64) * 8
+    nhwc = good_desc(layout=mb.MOCE_NHWC, k=24)
+    assert mb.moce_forward_path(nhwc, mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_SCHEDULED
+    assert lib.moce_forward_workspace_bytes(ctypes.byref(nhwc)) == 512 + 256 + 512 + 256 + 8 * (32 * 24 + 64) * 8
     f32 = good_desc(layout=mb.MOCE_NHWC, dtype=mb.MOCE_F32)
     assert lib.moce_forward_workspace_bytes(ctypes.byref(f32)) == 512 + 256 + 512
 

@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 CASES = [
     # workload, layout, batch of the first call, batch of the second (smaller) call
     ("resnet50_stage1", "nchw", 24, 7),     # pooling, then gate and mix in one kernel
-    ("resnet50_stage3", "nhwc", 16, 5),     # pooling, gate (statistics), generic mix
+    ("resnet50_stage3", "nhwc", 16, 5),     # pooling, gate (statistics), scheduled mix
     ("resnet50_stage3", "nchw", 12, 3),     # pooling, gate (coefficients), mix
     ("tiny", "nchw", 2, 1),
 ]
