@@ -71,6 +71,13 @@ size_t elem_bytes(const Shape& sh) { return sh.elem == MOCE_F32 ? 4 : 2; }
 struct WsLayout {
   size_t d, tau, stats, alpha, sched, total;
 };
+// the forward's scheduled matrix-core mix: where gmix applies and no earlier
+// path of forward_launch does
+bool uses_gmix(const Shape& sh) {
+  return !moce::mfmamix_eligible(sh) && !(sh.R > 0 && moce::tilemix_eligible(sh)) && !moce::gather_eligible(sh) &&
+         moce::gmix_eligible(sh);
+}
+
 WsLayout ws_layout(const Shape& sh) {
   WsLayout l{};
   size_t off = 0;
@@ -81,9 +88,11 @@ WsLayout ws_layout(const Shape& sh) {
   l.stats = off;
   off += round_up((size_t)3 * sh.B * sh.R * sizeof(float));
   l.alpha = off;
-  if (sh.layout == MOCE_NCHW || moce::gather_eligible(sh)) off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
+  const bool gm = uses_gmix(sh);
+  if ((sh.layout == MOCE_NCHW && !gm) || moce::gather_eligible(sh))
+    off += round_up((size_t)sh.B * sh.R * sh.k * sizeof(float));
   l.sched = off;
-  if (!moce::gather_eligible(sh) && moce::gmix_eligible(sh)) off += round_up(moce::gmix_sched_bytes(sh));
+  if (gm) off += round_up(moce::gmix_sched_bytes(sh));
   l.total = off;
   return l;
 }
@@ -219,11 +228,13 @@ int moce_forward_path(const moce_desc* desc, int gate_kind) {
   const moce_status st = check_desc(desc, &sh);
   if (st != MOCE_OK) return st;
   if (gate_kind != MOCE_GATE_SOFTPLUS_LINEAR && gate_kind != MOCE_GATE_MLP_SIGMOID) return MOCE_ERR_GATE;
+  // the order of forward_launch's tests
+  if (moce::mfmamix_eligible(sh))
+    return moce::mfmamix_gate_fusable(sh, gate_kind) ? MOCE_PATH_MFMA_GATE : MOCE_PATH_MFMA;
+  if (sh.R > 0 && moce::tilemix_eligible(sh)) return MOCE_PATH_TILE;
   if (moce::gather_eligible(sh)) return MOCE_PATH_GATHER;
   if (moce::gmix_eligible(sh)) return MOCE_PATH_SCHEDULED;
-  if (moce::mfmamix_gate_fusable(sh, gate_kind)) return MOCE_PATH_MFMA_GATE;
-  if (moce::mfmamix_eligible(sh)) return MOCE_PATH_MFMA;
-  return sh.R > 0 && moce::tilemix_eligible(sh) ? MOCE_PATH_TILE : MOCE_PATH_GENERIC;
+  return MOCE_PATH_GENERIC;
 }
 
 }  // extern "C"
@@ -255,8 +266,9 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
   float* d = reinterpret_cast<float*>(base + l.d);
   float* tau = reinterpret_cast<float*>(base + l.tau);
   float* stats = reinterpret_cast<float*>(base + l.stats);
-  float* alpha = sh.layout == MOCE_NCHW || moce::gather_eligible(sh) ? reinterpret_cast<float*>(base + l.alpha)
-                                                                       : nullptr;
+  float* alpha = (sh.layout == MOCE_NCHW && !uses_gmix(sh)) || moce::gather_eligible(sh)
+                     ? reinterpret_cast<float*>(base + l.alpha)
+                     : nullptr;
 
   // pooling reads x plane by plane (the order HBM serves best) and leaves it
   // in the infinity cache; the gate kernel writes tau and the coefficients;
@@ -291,8 +303,8 @@ moce_status forward_launch(const Shape& sh, const void* x, const int32_t* s, con
     return device_status(moce::launch_gather(sh, x, s, alpha, U, nU, y, stream, ep));
   }
   if (moce::gmix_eligible(sh)) {
-    // channels-last on the matrix cores: pooling with the support schedule
-    // beside it, the gate's softmax statistics, then the mix
+    // on the matrix cores: pooling with the support schedule (beside it for
+    // channels-last x), the gate's softmax statistics, then the mix
     hipError_t e = moce::launch_pool_sched(sh, x, d, s, w, U, nU, base + l.sched, stream);
     if (e != hipSuccess) return MOCE_ERR_DEVICE;
     e = moce::launch_gate(sh, d, s, w, *gate, tau, nullptr, stats, stream);

@@ -66,7 +66,7 @@ k_gate_softplus(const float* __restrict__ d, const int32_t* __restrict__ s, cons
                    o);
 }
 
-// The same for k <= W (W = 32): segments of W lanes, one per (image,
+// The same for k <= W (W = 8, 16 or 32): segments of W lanes, one per (image,
 // expert), 64 / W per wave, lane i of a segment holding support position i.
 // Every input of a position is read up front (the selected logit too), so the
 // only dependent reads are the descriptor gathers; the exponentials are
@@ -725,9 +725,17 @@ hipError_t launch_gate(const Shape& sh, const float* d, const int32_t* s, const 
   const Stats sp = stats ? stats_planes(stats, items, sh.R, 1) : Stats{nullptr, nullptr, nullptr, 0, 0};
   const unsigned blocks = (unsigned)((items + kGateWaves - 1) / kGateWaves);
   if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 32) {
-    const unsigned b32 = (unsigned)((items + 2 * kGateWaves - 1) / (2 * kGateWaves));
-    hipLaunchKernelGGL(k_gate_softplus_seg<32>, dim3(b32), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c,
-                       tau, alpha, sp, sh.B, sh.C, sh.R, sh.k);
+    // segments of 8, 16 or 32 lanes: the narrowest that holds k (the sums and
+    // maxima over the lanes past k add zeros, so every width gives the same
+    // bits)
+    const int W = sh.k <= 8 ? 8 : sh.k <= 16 ? 16 : 32;
+    const int64_t per = (int64_t)kGateWaves * (kWave / W);
+    const unsigned bs = (unsigned)((items + per - 1) / per);
+    using K = void (*)(const float*, const int32_t*, const float*, const float*, const float*, float*, float*, Stats,
+                       int64_t, int64_t, int, int);
+    const K kf = W == 8 ? k_gate_softplus_seg<8> : W == 16 ? k_gate_softplus_seg<16> : k_gate_softplus_seg<32>;
+    hipLaunchKernelGGL(kf, dim3(bs), dim3(kGateWaves * kWave), 0, st, d, s, w, g.a, g.c, tau, alpha, sp, sh.B,
+                       sh.C, sh.R, sh.k);
   } else if (g.kind == MOCE_GATE_SOFTPLUS_LINEAR && sh.k <= 128 && sh.C <= kLdsGateMaxC) {
     // 32 experts per workgroup, nbi images each, for about kLdsGateTargetBlocks
     // workgroups

@@ -43,6 +43,16 @@
 //    ring of LDS buffers with global-to-LDS loads, several chunks in flight.
 // At the end the consumers stage their results in LDS and every wave writes
 // whole rows of y.
+//
+// Channels-first x (NCHW) takes the same schedule and builders with the roles
+// of the operands exchanged: y_b = A_b x_b with A_b's rows (the B buffers
+// above, experts by channels) as the MFMA's A operand and the x tile as its B
+// operand.  The tile holds one row of MT positions per channel, copied 4 bytes
+// a lane by four loader waves (channel rows start only 8-byte aligned when H W
+// is a multiple of 4); the consumers read its columns with the transposing LDS
+// read, and the results are staged expert by expert and written as rows of
+// positions.  Each row is rotated by 64 bytes per group of 8 channels, so the
+// 16 rows one transposing read touches fall on distinct banks.
 #include <algorithm>
 #include <utility>
 
@@ -56,6 +66,8 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 #define GMIX_LDS __attribute__((address_space(3)))
 
 constexpr int kStep = 64;                 // channels per step: two K slices of the MFMA, one x chunk
@@ -64,9 +76,10 @@ constexpr int kBRow = kStep * 2;          // bytes of one expert row of one part
 constexpr int kMaxXRing = 8;              // x chunk buffers at most (the ring fills the LDS left over)
 constexpr int kConsumers = 4;
 constexpr int kBuilders = 8;
-constexpr int kLoaders = 2;
-constexpr int kWaves = kConsumers + kBuilders + kLoaders;
-constexpr int kThreads = 64 * kWaves;
+// loader waves: 16-byte copies of channels-last rows, 4-byte copies of
+// channels-first rows
+constexpr int loaders_of(bool NH) { return NH ? 2 : 4; }
+constexpr int threads_of(bool NH) { return 64 * (kConsumers + kBuilders + loaders_of(NH)); }
 constexpr int kGroup = 16;                // experts per group (one MFMA N block)
 constexpr int kGroupsPerBuilder = 2;      // 4 NB <= 16 groups per workgroup over 8 builders
 constexpr int kMaxSteps = 64;             // C <= 4096: offsets 0 .. 63 in one register, the total beside
@@ -223,7 +236,7 @@ k_pool_sched(const T* __restrict__ x, float* __restrict__ d, int C, int HW, int 
 }
 
 // ---------------------------------------------------------------- the mix
-template <int MB, int NB, int NS, int OCC>
+template <int MB, int NB, int NS, int OCC, bool NH>
 struct Layout {
   static constexpr int MT = 16 * MB;                 // positions per tile
   static constexpr int NE = 64 * NB;                 // experts per workgroup
@@ -237,7 +250,9 @@ struct Layout {
   // kMaxXRing, and so that one loader wave's outstanding copies stay within
   // its 6-bit counter
   static constexpr int XR_FIT = (kLdsBytes / OCC - 1024 - 2 * BBUF - 16 * NE) / XBUF;
-  static constexpr int ROUNDS = MB;                  // 16-byte copies per loader lane per chunk (MT / 16)
+  // copies per loader lane per chunk: MT / 16 of 16 bytes (channels-last),
+  // MT / 8 of 4 bytes (channels-first)
+  static constexpr int ROUNDS = NH ? MB : 2 * MB;
   static constexpr int XR_CNT = 63 / ROUNDS + 1;
   static constexpr int XR = XR_FIT < kMaxXRing ? (XR_FIT < XR_CNT ? XR_FIT : XR_CNT)
                                                : (kMaxXRing < XR_CNT ? kMaxXRing : XR_CNT);
@@ -245,12 +260,18 @@ struct Layout {
   static constexpr int OFF_X = 0;
   static constexpr int OFF_B = OFF_X + XR * XBUF;
   static constexpr int OFF_ST = OFF_B + 2 * BBUF;    // statistics, one float4 (rt, m, rzs, -) per expert
-  static constexpr int OROW = NE * 2 + 16;           // staging row of the results
+  // staging rows of the results: one per position (channels-last) or per
+  // expert (channels-first)
+  static constexpr int OROW = NH ? NE * 2 + 16 : MT * 2 + 16;
   static size_t bytes() {
     const size_t main = (size_t)OFF_ST + (size_t)16 * NE;
-    const size_t stage = (size_t)MT * OROW;
+    const size_t stage = (size_t)(NH ? MT : NE) * OROW;
     return std::max(main, stage);
   }
+  // channels-first x chunk: channel row r's byte u (positions u / 2) at
+  // r ROWB + (u + rot(r)) mod ROWB
+  static constexpr int ROWB = MT * 2;
+  __device__ static int rot(int r) { return (64 * ((r >> 3) & 3)) % ROWB; }
 };
 
 // the exact split of a float into bf16 parts (hi, the rounded remainder, ...)
@@ -274,7 +295,7 @@ __device__ __forceinline__ int unit_of(const GmArgs& p) {
 
 template <int MB, int NB, int NS, int OCC>
 __device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, int wv, int o0) {
-  using L = Layout<MB, NB, NS, OCC>;
+  using L = Layout<MB, NB, NS, OCC, true>;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, n = lane & 15;
   f32x4 acc[MB][NB];
@@ -364,9 +385,9 @@ __device__ __forceinline__ void consumer(const GmArgs& p, unsigned char* smem, i
       }
 }
 
-template <int MB, int NB, int NS, int OCC>
+template <int MB, int NB, int NS, int OCC, bool NH>
 __device__ __forceinline__ void builder(const GmArgs& p, unsigned char* smem, int j, int b, int q) {
-  using L = Layout<MB, NB, NS, OCC>;
+  using L = Layout<MB, NB, NS, OCC, NH>;
   constexpr int NG = 4 * NB;  // groups of the range
   constexpr int kRounds = rounds_of(NB);
   const int lane = threadIdx.x & 63;
@@ -517,7 +538,7 @@ __device__ __forceinline__ void wait_chunks(int n) {
 
 template <int MB, int NB, int NS, int OCC>
 __device__ __forceinline__ void loader(const GmArgs& p, unsigned char* smem, int lw, int b, int p0) {
-  using L = Layout<MB, NB, NS, OCC>;
+  using L = Layout<MB, NB, NS, OCC, true>;
   constexpr int XR = L::XR;
   const int lane = threadIdx.x & 63;
   const int nchunks = p.nsteps;
@@ -552,10 +573,136 @@ __device__ __forceinline__ void loader(const GmArgs& p, unsigned char* smem, int
   }
 }
 
+
+// Channels-first consumer: D[e][p] = A_b[e][:] x[:][p] with A = the B
+// buffers' expert rows, B = the x tile's columns through the transposing read.
+// Wave wv owns expert blocks NB wv .. NB wv + NB - 1 and all MT positions.
 template <int MB, int NB, int NS, int OCC>
-__global__ void __launch_bounds__(kThreads, OCC)
+__device__ __forceinline__ void consumer_t(const GmArgs& p, unsigned char* smem, int wv, int o0) {
+  using L = Layout<MB, NB, NS, OCC, false>;
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, n = lane & 15;
+  f32x4 acc[NB][MB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // A fragments: expert row 16 (NB wv + nb) + n, logical chunk 4 h + g
+  const int brow = (16 * NB * wv + n) * kBRow;
+  const int ch0 = (g ^ (n >> 1)) << 4, ch1 = ((4 + g) ^ (n >> 1)) << 4;
+  auto load_c = [&](const unsigned char* bb, int h, int nb, int pt) __attribute__((always_inline)) {
+    return __builtin_bit_cast(
+        bf16x8, *reinterpret_cast<const u32x4*>(bb + pt * L::PART + nb * 16 * kBRow + (h ? ch1 : ch0)));
+  };
+  // B fragments of K slice h, position block mb: lane j of 16-lane group G
+  // takes channels 32 h + 8 G .. + 7 at position 16 mb + j.  In each
+  // transposing read source lane 4 t + q of the group addresses channel row
+  // 32 h + 8 G + t (then + 4) at positions 16 mb + 4 q .. + 3; all of this
+  // lane's rows share the rotation of group G
+  const int t = (lane >> 2) & 3, q = lane & 3;
+  const int r0 = 8 * g + t;
+  const int ub = 8 * q + L::rot(r0);
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  auto load_x = [&](const unsigned char* xb, int h, int mb) __attribute__((always_inline)) {
+    int u = ub + 32 * mb;
+    u = u >= L::ROWB ? u - L::ROWB : u;
+    const unsigned char* a0 = xb + (32 * h + r0) * L::ROWB + u;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a0);
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a0 + 4 * L::ROWB));
+    const s16x8 v = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    return __builtin_bit_cast(bf16x8, v);
+  };
+  lds_barrier();  // prologue: chunk 0 and the step-0 coefficients are in LDS
+  for (int ks = 0; ks < p.nsteps; ++ks) {
+    const unsigned char* xb = smem + L::OFF_X + (ks % L::XR) * L::XBUF;
+    const unsigned char* bb = smem + L::OFF_B + (ks & 1) * L::BBUF + brow;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // the slice's A fragments, then its x fragments one position block at
+      // a time, each read one block ahead of its products
+      bf16x8 c0[NB], c1[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        c0[nb] = load_c(bb, h, nb, 0);
+        c1[nb] = load_c(bb, h, nb, 1);
+      }
+      bf16x8 xv = load_x(xb, h, 0);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const bf16x8 xn = load_x(xb, h, mb + 1 < MB ? mb + 1 : mb);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(c0[nb], xv, acc[nb][mb], 0, 0, 0);
+          acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(c1[nb], xv, acc[nb][mb], 0, 0, 0);
+        }
+        xv = xn;
+      }
+    }
+    lds_barrier();  // step ks done: its x chunk and B buffer may be reused
+  }
+  // results: D[e][p] of block (nb, mb) sits on lane p + 16 (e / 4), element
+  // e % 4; staged as rows of positions, one per expert
+  unsigned char* stg = smem;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * (NB * wv + nb) + 4 * g + r;
+        const int col = 16 * mb + n;
+        *reinterpret_cast<uint16_t*>(stg + row * L::OROW + col * 2) =
+            f32_to_bf16(epi_apply(p.ep, acc[nb][mb][r], min(o0 + row, p.E - 1)));
+      }
+}
+
+// Channels-first loader: chunk n is channels 64 n .. 64 n + 63 of the tile,
+// one rotated row of MT positions each, copied 4 bytes a lane.  Copy i of a
+// chunk fills LDS bytes 256 i .. 256 i + 255; loader wave lw issues copies
+// lw, lw + 4, ...  Positions past the image load its last two positions.
+template <int MB, int NB, int NS, int OCC>
+__device__ __forceinline__ void loader_t(const GmArgs& p, unsigned char* smem, int lw, int b, int p0) {
+  using L = Layout<MB, NB, NS, OCC, false>;
+  constexpr int XR = L::XR;
+  constexpr int NL = loaders_of(false);
+  const int lane = threadIdx.x & 63;
+  const int nchunks = p.nsteps;
+  // this lane's source offsets (elements from the chunk's first channel row)
+  int src[L::ROUNDS];
+#pragma unroll
+  for (int r = 0; r < L::ROUNDS; ++r) {
+    const int o = 256 * (lw + NL * r) + 4 * lane;
+    const int row = o / L::ROWB;
+    int u = o - row * L::ROWB - L::rot(row);
+    if (u < 0) u += L::ROWB;
+    const int pos = min(p0 + u / 2, p.HW - 2);
+    src[r] = row * p.HW + pos;
+  }
+  const uint16_t* xb = p.x + (int64_t)b * p.C * p.HW;
+  auto copy = [&](int n) __attribute__((always_inline)) {
+    GMIX_LDS unsigned char* dst = (GMIX_LDS unsigned char*)(smem + L::OFF_X + (n % XR) * L::XBUF);
+    const uint16_t* cb = xb + (int64_t)n * kStep * p.HW;
+#pragma unroll
+    for (int r = 0; r < L::ROUNDS; ++r)
+      __builtin_amdgcn_global_load_lds((const void*)(cb + src[r]), (GMIX_LDS void*)(dst + 256 * (lw + NL * r)), 4,
+                                       0, kCachePolicyNT);
+  };
+  const int first = min(XR - 1, nchunks);
+  for (int n = 0; n < first; ++n) copy(n);
+  wait_chunks<L::ROUNDS, XR>(first - 1);
+  lds_barrier();  // prologue
+  for (int ks = 0; ks < p.nsteps; ++ks) {
+    if (ks + XR - 1 < nchunks) copy(ks + XR - 1);
+    if (ks + 1 < nchunks) wait_chunks<L::ROUNDS, XR>(min(ks + XR - 1, nchunks - 1) - (ks + 1));
+    lds_barrier();
+  }
+}
+
+template <int MB, int NB, int NS, int OCC, bool NH>
+__global__ void __launch_bounds__(threads_of(NH), OCC)
 k_gmix(GmArgs p) {
-  using L = Layout<MB, NB, NS, OCC>;
+  using L = Layout<MB, NB, NS, OCC, NH>;
+  constexpr int kThreads = threads_of(NH);
   extern __shared__ __align__(16) unsigned char smem[];
   const int v = unit_of(p);
   if (v >= p.units) return;  // uniform per workgroup: no barrier is skipped by part of it
@@ -565,13 +712,33 @@ k_gmix(GmArgs p) {
   const int jt = r / p.nq, q = r - (r / p.nq) * p.nq;
   const int p0 = jt * L::MT, o0 = q * L::NE;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (wv < kConsumers)
-    consumer<MB, NB, NS, OCC>(p, smem, wv, o0);
-  else if (wv < kConsumers + kBuilders)
-    builder<MB, NB, NS, OCC>(p, smem, wv - kConsumers, b, q);
-  else
-    loader<MB, NB, NS, OCC>(p, smem, wv - kConsumers - kBuilders, b, p0);
+  if (wv < kConsumers) {
+    if constexpr (NH)
+      consumer<MB, NB, NS, OCC>(p, smem, wv, o0);
+    else
+      consumer_t<MB, NB, NS, OCC>(p, smem, wv, o0);
+  } else if (wv < kConsumers + kBuilders) {
+    builder<MB, NB, NS, OCC, NH>(p, smem, wv - kConsumers, b, q);
+  } else {
+    if constexpr (NH)
+      loader<MB, NB, NS, OCC>(p, smem, wv - kConsumers - kBuilders, b, p0);
+    else
+      loader_t<MB, NB, NS, OCC>(p, smem, wv - kConsumers - kBuilders, b, p0);
+  }
   lds_barrier();  // results staged
+  if constexpr (!NH) {
+    // rows of 4 positions (8 bytes: H W is a multiple of 4) to y[b][o0 + row][p0 ..]
+    constexpr int kQuads = L::MT / 4;
+    for (int i = threadIdx.x; i < L::NE * kQuads; i += kThreads) {
+      const int row = i / kQuads, c4 = i - row * kQuads;
+      const int pos = p0 + 4 * c4, o = o0 + row;
+      if (pos < p.HW && o < p.E) {
+        const u32x2 val = *reinterpret_cast<const u32x2*>(smem + row * L::OROW + c4 * 8);
+        __builtin_nontemporal_store(val, reinterpret_cast<u32x2*>(p.y + ((int64_t)b * p.E + o) * p.HW + pos));
+      }
+    }
+    return;
+  }
   // whole 16-byte pieces of the staged rows to y[b][p0 + row][o0 ..]
   constexpr int kPieces = L::NE / 8;
   for (int i = threadIdx.x; i < L::MT * kPieces; i += kThreads) {
@@ -586,11 +753,12 @@ k_gmix(GmArgs p) {
 
 using GmKernel = void (*)(GmArgs);
 
-template <int MB, int NB, int NS, int OCC>
-size_t lds_of() { return Layout<MB, NB, NS, OCC>::bytes(); }
+template <int MB, int NB, int NS, int OCC, bool NH>
+size_t lds_of() { return Layout<MB, NB, NS, OCC, NH>::bytes(); }
 
 struct Variant {
   int MB, NB, NS, OCC;
+  bool NH;
   GmKernel k;
   size_t (*lds)();
 };
@@ -598,10 +766,14 @@ struct Variant {
 constexpr int kParts = 2;
 
 const Variant kVariants[] = {
-    {4, 4, 2, 1, k_gmix<4, 4, 2, 1>, lds_of<4, 4, 2, 1>},
-    {4, 3, 2, 1, k_gmix<4, 3, 2, 1>, lds_of<4, 3, 2, 1>},
-    {7, 2, 2, 1, k_gmix<7, 2, 2, 1>, lds_of<7, 2, 2, 1>},
-    {5, 3, 2, 1, k_gmix<5, 3, 2, 1>, lds_of<5, 3, 2, 1>},
+    {4, 4, 2, 1, true, k_gmix<4, 4, 2, 1, true>, lds_of<4, 4, 2, 1, true>},
+    {4, 3, 2, 1, true, k_gmix<4, 3, 2, 1, true>, lds_of<4, 3, 2, 1, true>},
+    {7, 2, 2, 1, true, k_gmix<7, 2, 2, 1, true>, lds_of<7, 2, 2, 1, true>},
+    {5, 3, 2, 1, true, k_gmix<5, 3, 2, 1, true>, lds_of<5, 3, 2, 1, true>},
+    {4, 4, 2, 1, false, k_gmix<4, 4, 2, 1, false>, lds_of<4, 4, 2, 1, false>},
+    {4, 3, 2, 1, false, k_gmix<4, 3, 2, 1, false>, lds_of<4, 3, 2, 1, false>},
+    {7, 2, 2, 1, false, k_gmix<7, 2, 2, 1, false>, lds_of<7, 2, 2, 1, false>},
+    {5, 3, 2, 1, false, k_gmix<5, 3, 2, 1, false>, lds_of<5, 3, 2, 1, false>},
 };
 
 int cu_count() {
@@ -620,7 +792,7 @@ const Variant* pick(const Shape& sh) {
   const Variant* best = nullptr;
   int64_t best_cost = 0;
   for (const Variant& v : kVariants) {
-    if (v.NS != kParts) continue;
+    if (v.NS != kParts || v.NH != (sh.layout == MOCE_NHWC)) continue;
     if (v.lds() * v.OCC > (size_t)kLdsBytes) continue;
     const int64_t nt = (sh.HW + 16 * v.MB - 1) / (16 * v.MB);
     const int64_t nq = (nblk + 4 * v.NB - 1) / (4 * v.NB);
@@ -655,8 +827,10 @@ SchedShape sched_shape(const Shape& sh, const Variant& v) {
 }  // namespace
 
 bool gmix_eligible(const Shape& sh) {
-  if (sh.layout != MOCE_NHWC || sh.elem != MOCE_BF16 || sh.R < 1) return false;
+  if (sh.elem != MOCE_BF16 || sh.R < 1) return false;
   if (sh.C % kStep != 0 || sh.C > kStep * kMaxSteps || sh.E % 8 != 0) return false;
+  // channels-first rows start 8-byte aligned and are copied 4 bytes at a time
+  if (sh.layout == MOCE_NCHW && sh.HW % 4 != 0) return false;
   if ((int64_t)sh.B * sh.HW > INT32_MAX / 2) return false;
   return pick(sh) != nullptr;
 }
@@ -685,6 +859,14 @@ hipError_t launch_pool_sched(const Shape& sh, const void* x, float* d, const int
   a.nbuckets = ss.nbuckets;
   a.off = static_cast<int32_t*>(sched);
   a.ent = reinterpret_cast<uint2*>(static_cast<char*>(sched) + ss.off_bytes);
+  if (sh.layout == MOCE_NCHW) {
+    // channels-first: the plane pooling kernel, then the schedule alone
+    const hipError_t e = launch_pool(sh, x, d, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_pool_sched<uint16_t>), dim3((unsigned)ss.nbuckets), dim3(kPoolThreads), 0, st,
+                       static_cast<const uint16_t*>(x), d, (int)sh.C, (int)sh.HW, 1, a);
+    return hipGetLastError();
+  }
   const int nblk = (int)((sh.C / PoolVec<uint16_t>::EPV + 31) / 32);
   const unsigned grid = (unsigned)(ss.nbuckets + sh.B * nblk);
   hipLaunchKernelGGL((k_pool_sched<uint16_t>), dim3(grid), dim3(kPoolThreads), 0, st,
@@ -721,7 +903,7 @@ hipError_t launch_gmix(const Shape& sh, const void* x, const float* stats, int n
   const size_t lds = v->lds();
   hipError_t e = hipFuncSetAttribute((const void*)v->k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(v->k, dim3(8 * p.per), dim3(kThreads), lds, st, p);
+  hipLaunchKernelGGL(v->k, dim3(8 * p.per), dim3(threads_of(v->NH)), lds, st, p);
   return hipGetLastError();
 }
 

@@ -243,8 +243,9 @@ def test_forward_static_host_errors(lib):
     assert _call_static(desc, gate, U=None, nU=2) == -1
     assert _call_static(desc, gate, nU=65) == -2
     assert _call_static(desc, gate, y=FAKE_UNALIGNED) == -8
-    # a workspace beyond the array: B * R * k coefficients of 4 bytes alone exceed 16 MiB
-    big = good_desc(B=64, C=4096, E=4096, k=64, H=2, W=2)
+    # a workspace beyond the array: B * R * k coefficients of 4 bytes alone exceed 16 MiB (H W = 2 keeps
+    # the shape off the scheduled mix, which holds no coefficients)
+    big = good_desc(B=64, C=4096, E=4096, k=64, H=1, W=2)
     assert lib.moce_forward_workspace_bytes(ctypes.byref(big)) > mb.MOCE_STATIC_SCRATCH_BYTES
     assert _call_static(big, gate) == -7
 

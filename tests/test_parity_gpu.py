@@ -542,7 +542,10 @@ def test_forward_path_choice():
     assert path(4, 2048, 520, 12, 7, 7, layout="nhwc") == mb.PATH_SCHEDULED  # E - 1 > 512 with k > 8
     assert path(4, 2048, 513, 12, 7, 7, layout="nhwc") == mb.PATH_GATHER
     assert path(4, 100, 24, 8, 7, 7, layout="nhwc") == mb.PATH_GENERIC      # C not a multiple of 8
-    assert path(4, 512, 64, 32, 16, 16) == mb.PATH_GENERIC       # C > 256
+    assert path(4, 512, 64, 32, 16, 16) == mb.PATH_SCHEDULED     # C > 256: the scheduled product
+    assert path(64, 1024, 256, 64, 14, 14) == mb.PATH_SCHEDULED  # the stage-3 layer, channels-first
+    assert path(4, 512, 64, 32, 15, 15) == mb.PATH_GENERIC       # H W not a multiple of 4
+    assert path(4, 520, 64, 32, 16, 16) == mb.PATH_GENERIC       # C not a multiple of 64
     assert path(4, 96, 24, 12, 30, 30) == mb.PATH_GENERIC        # H*W not a multiple of 8
     assert path(4, 64, 1, 8, 8, 8) == mb.PATH_GENERIC            # no routed expert
 
@@ -633,6 +636,35 @@ def test_scheduled_forward_shapes(B, C, E, k, H, W, extra):
     check_y(y, ref["y"], ref["mag"], "bf16")
     if ref["nU"] == 0:
         assert np.all(y[..., E - 1] == 0.0)
+
+
+SCHEDULED_NCHW = [
+    # B, C, E, k, H, W, extra: channels-first shapes served by the scheduled product
+    (3, 1024, 256, 64, 14, 14, {}),            # stage-3 layer: 196 positions over two 112-row tiles
+    (2, 2048, 512, 128, 7, 8, {}),             # 32 steps, four expert ranges
+    (2, 512, 64, 32, 16, 16, dict(signed=True)),
+    (2, 320, 40, 17, 6, 10, {}),               # 5 steps; residual row in a partial group; 60 positions
+    (1, 64, 64, 64, 1, 4, {}),                 # one step, E = C = k, 4 positions (off the tile paths)
+    (2, 512, 24, 17, 3, 12, dict(cyclic=True)),  # cyclic supports: U = channels 391..511
+    (2, 384, 56, 8, 4, 4, dict(cyclic=True)),  # cyclic supports wrapping past C: U empty
+    (3, 768, 192, 48, 8, 25, dict(signed=True)),  # 200 positions: ragged last tile
+    (4, 512, 40, 1, 6, 6, {}),                 # k = 1: exact copies
+    (1, 4096, 16, 20, 2, 2, {}),               # C = 4096: 64 steps
+]
+
+
+@pytest.mark.parametrize("B,C,E,k,H,W,extra", SCHEDULED_NCHW)
+def test_scheduled_nchw_forward_shapes(B, C, E, k, H, W, extra):
+    x, s, w, a, c = _custom(B, C, E, k, H, W, "bf16", "nchw", seed=B * 37 + C + E + k, **extra)
+    ref = oracle.forward(x, s, w, E, oracle.NCHW, a=a, c=c)
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nchw", s, w, a=a, c=c)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_SCHEDULED
+    y = to_host_f64(layer.forward(to_device_x(x, "bf16")))
+    check_y(y, ref["y"], ref["mag"], "bf16")
+    if ref["nU"] == 0:
+        assert np.all(y[:, E - 1] == 0.0)
+    if k == 1:
+        assert np.array_equal(y[:, :E - 1], ref["y"][:, :E - 1])
 
 
 def test_scheduled_forward_mlp_gate_and_one_hot():
