@@ -86,6 +86,113 @@ __host__ __device__ inline int list_len(int k) {
 }
 __host__ __device__ inline int wave_words(int k) { return 256 + 2 * list_len(k); }
 
+// The top k of one logit row by one wave: the k-th largest key by a radix
+// select, most significant byte first, then the keys above it and the
+// lowest-channel ones equal to it, sorted into the canonical order (logit
+// descending, channel ascending).  hist: 256 words of LDS; lkey, lch: P
+// entries each (P = list_len(k)), which may overlap hist.
+__device__ __forceinline__ void select_row(const float* row, uint32_t* hist, uint32_t* lkey, int32_t* lch, int C,
+                                           int k, int P, int lane, int32_t* __restrict__ Sout,
+                                           float* __restrict__ Wout) {
+    // the k-th largest key, most significant byte first: after each round,
+  // `prefix` holds the known high bytes and kk the rank still to find
+  // among the keys with that prefix
+  uint32_t prefix = 0, mask = 0;
+  int kk = k;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = lane; i < 256; i += kWave) hist[i] = 0;
+    lds_wait();
+    for (int c = lane; c < C; c += kWave) {
+      const uint32_t key = fkey(row[c]);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    lds_wait();
+    // lane l holds bins 4 l .. 4 l + 3; counts above a lane's bins by a
+    // suffix sum over the lanes
+    uint32_t cnt[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cnt[j] = hist[4 * lane + j];
+    const uint32_t mine = cnt[0] + cnt[1] + cnt[2] + cnt[3];
+    uint32_t incl = mine;  // sum over lanes >= this one
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const uint32_t o = __shfl_down(incl, off, kWave);
+      if (lane + off < kWave) incl += o;
+    }
+    uint32_t above = incl - mine;
+    int digit = -1;
+    uint32_t before_digit = 0;
+    if (above < (uint32_t)kk && (uint32_t)kk <= incl) {
+#pragma unroll
+      for (int j = 3; j >= 0; --j) {
+        if (digit < 0 && above + cnt[j] >= (uint32_t)kk) {
+          digit = 4 * lane + j;
+          before_digit = above;
+        }
+        above += cnt[j];
+      }
+    }
+    const uint64_t found = __ballot(digit >= 0);
+    const int src = __builtin_ctzll(found);
+    digit = __shfl(digit, src, kWave);
+    before_digit = __shfl(before_digit, src, kWave);
+    kk -= (int)before_digit;
+    prefix |= (uint32_t)digit << shift;
+    mask |= 255u << shift;
+    lds_wait();
+  }
+  // every key above the k-th is taken, and the lowest-channel kk of those
+  // equal to it; gathered in channel order
+  const uint32_t kstar = prefix;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int taken = 0, eq_seen = 0;
+  for (int c0 = 0; c0 < C; c0 += kWave) {
+    const int c = c0 + lane;
+    const uint32_t key = c < C ? fkey(row[c]) : 0u;
+    const bool eq = c < C && key == kstar;
+    const uint64_t beq = __ballot(eq);
+    const bool sel = (c < C && key > kstar) || (eq && eq_seen + __popcll(beq & below) < kk);
+    const uint64_t bsel = __ballot(sel);
+    if (sel && taken + __popcll(bsel & below) < P) {
+      const int pos = taken + __popcll(bsel & below);
+      lkey[pos] = key;
+      lch[pos] = c;
+    }
+    taken += __popcll(bsel);
+    eq_seen += __popcll(beq);
+  }
+  // bitonic sort of the k (padded to a power of two with entries that sort
+  // last) into the canonical order
+  for (int i = k + lane; i < P; i += kWave) {
+    lkey[i] = 0u;
+    lch[i] = INT_MAX;
+  }
+  lds_wait();
+  for (int size = 2; size <= P; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = lane; i < P / 2; i += kWave) {
+        const int lo = 2 * stride * (i / stride) + (i % stride), hi = lo + stride;
+        const uint32_t ka = lkey[lo], kb = lkey[hi];
+        const int ca = lch[lo], cb = lch[hi];
+        // runs of `size` alternate between the canonical order and its reverse
+        const bool forward = (lo & size) == 0;
+        if (forward ? before(kb, cb, ka, ca) : before(ka, ca, kb, cb)) {
+          lkey[lo] = kb;
+          lch[lo] = cb;
+          lkey[hi] = ka;
+          lch[hi] = ca;
+        }
+      }
+      lds_wait();
+    }
+  }
+  for (int i = lane; i < k; i += kWave) {
+    Sout[i] = lch[i];
+    Wout[i] = fkey_value(lkey[i]);
+  }
+  lds_wait();
+}
+
 // EB experts of one image per workgroup of EB waves (a row each); DD >= the
 // bottleneck width
 template <int EB, int DD>
@@ -133,105 +240,79 @@ k_dyn_select(const float* __restrict__ h, const float* __restrict__ L, const flo
   __syncthreads();
   // each wave: one row
   for (int e = wv; e < ne; e += EB) {
-    const float* row = rows + e * C;
-    // the k-th largest key, most significant byte first: after each round,
-    // `prefix` holds the known high bytes and kk the rank still to find
-    // among the keys with that prefix
-    uint32_t prefix = 0, mask = 0;
-    int kk = k;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = lane; i < 256; i += kWave) hist[i] = 0;
-      lds_wait();
-      for (int c = lane; c < C; c += kWave) {
-        const uint32_t key = fkey(row[c]);
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-      }
-      lds_wait();
-      // lane l holds bins 4 l .. 4 l + 3; counts above a lane's bins by a
-      // suffix sum over the lanes
-      uint32_t cnt[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) cnt[j] = hist[4 * lane + j];
-      const uint32_t mine = cnt[0] + cnt[1] + cnt[2] + cnt[3];
-      uint32_t incl = mine;  // sum over lanes >= this one
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const uint32_t o = __shfl_down(incl, off, kWave);
-        if (lane + off < kWave) incl += o;
-      }
-      uint32_t above = incl - mine;
-      int digit = -1;
-      uint32_t before_digit = 0;
-      if (above < (uint32_t)kk && (uint32_t)kk <= incl) {
-#pragma unroll
-        for (int j = 3; j >= 0; --j) {
-          if (digit < 0 && above + cnt[j] >= (uint32_t)kk) {
-            digit = 4 * lane + j;
-            before_digit = above;
-          }
-          above += cnt[j];
-        }
-      }
-      const uint64_t found = __ballot(digit >= 0);
-      const int src = __builtin_ctzll(found);
-      digit = __shfl(digit, src, kWave);
-      before_digit = __shfl(before_digit, src, kWave);
-      kk -= (int)before_digit;
-      prefix |= (uint32_t)digit << shift;
-      mask |= 255u << shift;
-      lds_wait();
-    }
-    // every key above the k-th is taken, and the lowest-channel kk of those
-    // equal to it; gathered in channel order
-    const uint32_t kstar = prefix;
-    const uint64_t below = (1ull << lane) - 1ull;
-    int taken = 0, eq_seen = 0;
-    for (int c0 = 0; c0 < C; c0 += kWave) {
-      const int c = c0 + lane;
-      const uint32_t key = c < C ? fkey(row[c]) : 0u;
-      const bool eq = c < C && key == kstar;
-      const uint64_t beq = __ballot(eq);
-      const bool sel = (c < C && key > kstar) || (eq && eq_seen + __popcll(beq & below) < kk);
-      const uint64_t bsel = __ballot(sel);
-      if (sel && taken + __popcll(bsel & below) < P) {
-        const int pos = taken + __popcll(bsel & below);
-        lkey[pos] = key;
-        lch[pos] = c;
-      }
-      taken += __popcll(bsel);
-      eq_seen += __popcll(beq);
-    }
-    // bitonic sort of the k (padded to a power of two with entries that sort
-    // last) into the canonical order
-    for (int i = k + lane; i < P; i += kWave) {
-      lkey[i] = 0u;
-      lch[i] = INT_MAX;
-    }
-    lds_wait();
-    for (int size = 2; size <= P; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int i = lane; i < P / 2; i += kWave) {
-          const int lo = 2 * stride * (i / stride) + (i % stride), hi = lo + stride;
-          const uint32_t ka = lkey[lo], kb = lkey[hi];
-          const int ca = lch[lo], cb = lch[hi];
-          // runs of `size` alternate between the canonical order and its reverse
-          const bool forward = (lo & size) == 0;
-          if (forward ? before(kb, cb, ka, ca) : before(ka, ca, kb, cb)) {
-            lkey[lo] = kb;
-            lch[lo] = cb;
-            lkey[hi] = ka;
-            lch[hi] = ca;
-          }
-        }
-        lds_wait();
-      }
-    }
     const int64_t item = b * R + e0 + e;
-    for (int i = lane; i < k; i += kWave) {
-      S[item * k + i] = lch[i];
-      W[item * k + i] = fkey_value(lkey[i]);
+    select_row(rows + e * C, hist, lkey, lch, C, k, P, lane, S + item * k, W + item * k);
+  }
+}
+
+// The same with the channel embeddings read once per workgroup: 16 waves hold
+// v_c of CPT channels each in registers and walk nbp consecutive blocks of 16
+// experts of one image, forming the block's rows in LDS (the same arithmetic,
+// in the same order, as k_dyn_select) and selecting a row per wave.  Where
+// 2 P <= 256 a wave's list overlaps its histogram (the histogram is dead once
+// the k-th key is known).
+constexpr int kSel2Waves = 16;
+__host__ __device__ inline int wave_words2(int k) {
+  return 2 * list_len(k) <= 256 ? 256 : 256 + 2 * list_len(k);
+}
+
+template <int DD, int CPT>
+__global__ void __launch_bounds__(kSel2Waves * kWave)
+k_dyn_select2(const float* __restrict__ h, const float* __restrict__ L, const float* __restrict__ q,
+              const float* __restrict__ vT, int32_t* __restrict__ S, float* __restrict__ W, int C, int R, int k,
+              int dd, int nblk, int nbp, int nsplit) {
+  constexpr int EB = kSel2Waves;
+  extern __shared__ float sm[];
+  float* rows = sm;              // [EB][C]
+  float* qh = rows + EB * C;     // [EB][DD]
+  const int P = list_len(k);
+  const int ww = wave_words2(k);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(qh + EB * DD) + (threadIdx.x >> 6) * ww;
+  uint32_t* lkey = ww == 256 ? hist : hist + 256;
+  int32_t* lch = reinterpret_cast<int32_t*>(lkey + P);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t b = blockIdx.x / nsplit;
+  const int blk0 = (int)(blockIdx.x % nsplit) * nbp;
+  const int blk1 = min(blk0 + nbp, nblk);
+  float vr[CPT][DD];
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    const int c = min((int)threadIdx.x + j * EB * kWave, C - 1);
+#pragma unroll
+    for (int t = 0; t < DD; ++t) {
+      const float x = vT[(int64_t)min(t, dd - 1) * C + c];
+      vr[j][t] = t < dd ? x : 0.f;
     }
-    lds_wait();
+  }
+  for (int blk = blk0; blk < blk1; ++blk) {
+    const int e0 = blk * EB;
+    const int ne = min(EB, R - e0);
+    for (int i = threadIdx.x; i < EB * DD; i += blockDim.x) {
+      const int e = i / DD, t = i - e * DD;
+      const float qv = q[(int64_t)min(e0 + e, R - 1) * dd + min(t, dd - 1)];
+      const float hv = h[b * dd + min(t, dd - 1)];
+      qh[i] = t < dd ? qv * hv : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int c = (int)threadIdx.x + j * EB * kWave;
+      if (c < C) {
+#pragma unroll 4
+        for (int e = 0; e < EB; ++e) {
+          float off = 0.f;
+#pragma unroll
+          for (int t = 0; t < DD; ++t) off += qh[e * DD + t] * vr[j][t];
+          rows[e * C + c] = L[(int64_t)min(e0 + e, R - 1) * C + c] + off;
+        }
+      }
+    }
+    __syncthreads();
+    if (wv < ne) {
+      const int64_t item = b * R + e0 + wv;
+      select_row(rows + wv * C, hist, lkey, lch, C, k, P, lane, S + item * k, W + item * k);
+    }
+    __syncthreads();  // rows and qh free for the next block
   }
 }
 
@@ -412,15 +493,51 @@ int select_eb(const Shape& sh, int DD) {
   return 0;
 }
 
+size_t select2_lds(const Shape& sh, int DD) {
+  return ((size_t)kSel2Waves * sh.C + (size_t)kSel2Waves * DD + (size_t)kSel2Waves * wave_words2(sh.k)) * 4;
+}
+// channels per thread of k_dyn_select2, or 0 where its registers or LDS do
+// not hold the shape
+int select2_cpt(const Shape& sh, int DD) {
+  const int cpt = (int)((sh.C + kSel2Waves * kWave - 1) / (kSel2Waves * kWave));
+  if (cpt * DD > 64 || select2_lds(sh, DD) > kDynLds) return 0;
+  return cpt;
+}
+
 template <int DD>
 hipError_t launch_select_dd(const Shape& sh, const float* h, const float* L, const float* q, const float* vT,
                             int32_t* S, float* W, int dd, hipStream_t st) {
+  using K = void (*)(const float*, const float*, const float*, const float*, int32_t*, float*, int, int, int, int,
+                     int);
+  using K2 = void (*)(const float*, const float*, const float*, const float*, int32_t*, float*, int, int, int, int,
+                      int, int, int);
+  // the register-held embeddings where the per-block kernel's LDS limits its
+  // blocks below eight experts (each block then reads every embedding for
+  // fewer than eight rows)
+  const int cpt = select_eb(sh, DD) < 8 ? select2_cpt(sh, DD) : 0;
+  if (cpt > 0) {
+    // blocks of 16 experts, nbp per workgroup, for about two workgroups per CU
+    const int nblk = (sh.R + kSel2Waves - 1) / kSel2Waves;
+    int cus = 256, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    const int64_t total = sh.B * nblk;
+    const int nbp = (int)std::max<int64_t>(1, std::min<int64_t>(nblk, total / (2 * cus)));
+    const int nsplit = (nblk + nbp - 1) / nbp;
+    const size_t lds = select2_lds(sh, DD);
+    const K2 kern = cpt == 1 ? k_dyn_select2<DD, 1> : k_dyn_select2<DD, (DD <= 32 ? 2 : 1)>;
+    if (cpt == 2 && DD > 32) return hipErrorInvalidValue;
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(sh.B * nsplit)), dim3(kSel2Waves * kWave), lds, st, h, L, q, vT, S, W,
+                       (int)sh.C, sh.R, sh.k, dd, nblk, nbp, nsplit);
+    return hipGetLastError();
+  }
   const int eb = select_eb(sh, DD);
   if (eb == 0) return hipErrorInvalidValue;
   const int nblk = (sh.R + eb - 1) / eb;
   const size_t lds = select_lds(sh, eb, DD);
-  using K = void (*)(const float*, const float*, const float*, const float*, int32_t*, float*, int, int, int, int,
-                     int);
   const K kern = eb == 8 ? k_dyn_select<8, DD> : eb == 4 ? k_dyn_select<4, DD> : eb == 2 ? k_dyn_select<2, DD>
                                                                                        : k_dyn_select<1, DD>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
