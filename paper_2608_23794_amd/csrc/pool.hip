@@ -170,15 +170,8 @@ hipError_t pool_nhwc(const Shape& sh, const T* x, float* d, hipStream_t st) {
                        HW, nblk);
     return hipGetLastError();
   }
-  if ((sh.C * sizeof(T)) % 16 == 0) {
-    const int nblk = (C / EPV16 + 63) / 64;
-    hipLaunchKernelGGL((k_pool_nhwc<T, EPV16>), dim3((unsigned)(sh.B * nblk)), dim3(256), 0, st, x, d,
-                       C, HW, nblk);
-  } else {
-    const int nblk = (C + 63) / 64;
-    hipLaunchKernelGGL((k_pool_nhwc<T, 1>), dim3((unsigned)(sh.B * nblk)), dim3(256), 0, st, x, d, C,
-                       HW, nblk);
-  }
+  const int nblk = (C + 63) / 64;
+  hipLaunchKernelGGL((k_pool_nhwc<T, 1>), dim3((unsigned)(sh.B * nblk)), dim3(256), 0, st, x, d, C, HW, nblk);
   return hipGetLastError();
 }
 

@@ -31,43 +31,50 @@ template <> struct PoolVec<float> {
 };
 
 // Channels of block cb: 32 EPV of them from channel 32 EPV cb (C a multiple of
-// EPV; vectors past C are skipped).  `part` is LDS of
-// kPoolGroups * 32 * EPV floats.  The mean of channel c of image b goes to
-// d[b sb + c sc]: sb = C, sc = 1 for d[B][C], sb = 1, sc = B for its transpose.
+// EPV).  A block with nv < 32 vectors (C below 32 EPV) gives each vector
+// rep = 32 / nv lanes of a row group, which take positions in turn, so that
+// no lane idles; with nv = 32 lane l reads vector l at positions rg,
+// rg + 32, ...  `part` is LDS of kPoolGroups * 32 * EPV floats.  The mean of
+// channel c of image b goes to d[b sb + c sc]: sb = C, sc = 1 for d[B][C],
+// sb = 1, sc = B for its transpose.
 template <typename T>
 __device__ __forceinline__ void pool_rows_block(const T* __restrict__ x, float* __restrict__ d, int C, int HW,
                                                 int64_t b, int cb, float* part, int64_t sb, int64_t sc) {
   constexpr int EPV = PoolVec<T>::EPV;
   const int l = threadIdx.x & 31, rg = threadIdx.x >> 5;
-  const int c0 = (cb * 32 + l) * EPV;
+  const int nv = min(32, C / EPV - 32 * cb);
+  const int rep = 32 / nv;
+  const int v = l % nv, sub = l / nv;
+  const int c0 = (cb * 32 + v) * EPV;
   float acc[EPV];
 #pragma unroll
   for (int j = 0; j < EPV; ++j) acc[j] = 0.f;
-  if (c0 < C) {
+  if (sub < rep) {
     const T* col = x + b * HW * (int64_t)C + c0;
-    for (int p0 = rg; p0 < HW; p0 += 4 * kPoolGroups) {
-      uint4 v[4];
+    const int stride = kPoolGroups * rep;  // positions between a lane's consecutive reads
+    for (int p0 = rg * rep + sub; p0 < HW; p0 += 4 * stride) {
+      uint4 vv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int p = min(p0 + u * kPoolGroups, HW - 1);
-        v[u] = *reinterpret_cast<const uint4*>(col + (int64_t)p * C);
+        const int p = min(p0 + u * stride, HW - 1);
+        vv[u] = *reinterpret_cast<const uint4*>(col + (int64_t)p * C);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        if (p0 + u * kPoolGroups < HW) PoolVec<T>::add(v[u], acc);
+        if (p0 + u * stride < HW) PoolVec<T>::add(vv[u], acc);
     }
   }
 #pragma unroll
   for (int j = 0; j < EPV; ++j) part[(rg * 32 + l) * EPV + j] = acc[j];
   __syncthreads();
-  // channel i of the block: the 32 row groups' sums in order
-  for (int i = threadIdx.x; i < 32 * EPV; i += kPoolThreads) {
-    const int c = cb * 32 * EPV + i;
-    if (c < C) {
-      float s = 0.f;
-      for (int r = 0; r < kPoolGroups; ++r) s += part[r * 32 * EPV + i];
-      d[b * sb + c * sc] = s / (float)HW;
-    }
+  // channel i of the block: the partial sums of its rep lanes in each of the
+  // 32 row groups, in a fixed order
+  for (int i = threadIdx.x; i < nv * EPV; i += kPoolThreads) {
+    const int vi = i / EPV, j = i - vi * EPV;
+    float s = 0.f;
+    for (int r = 0; r < kPoolGroups; ++r)
+      for (int m = 0; m < rep; ++m) s += part[(r * 32 + vi + m * nv) * EPV + j];
+    d[b * sb + (int64_t)(cb * 32 * EPV + i) * sc] = s / (float)HW;
   }
 }
 
