@@ -56,3 +56,29 @@ def test_static_forward_full_stage1_batch():
     mb.moce_forward_static(layer.desc(wl.B), x, layer.s_c, layer.w_c, layer.gate, None, layer.nU, y)
     torch.cuda.synchronize()
     assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
+
+
+def test_static_forward_on_the_gather_path():
+    """A channels-last layer with small supports (the gather path: coefficients in the array), two
+    calls in a row, the second on fewer images with other values."""
+    rng = np.random.default_rng(91)
+    B, C, E, k, H, W = 6, 256, 72, 8, 9, 9
+    R = E - 1
+    s = np.array([rng.choice(C, k, replace=False) for _ in range(R)], np.int32)
+    w = rng.standard_normal((R, k)).astype(np.float32)
+    a = (rng.standard_normal((R, k)) * k ** -0.5).astype(np.float32)
+    c = np.zeros(R, np.float32)
+    x = inputs.f32_to_bf16_bits(np.maximum(rng.standard_normal((B, H, W, C)), 0).astype(np.float32))
+    layer = MoceLayer(C, E, k, H, W, "bf16", "nhwc", s, w, a=a, c=c)
+    assert mb.moce_forward_path(layer.desc(B), mb.MOCE_GATE_SOFTPLUS_LINEAR) == mb.PATH_GATHER
+    x1 = to_device_x(x, "bf16")
+    x2 = (x1[:2].float() * -1.5 + 0.25).to(x1.dtype).contiguous()
+    U = layer.U if layer.nU else None
+    for xx in (x1, x2):
+        desc = layer.desc(xx.shape[0])
+        y_ref = layer.forward(xx)
+        y = torch.full_like(y_ref, float("nan"))
+        mb.moce_forward_static(desc, xx, layer.s_c, layer.w_c, layer.gate, U, layer.nU, y,
+                               torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
