@@ -150,7 +150,7 @@ hipError_t pool_nchw(const Shape& sh, const T* x, float* d, hipStream_t st) {
   return hipGetLastError();
 }
 
-// 1024 threads per (image, block of 32 16-byte channel vectors)
+// kPoolThreads threads per (image, block of 32 16-byte channel vectors)
 template <typename T>
 __global__ void __launch_bounds__(kPoolThreads)
 k_pool_nhwc_rows(const T* __restrict__ x, float* __restrict__ d, int C, int HW, int nblk) {

@@ -1,8 +1,10 @@
-// Channels-last pooling of one (image, channel block) by a 1024-thread
-// workgroup (Sec. 3.3: the descriptor is the spatial mean of each channel).
-// Lane l of the 32-lane row groups reads the 16-byte channel vector l of the
-// block; row group r takes positions r, r + 32, ..., four of them per round
-// with all four loads in flight.  The 32 partial sums of each channel are then
+// Channels-last pooling of one (image, channel block) by a workgroup of
+// kPoolThreads threads (Sec. 3.3: the descriptor is the spatial mean of each
+// channel); 512 threads, so that several workgroups share a CU and small
+// images still keep enough loads in flight.  Lane l of the 32-lane row groups
+// reads the 16-byte channel vector l of the block; row group r takes
+// positions r, r + kPoolGroups, ..., four of them per round with all four
+// loads in flight.  The kPoolGroups partial sums of each channel are then
 // added in a fixed order through LDS, so the result does not depend on
 // timing.
 #pragma once
@@ -11,7 +13,7 @@
 
 namespace moce {
 
-constexpr int kPoolThreads = 1024;
+constexpr int kPoolThreads = 512;
 constexpr int kPoolGroups = kPoolThreads / 32;  // row groups
 
 template <typename T> struct PoolVec;
