@@ -393,6 +393,15 @@ __device__ __forceinline__ void builder(const GmArgs& p, unsigned char* smem, in
   const int lane = threadIdx.x & 63;
   float4* st = reinterpret_cast<float4*>(smem + L::OFF_ST);
   const int o0 = q * L::NE;
+  const int bucket = q * kBuilders + j;
+  const int32_t* ob = p.off + (int64_t)bucket * (p.nsteps + 1);
+  const uint2* eb = p.ent + (int64_t)bucket * p.cap;
+  // step 0's list starts at the bucket's first entry, so its loads go out
+  // first, beside those of the offsets and the statistics: the prologue waits
+  // for one round trip to memory instead of two
+  uint2 e0[kRounds];
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) e0[r] = eb[min(64 * r + lane, p.cap - 1)];
   // this builder's groups' statistics into LDS and their B rows (both
   // buffers, every part) zeroed; the bucket's offsets into registers
 #pragma unroll
@@ -411,11 +420,8 @@ __device__ __forceinline__ void builder(const GmArgs& p, unsigned char* smem, in
           u32x4{0u, 0u, 0u, 0u};
     }
   }
-  const int bucket = q * kBuilders + j;
-  const int32_t* ob = p.off + (int64_t)bucket * (p.nsteps + 1);
   const int ofr = ob[min(lane, p.nsteps)];
   const int tot = __builtin_amdgcn_readfirstlane(ob[p.nsteps]);
-  const uint2* eb = p.ent + (int64_t)bucket * p.cap;
   // offset t of the bucket (t uniform, 0 <= t <= nsteps <= 64)
   auto ofs = [&](int t) __attribute__((always_inline)) {
     return t < kMaxSteps ? __builtin_amdgcn_readlane(ofr, t) : tot;
@@ -486,7 +492,10 @@ __device__ __forceinline__ void builder(const GmArgs& p, unsigned char* smem, in
   uint2 ring[kAhead][kRounds];
   int cnt[kAhead];
 #pragma unroll
-  for (int a = 0; a < kAhead; ++a) cnt[a] = fetch(a, ring[a]);
+  for (int r = 0; r < kRounds; ++r) ring[0][r] = e0[r];
+  cnt[0] = ofs(min(1, p.nsteps)) - ofs(0);
+#pragma unroll
+  for (int a = 1; a < kAhead; ++a) cnt[a] = fetch(a, ring[a]);
   uint2 prev[2][kRounds];
   int pcnt[2] = {0, 0};
   __builtin_amdgcn_s_waitcnt(vm_wait((kAhead - 1) * kRounds));
