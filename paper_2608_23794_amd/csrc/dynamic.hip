@@ -585,6 +585,7 @@ hipError_t launch_dynamic(const Shape& sh, const void* x, const float* L, const 
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  if (tilemix_dynamic_eligible(sh)) return launch_tilemix_dynamic(sh, x, S, alpha, U, nU, y, st);
   const int ntiles = (int)((sh.HW + kDynTP - 1) / kDynTP);
   const size_t lds = (size_t)sh.C * kDynTP * sizeof(float);
   const unsigned grid = (unsigned)(sh.B * ntiles);

@@ -158,6 +158,11 @@ bool tilemix_eligible(const Shape& sh);
 size_t tilemix_lds_bytes(const Shape& sh);
 hipError_t launch_tilemix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
                           int nU, void* y, hipStream_t st);
+// The same mix with input-conditioned supports S [B][R][k], uncovered lists
+// U [B][C] and counts nU [B].
+bool tilemix_dynamic_eligible(const Shape& sh);
+hipError_t launch_tilemix_dynamic(const Shape& sh, const void* x, const int32_t* S, const float* alpha,
+                                  const int32_t* U, const int32_t* nU, void* y, hipStream_t st);
 
 // Mixing as a dense bf16 product on the matrix cores (mfmamix.hip), for NCHW
 // bfloat16 with R >= 1, C a multiple of 32 up to 256, E <= 64 and H*W a

@@ -31,6 +31,9 @@ constexpr int kExpertsPerPass = 4 * kWaves;
 struct TileArgs {
   int B, C, HW, E, R, k, kq, nU;  // kq: k rounded up to a multiple of 4
   int nt, ntiles;                 // tiles per image, tiles in the batch
+  // input-conditioned supports: per image rows s[b][R][k], uncovered lists
+  // U[b][C] and counts nUb[b] (null for the static supports)
+  const int32_t* nUb;
 };
 
 // LDS regions in bytes: tile [C][kTT] float, coefficients [R][kq] float,

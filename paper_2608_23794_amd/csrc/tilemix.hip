@@ -43,6 +43,9 @@ k_tilemix(TileArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rkq = p.R * p.kq;
+  const bool dyn = p.nUb != nullptr;
+  // the support rows of image b (the same rows for every image when static)
+  auto srows = [&](int b) { return dyn ? s + (int64_t)b * p.R * p.k : s; };
 
   // The first two tiles' loads go out first; the support offsets and the
   // first image's coefficients are then read with all loads issued before
@@ -55,11 +58,12 @@ k_tilemix(TileArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, 
   if (pre) {
     int32_t sv[kASlots];
     float av[kASlots];
+    const int32_t* sr = srows(cur);
 #pragma unroll
     for (int q = 0; q < kASlots; ++q) {
       const int e = threadIdx.x + q * kThreads;
       const int o = e / p.kq, i = e - (e / p.kq) * p.kq;
-      sv[q] = s[min((int64_t)o * p.k + i, (int64_t)p.R * p.k - 1)];
+      sv[q] = min(max(sr[min((int64_t)o * p.k + i, (int64_t)p.R * p.k - 1)], 0), p.C - 1);
       av[q] = alpha[min((int64_t)cur * p.R * p.k + (int64_t)o * p.k + i, (int64_t)p.B * p.R * p.k - 1)];
     }
 #pragma unroll
@@ -73,9 +77,10 @@ k_tilemix(TileArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, 
       }
     }
   } else {
+    const int32_t* sr = srows(cur);
     for (int e = threadIdx.x; e < rkq; e += kThreads) {
       const int o = e / p.kq, i = e - (e / p.kq) * p.kq;
-      const int32_t sv = s[min((int64_t)o * p.k + i, (int64_t)p.R * p.k - 1)];
+      const int32_t sv = min(max(sr[min((int64_t)o * p.k + i, (int64_t)p.R * p.k - 1)], 0), p.C - 1);
       sofs[e] = (uint16_t)((i < p.k ? sv : 0) * kRowBytes);
       al[e] = alpha_entry(p, alpha, cur, e);
     }
@@ -105,6 +110,14 @@ k_tilemix(TileArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, 
       } else {
         for (int e = threadIdx.x; e < rkq; e += kThreads) al[e] = alpha_entry(p, alpha, b, e);
       }
+      if (dyn) {  // the image's own supports
+        const int32_t* sr = srows(b);
+        for (int e = threadIdx.x; e < rkq; e += kThreads) {
+          const int o = e / p.kq, i = e - (e / p.kq) * p.kq;
+          const int32_t sv = min(max(sr[min((int64_t)o * p.k + i, (int64_t)p.R * p.k - 1)], 0), p.C - 1);
+          sofs[e] = (uint16_t)((o < p.R && i < p.k ? sv : 0) * kRowBytes);
+        }
+      }
       cur = b;
       __syncthreads();
     }
@@ -131,7 +144,7 @@ k_tilemix(TileArgs p, const uint16_t* __restrict__ x, uint16_t* __restrict__ y, 
         if (o < p.R)
           acc = mix_expert<K>(sofs + o * p.kq, al + o * p.kq, base, p.kq);
         else if (o == p.R)
-          acc = residual(U, p.nU, base);
+          acc = dyn ? residual(U + (int64_t)b * p.C, p.nUb[b], base) : residual(U, p.nU, base);
         if (NP > 0)
           res[q] = acc;
         else if (store && o <= p.R)
@@ -306,9 +319,12 @@ bool tilemix_eligible(const Shape& sh) {
   return tilemix_lds_bytes(sh) <= (size_t)kMaxLds;
 }
 
-hipError_t launch_tilemix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
-                          int nU, void* y, hipStream_t st) {
+namespace {
+
+hipError_t tilemix_launch(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
+                          int nU, const int32_t* nUb, void* y, hipStream_t st) {
   TileArgs p;
+  p.nUb = nUb;
   p.B = (int)sh.B;
   p.C = (int)sh.C;
   p.HW = (int)sh.HW;
@@ -324,14 +340,35 @@ hipError_t launch_tilemix(const Shape& sh, const void* x, const int32_t* s, cons
   if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
   const int grid = (int)std::min<int64_t>((int64_t)cus * kPerCU, p.ntiles);
-  const size_t lds = tilemix_lds_bytes(sh);
-  const TileKernel kern = pick_kernel(sh);
+  // input-conditioned supports take the LDS-table kernel, which reloads the
+  // support rows when the image changes
+  const size_t lds = nUb ? tile_lds((int)sh.C, sh.R, rounded_k(sh)).total : tilemix_lds_bytes(sh);
+  const TileKernel kern = nUb ? k_tilemix<0, 0> : pick_kernel(sh);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, st, p, static_cast<const uint16_t*>(x),
                      static_cast<uint16_t*>(y), s, alpha, U);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_tilemix(const Shape& sh, const void* x, const int32_t* s, const float* alpha, const int32_t* U,
+                          int nU, void* y, hipStream_t st) {
+  return tilemix_launch(sh, x, s, alpha, U, nU, nullptr, y, st);
+}
+
+bool tilemix_dynamic_eligible(const Shape& sh) {
+  if (sh.layout != MOCE_NCHW || sh.elem != MOCE_BF16 || sh.R < 1) return false;
+  if (sh.HW % 8 != 0 || sh.C > 256) return false;
+  if (sh.B * tiles_per_image(sh) > INT32_MAX / 2) return false;
+  return tile_lds((int)sh.C, sh.R, rounded_k(sh)).total <= (size_t)kMaxLds;
+}
+
+hipError_t launch_tilemix_dynamic(const Shape& sh, const void* x, const int32_t* S, const float* alpha,
+                                  const int32_t* U, const int32_t* nU, void* y, hipStream_t st) {
+  return tilemix_launch(sh, x, S, alpha, U, 0, nU, y, st);
 }
 
 }  // namespace moce

@@ -111,6 +111,12 @@ def test_dynamic_forward_mlp_gate(name, layout):
     (2, 300, 20, 200, 64, 1, 5, "f32", "nhwc"),  # k past a power of two, the widest router
     (1, 70, 2, 9, 5, 1, 1, "bf16", "nchw"),      # one routed expert, one position
     (2, 4096, 9, 512, 16, 1, 2, "f32", "nhwc"),  # the size limits: C = 4096, k = 512
+    # bfloat16 NCHW with C <= 256 and H W a multiple of 8 takes the tile mix, which reloads the
+    # supports when the image changes: one tile per image, a ragged last tile, and a coefficient
+    # table too large to prefetch in registers
+    (6, 64, 17, 8, 4, 4, 6, "bf16", "nchw"),
+    (3, 256, 64, 16, 8, 12, 12, "bf16", "nchw"),
+    (2, 200, 200, 12, 8, 8, 8, "bf16", "nchw"),
 ])
 def test_dynamic_forward_edges(B, C, E, k, d, H, W, dtype, layout):
     rng = np.random.default_rng(B * 7919 + C)
