@@ -235,6 +235,23 @@ k_pool_sched(const T* __restrict__ x, float* __restrict__ d, int C, int HW, int 
   pool_rows_block<T>(x, d, C, HW, i / nblk, i % nblk, part, C, 1);
 }
 
+// The same for channels-first planes of a multiple of 4 positions:
+// workgroups below nbuckets build a schedule bucket each, the rest pool
+// planes with L lanes each (the lanes and order of the plane pooling kernel,
+// so the descriptor has the same bits).
+template <int L>
+__global__ void __launch_bounds__(kPoolThreads)
+k_pool_sched_planes(const uint16_t* __restrict__ x, float* __restrict__ d, int64_t planes, int HW, SchedArgs a) {
+  if ((int)blockIdx.x < a.nbuckets) {
+    __shared__ int cc[2 * kMaxSteps];
+    sched_bucket(a, blockIdx.x, cc, cc + kMaxSteps);
+    return;
+  }
+  const int64_t group = ((int64_t)(blockIdx.x - a.nbuckets) * kPoolThreads + threadIdx.x) / L;
+  const int64_t ngroups = ((int64_t)(gridDim.x - a.nbuckets) * kPoolThreads) / L;
+  pool_planes8<L>(x, d, planes, HW, group, ngroups);
+}
+
 // ---------------------------------------------------------------- the mix
 template <int MB, int NB, int NS, int OCC, bool NH>
 struct Layout {
@@ -868,8 +885,24 @@ hipError_t launch_pool_sched(const Shape& sh, const void* x, float* d, const int
   a.nbuckets = ss.nbuckets;
   a.off = static_cast<int32_t*>(sched);
   a.ent = reinterpret_cast<uint2*>(static_cast<char*>(sched) + ss.off_bytes);
+  if (sh.layout == MOCE_NCHW && !(sh.HW % 8 == 0 && sh.HW / 8 >= 256)) {
+    // channels-first planes pooled 8 bytes at a time, beside the schedule
+    const int64_t planes = sh.B * sh.C;
+    const int L = planes8_lanes(sh.HW);
+    const int64_t per = kPoolThreads / L;
+    const unsigned grid = (unsigned)(ss.nbuckets + std::min<int64_t>((planes + per - 1) / per, 32768));
+    const uint16_t* xb = static_cast<const uint16_t*>(x);
+    const int HW = (int)sh.HW;
+    switch (L) {
+      case 64: hipLaunchKernelGGL(k_pool_sched_planes<64>, dim3(grid), dim3(kPoolThreads), 0, st, xb, d, planes, HW, a); break;
+      case 32: hipLaunchKernelGGL(k_pool_sched_planes<32>, dim3(grid), dim3(kPoolThreads), 0, st, xb, d, planes, HW, a); break;
+      case 16: hipLaunchKernelGGL(k_pool_sched_planes<16>, dim3(grid), dim3(kPoolThreads), 0, st, xb, d, planes, HW, a); break;
+      default: hipLaunchKernelGGL(k_pool_sched_planes<8>, dim3(grid), dim3(kPoolThreads), 0, st, xb, d, planes, HW, a); break;
+    }
+    return hipGetLastError();
+  }
   if (sh.layout == MOCE_NCHW) {
-    // channels-first: the plane pooling kernel, then the schedule alone
+    // long aligned planes: the plane pooling kernel, then the schedule alone
     const hipError_t e = launch_pool(sh, x, d, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((k_pool_sched<uint16_t>), dim3((unsigned)ss.nbuckets), dim3(kPoolThreads), 0, st,

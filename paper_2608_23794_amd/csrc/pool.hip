@@ -78,30 +78,13 @@ k_pool_planes(const T* __restrict__ x, float* __restrict__ d, int64_t planes, in
   }
 }
 
-// bf16 planes of a multiple of 4 positions (so every plane starts 8-byte
-// aligned): L lanes per plane read 8-byte pieces, four per lane in flight,
-// instead of the head, vector and tail loads of k_pool_nchw.
+// bf16 planes of a multiple of 4 positions: L lanes per plane (pool_rows.h)
 template <int L>
 __global__ void __launch_bounds__(256)
 k_pool_nchw8(const uint16_t* __restrict__ x, float* __restrict__ d, int64_t planes, int HW) {
-  const int lane = threadIdx.x % L;
   const int64_t group = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / L;
   const int64_t ngroups = ((int64_t)gridDim.x * blockDim.x) / L;
-  const int nq = HW / 4;
-  for (int64_t pl = group; pl < planes; pl += ngroups) {
-    const uint2* q = reinterpret_cast<const uint2*>(x + pl * HW);
-    float sum = 0.f;
-    for (int v0 = lane; v0 < nq; v0 += 4 * L) {
-      uint2 buf[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) buf[u] = q[min(v0 + u * L, nq - 1)];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (v0 + u * L < nq) sum += (bf16_lo(buf[u].x) + bf16_hi(buf[u].x)) + (bf16_lo(buf[u].y) + bf16_hi(buf[u].y));
-    }
-    sum = wave_sum<L>(sum);
-    if (lane == 0) d[pl] = sum / (float)HW;
-  }
+  pool_planes8<L>(x, d, planes, HW, group, ngroups);
 }
 
 // grid B * nblk (nblk = ceil(vectors per row / 64)), block 256.  EPV channels per lane.
@@ -164,8 +147,7 @@ hipError_t pool_nchw(const Shape& sh, const T* x, float* d, hipStream_t st) {
   }
   if constexpr (sizeof(T) == 2) {
     if (sh.HW % 4 == 0) {
-      const int nq = (int)(sh.HW / 4);
-      const int L8 = nq >= 192 ? 64 : nq >= 96 ? 32 : nq >= 32 ? 16 : 8;
+      const int L8 = planes8_lanes(sh.HW);
       int64_t blocks8 = (planes + 256 / L8 - 1) / (256 / L8);
       if (blocks8 > 65536) blocks8 = 65536;
       const int HW = (int)sh.HW;

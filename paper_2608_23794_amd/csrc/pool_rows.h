@@ -16,6 +16,37 @@ namespace moce {
 constexpr int kPoolThreads = 512;
 constexpr int kPoolGroups = kPoolThreads / 32;  // row groups
 
+// Channels-first bfloat16 planes of H W positions, H W a multiple of 4 (so
+// every plane starts 8-byte aligned): L lanes per plane read 8-byte pieces,
+// four per lane in flight.  Lane group `group` of `ngroups` takes planes
+// group, group + ngroups, ...; a plane's sum depends only on L, so every
+// launch shape with the same L gives the same bits.
+inline int planes8_lanes(int64_t HW) {
+  const int64_t nq = HW / 4;
+  return nq >= 192 ? 64 : nq >= 96 ? 32 : nq >= 32 ? 16 : 8;
+}
+
+template <int L>
+__device__ __forceinline__ void pool_planes8(const uint16_t* __restrict__ x, float* __restrict__ d, int64_t planes,
+                                             int HW, int64_t group, int64_t ngroups) {
+  const int lane = threadIdx.x % L;
+  const int nq = HW / 4;
+  for (int64_t pl = group; pl < planes; pl += ngroups) {
+    const uint2* q = reinterpret_cast<const uint2*>(x + pl * HW);
+    float sum = 0.f;
+    for (int v0 = lane; v0 < nq; v0 += 4 * L) {
+      uint2 buf[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) buf[u] = q[min(v0 + u * L, nq - 1)];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (v0 + u * L < nq) sum += (bf16_lo(buf[u].x) + bf16_hi(buf[u].x)) + (bf16_lo(buf[u].y) + bf16_hi(buf[u].y));
+    }
+    sum = wave_sum<L>(sum);
+    if (lane == 0) d[pl] = sum / (float)HW;
+  }
+}
+
 template <typename T> struct PoolVec;
 template <> struct PoolVec<uint16_t> {
   static constexpr int EPV = 8;

@@ -650,6 +650,8 @@ SCHEDULED_NCHW = [
     (3, 768, 192, 48, 8, 25, dict(signed=True)),  # 200 positions: ragged last tile
     (4, 512, 40, 1, 6, 6, {}),                 # k = 1: exact copies
     (1, 4096, 16, 20, 2, 2, {}),               # C = 4096: 64 steps
+    (2, 320, 48, 12, 20, 20, {}),              # 400 positions: planes pooled by 32 lanes
+    (2, 512, 64, 16, 28, 28, dict(signed=True)),  # 784 positions: planes pooled by 64 lanes
 ]
 
 
