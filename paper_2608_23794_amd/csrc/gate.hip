@@ -318,6 +318,28 @@ k_gate_softplus_lds(const float* __restrict__ d, const int32_t* __restrict__ s, 
   // vectors; a vector that starts past k is read from the row's first
   // entries)
   auto pos = [&](int t, int q) __attribute__((always_inline)) { return 8 * VW * t + VW * h + q; };
+  // descriptor row of image i (clamped into the workgroup's images) into
+  // ring slot i % kGateRing by direct global-to-LDS copies.  Every wave
+  // issues exactly fpw copies per row (64-float pieces v, v + nwaves, ...,
+  // the last piece repeated where the row runs out; a piece past C repeats
+  // entry C - 1 into the padding), so a row is complete once at most
+  // fpw times the number of rows issued after it are outstanding.
+  const int wv_id = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  const int npieces = cpad / 64;
+  const int fpw = (npieces + nwaves - 1) / nwaves;
+  auto fetch = [&](int i) __attribute__((always_inline)) {
+    const float* db = d + (b0 + min(i, nimg - 1)) * C;
+    float* buf = gsm + (i % kGateRing) * cpad;
+    for (int u = 0; u < fpw; ++u) {
+      const int q = min(wv_id + nwaves * u, npieces - 1);
+      __builtin_amdgcn_global_load_lds((const void*)(db + min(q * 64 + lane, C - 1)),
+                                       (__attribute__((address_space(3))) void*)(buf + q * 64), 4, 0, 0);
+    }
+  };
+  // the first rows go out before the expert rows' loads, so that both
+  // arrive in one round trip
+#pragma unroll
+  for (int i = 0; i < kGateRing - 1; ++i) fetch(i);
   int ch[PER];
   float av[PER], wv[PER];
   float wmax = -INFINITY;
@@ -340,26 +362,6 @@ k_gate_softplus_lds(const float* __restrict__ d, const int32_t* __restrict__ s, 
   }
   wmax = row8_max(wmax, lane);
   const float co = c[o];
-  // descriptor row of image i (clamped into the workgroup's images) into
-  // ring slot i % kGateRing by direct global-to-LDS copies.  Every wave
-  // issues exactly fpw copies per row (64-float pieces v, v + nwaves, ...,
-  // the last piece repeated where the row runs out; a piece past C repeats
-  // entry C - 1 into the padding), so a row is complete once at most
-  // fpw times the number of rows issued after it are outstanding.
-  const int wv_id = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
-  const int npieces = cpad / 64;
-  const int fpw = (npieces + nwaves - 1) / nwaves;
-  auto fetch = [&](int i) __attribute__((always_inline)) {
-    const float* db = d + (b0 + min(i, nimg - 1)) * C;
-    float* buf = gsm + (i % kGateRing) * cpad;
-    for (int u = 0; u < fpw; ++u) {
-      const int q = min(wv_id + nwaves * u, npieces - 1);
-      __builtin_amdgcn_global_load_lds((const void*)(db + min(q * 64 + lane, C - 1)),
-                                       (__attribute__((address_space(3))) void*)(buf + q * 64), 4, 0, 0);
-    }
-  };
-#pragma unroll
-  for (int i = 0; i < kGateRing - 1; ++i) fetch(i);
   wait_vm_at_most((kGateRing - 2) * fpw);  // row 0 has landed
   __syncthreads();
   for (int i = 0; i < nimg; ++i) {
