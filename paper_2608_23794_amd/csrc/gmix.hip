@@ -178,15 +178,27 @@ __device__ __forceinline__ void sched_bucket(const SchedArgs& a, int bk, int* cn
       wv = 0.f;
     }
   };
+  // each thread reads kHold entries (all loads in flight) before it counts
+  // or places any of them
+  constexpr int kHold = 8;
+  auto each = [&](auto&& f) __attribute__((always_inline)) {
+    for (int e0 = tid; e0 < total; e0 += kHold * nth) {
+      int o[kHold], c[kHold];
+      float wv[kHold];
+      bool res[kHold];
+#pragma unroll
+      for (int u = 0; u < kHold; ++u) {
+        c[u] = -1;
+        if (e0 + u * nth < total) entry(e0 + u * nth, o[u], c[u], wv[u], res[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < kHold; ++u)
+        if (c[u] >= 0) f(o[u], c[u], wv[u], res[u]);
+    }
+  };
   for (int t = tid; t < a.nsteps; t += nth) cnt[t] = 0;
   __syncthreads();
-  for (int e = tid; e < total; e += nth) {
-    int o, c;
-    float wv;
-    bool res;
-    entry(e, o, c, wv, res);
-    atomicAdd(&cnt[c >> 6], 1);
-  }
+  each([&](int, int c, float, bool) __attribute__((always_inline)) { atomicAdd(&cnt[c >> 6], 1); });
   __syncthreads();
   // exclusive scan of the counts (nsteps <= 64: one wave)
   int32_t* ob = a.off + (int64_t)bk * (a.nsteps + 1);
@@ -207,16 +219,12 @@ __device__ __forceinline__ void sched_bucket(const SchedArgs& a, int bk, int* cn
   __syncthreads();
   const int ne = a.ng * kGroup;
   uint2* eb = a.ent + (int64_t)bk * a.cap;
-  for (int e = tid; e < total; e += nth) {
-    int o, c;
-    float wv;
-    bool res;
-    entry(e, o, c, wv, res);
+  each([&](int o, int c, float wv, bool res) __attribute__((always_inline)) {
     const int pos = atomicAdd(&cur[c >> 6], 1);
     const int ow = o - q * ne;  // the expert's slot within the range
     const uint32_t packed = (uint32_t)b_off(ow, c & 63) | ((uint32_t)ow << kSlotShift) | (res ? kResidualFlag : 0u);
     eb[pos] = make_uint2(packed, __float_as_uint(wv));
-  }
+  });
 }
 
 // Pooling and the schedule in one launch: workgroups below nbuckets build a
