@@ -68,8 +68,8 @@ def test_traffic_record_is_the_calibrated_counters():
         return
     assert t == int(rec["traffic_bytes"])
     # the record is the calibrated sum of the two counters
-    fetch = int(rec["fetch_kib_per_dispatch"]) * 1024 * float(rec["fetch_scale"])
-    write = int(rec["write_kib_per_dispatch"]) * 1024 * float(rec["write_scale"])
+    fetch = float(rec["fetch_kib_per_dispatch"]) * 1024 * float(rec["fetch_scale"])
+    write = float(rec["write_kib_per_dispatch"]) * 1024 * float(rec["write_scale"])
     assert t == pytest.approx(fetch + write, rel=1e-6)
     assert bench.measured_traffic("another_kernel") is None
 
