@@ -681,16 +681,18 @@ __device__ __forceinline__ void consumer_run(const Run& r, const int32_t* __rest
   }
 }
 
-// Loader waves: tile t0 is requested first, before the prologue's barrier
-// (every workgroup starting at once would otherwise queue the consumers'
-// small coefficient reads behind megabytes of tiles), then up to three
-// tiles stay in flight.
+// Loader waves: the first tiles are requested after the prologue's barrier,
+// once the consumers' index and descriptor reads are back (with every
+// workgroup starting at once, tiles requested earlier queue those small
+// reads behind megabytes of x; the consumers' gate and first build still
+// take longer than tile t0's round trip), then up to three tiles stay in
+// flight.
 template <int NR>
 __device__ __forceinline__ void loader_run(const Run& r, const uint16_t* __restrict__ x) {
   const MixArgs& p = r.p;
   const int lt = r.tid - kCThreads;
-  copy_tile<NR>(p, x, r.t0, r.ring, lt);
   lds_barrier();
+  copy_tile<NR>(p, x, r.t0, r.ring, lt);
   if (r.t0 + 1 < r.t1) copy_tile<NR>(p, x, r.t0 + 1, r.ring + r.tileb, lt);
   if (r.t0 + 2 < r.t1) copy_tile<NR>(p, x, r.t0 + 2, r.ring + 2 * r.tileb, lt);
   for (int n = r.t0; n < r.t1; ++n) {
