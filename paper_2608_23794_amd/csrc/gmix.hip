@@ -592,11 +592,11 @@ __device__ __forceinline__ void loader(const GmArgs& p, unsigned char* smem, int
       __builtin_amdgcn_global_load_lds((const void*)src, (GMIX_LDS void*)(dst + u * 1024), 16, 0, kCachePolicyNT);
     }
   };
-  // prologue: chunks 0 .. XR - 2 in flight, chunk 0 complete
-  const int first = min(XR - 1, nchunks);
-  for (int n = 0; n < first; ++n) copy(n);
-  wait_chunks<L::ROUNDS, XR>(first - 1);
+  // prologue: chunk 0 complete; chunks 1 .. XR - 2 go out after the barrier
+  copy(0);
+  wait_chunks<L::ROUNDS, XR>(0);
   lds_barrier();  // prologue
+  for (int n = 1; n < min(XR - 1, nchunks); ++n) copy(n);
   for (int ks = 0; ks < p.nsteps; ++ks) {
     // chunk ks + XR - 1 into the slot chunk ks - 1 left (free since the
     // barrier that ended step ks - 1); chunk ks + 1 complete before this
